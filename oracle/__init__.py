@@ -1,0 +1,257 @@
+"""CPU oracle for Poseidon's per-layer synchronisation compute (arXiv 1706.03292).
+
+TEST INFRASTRUCTURE.  Only the test suite, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  It shares no code
+with the HIP library it checks and never imports it.
+
+Thin ctypes wrapper over ``poseidon_oracle.c`` (plain C, fp64 sums).  Arrays are
+numpy; inputs are fp32 like the layers they stand for, outputs are fresh arrays
+(the caller's arrays are never modified).
+
+Functions and the passages they follow:
+
+* ``sf_delta`` / ``sf_apply`` / ``sf_apply_points`` -- sufficient-factor
+  reconstruction of a fully-connected layer's gradient, the sum over the P*B
+  rank-1 factor pairs (Sec. 2.1 "Sufficient Factor Broadcasting", Eq. 2),
+  applied by one SGD step (Eq. 1).
+* ``ps_apply`` / ``ps_apply_points`` -- parameter-server aggregation of the P
+  workers' dense gradients and its application (Sec. 2.1 "Parameter Server",
+  Sec. 4.1 "KV Store", "Managing Consistency"), with heavy-ball momentum.
+* ``hybcomm_traffic`` / ``hybcomm_choose`` / ``best_scheme`` -- the hybrid
+  communication decision by exhaustive message counting (Sec. 3.2, Table 1,
+  Alg. 1).
+* ``sync_iteration`` -- one node's synchronisation of every layer of a network
+  for one iteration, layer by layer in backpropagation order (Sec. 3, Alg. 2).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+PS = 0
+SFB = 1
+ADAM = 2
+ROLE_WORKER = 1
+ROLE_SERVER = 2
+
+_f32p = np.ctypeslib.ndpointer(dtype=np.float32, flags="C_CONTIGUOUS")
+_f64p = np.ctypeslib.ndpointer(dtype=np.float64, flags="C_CONTIGUOUS")
+_i64p = np.ctypeslib.ndpointer(dtype=np.int64, flags="C_CONTIGUOUS")
+_i32p = np.ctypeslib.ndpointer(dtype=np.int32, flags="C_CONTIGUOUS")
+_i64 = ctypes.c_int64
+_i32 = ctypes.c_int32
+_f32 = ctypes.c_float
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        from . import build as _build
+        _build.build()
+    lib = ctypes.CDLL(_LIB_PATH)
+    lib.oracle_sf_delta.argtypes = [_f64p, _f32p, _f32p, _i64, _i64, _i64]
+    lib.oracle_sf_delta.restype = None
+    lib.oracle_sf_apply_rows.argtypes = [_f32p, _f32p, _f32p, _i64, _i64, _i64,
+                                         _f32, _i64, _i64]
+    lib.oracle_sf_apply_rows.restype = None
+    lib.oracle_sf_apply_points.argtypes = [_f32p, _f32p, _f32p, _i64, _i64, _i64,
+                                           _f32, _i64p, _i64p, _i64, _f32p]
+    lib.oracle_sf_apply_points.restype = None
+    lib.oracle_ps_apply_range.argtypes = [_f32p, _f32p, _i32, _i64, _f32, _f32,
+                                          ctypes.c_void_p, _i64, _i64]
+    lib.oracle_ps_apply_range.restype = ctypes.c_int
+    lib.oracle_ps_apply_points.argtypes = [_f32p, _f32p, _i32, _i64, _f32, _f32,
+                                           ctypes.c_void_p, _i64p, _i64, _f32p,
+                                           ctypes.c_void_p]
+    lib.oracle_ps_apply_points.restype = ctypes.c_int
+    lib.oracle_hybcomm_traffic.argtypes = [_i64, _i64, _i64, _i32p, _i32, _i32, _i64p]
+    lib.oracle_hybcomm_traffic.restype = ctypes.c_int
+    lib.oracle_hybcomm_choose.argtypes = [_i64, _i64, _i64, _i64]
+    lib.oracle_hybcomm_choose.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def _f32c(a) -> np.ndarray:
+    a = np.ascontiguousarray(a)
+    if a.dtype != np.float32:
+        raise TypeError(f"oracle expects float32 arrays, got {a.dtype}")
+    return a
+
+
+# --------------------------------------------------------------------------
+# Sufficient-factor reconstruction (Sec. 2.1; Eq. 1, Eq. 2)
+# --------------------------------------------------------------------------
+
+def _sf_dims(U, V):
+    if U.ndim != 2 or V.ndim != 2 or U.shape[0] != V.shape[0]:
+        raise ValueError("U must be K x M and V must be K x N")
+    K, M = U.shape
+    N = V.shape[1]
+    return M, N, K
+
+
+def sf_delta(U, V) -> np.ndarray:
+    """dW = sum_k u_k v_k^T in fp64, k in increasing order (M x N)."""
+    U, V = _f32c(U), _f32c(V)
+    M, N, K = _sf_dims(U, V)
+    dW = np.empty((M, N), dtype=np.float64)
+    _load().oracle_sf_delta(dW, U, V, M, N, K)
+    return dW
+
+
+def sf_apply(W, U, V, lr: float, rows: tuple[int, int] | None = None) -> np.ndarray:
+    """Return W - lr * U^T V (fp64 sum, rounded once to fp32).
+
+    ``rows=(m0, m1)`` updates only those rows (the rest are copied unchanged)."""
+    W, U, V = _f32c(W), _f32c(U), _f32c(V)
+    M, N, K = _sf_dims(U, V)
+    if W.shape != (M, N):
+        raise ValueError(f"W must be {M} x {N}")
+    out = W.copy()
+    m0, m1 = rows if rows is not None else (0, M)
+    _load().oracle_sf_apply_rows(out, U, V, M, N, K, np.float32(lr), m0, m1)
+    return out
+
+
+def sf_apply_points(W, U, V, lr: float, rows, cols) -> np.ndarray:
+    """Updated values of W at the points (rows[i], cols[i])."""
+    W, U, V = _f32c(W), _f32c(U), _f32c(V)
+    M, N, K = _sf_dims(U, V)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    if rows.shape != cols.shape:
+        raise ValueError("rows and cols must have the same shape")
+    if rows.size and (rows.min() < 0 or rows.max() >= M or cols.min() < 0 or cols.max() >= N):
+        raise IndexError("point outside W")
+    out = np.empty(rows.shape, dtype=np.float32)
+    _load().oracle_sf_apply_points(W.reshape(-1) if W.size else W, U, V, M, N, K,
+                                   np.float32(lr), rows, cols, rows.size, out)
+    return out
+
+
+# --------------------------------------------------------------------------
+# Parameter-server aggregation + apply (Sec. 2.1, Sec. 4.1)
+# --------------------------------------------------------------------------
+
+def _ps_args(W, shards, buf, mu):
+    W, shards = _f32c(W).reshape(-1), _f32c(shards)
+    if shards.ndim != 2:
+        raise ValueError("shards must be P x n")
+    P, n = shards.shape
+    if W.size != n:
+        raise ValueError("W must have n elements")
+    if buf is None and mu != 0.0:
+        raise ValueError("momentum needs a buffer")
+    if buf is not None:
+        buf = _f32c(buf).reshape(-1)
+        if buf.size != n:
+            raise ValueError("buf must have n elements")
+    return W, shards, buf, P, n
+
+
+def ps_apply(W, shards, lr: float, mu: float = 0.0, buf=None,
+             elems: tuple[int, int] | None = None):
+    """Return (W', buf') after buf <- mu*buf + sum_p G_p; W <- W - lr*buf.
+
+    Without ``buf`` (mu must be 0) W' = W - lr * sum_p G_p and buf' is None.
+    The per-element sum is taken in ascending-value order in fp64, so the
+    result is exactly the same for any order of the P shards."""
+    W, shards, buf, P, n = _ps_args(W, shards, buf, mu)
+    w_out = W.copy()
+    b_out = buf.copy() if buf is not None else None
+    i0, i1 = elems if elems is not None else (0, n)
+    rc = _load().oracle_ps_apply_range(
+        w_out, shards, P, n, np.float32(lr), np.float32(mu),
+        b_out.ctypes.data if b_out is not None else None, i0, i1)
+    if rc != 0:
+        raise RuntimeError("oracle_ps_apply_range failed")
+    return w_out, b_out
+
+
+def ps_apply_points(W, shards, lr: float, mu: float, buf, idx):
+    """(W', buf') at element indices idx; buf' is None without a buffer."""
+    W, shards, buf, P, n = _ps_args(W, shards, buf, mu)
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    if idx.size and (idx.min() < 0 or idx.max() >= n):
+        raise IndexError("index outside W")
+    w_out = np.empty(idx.shape, dtype=np.float32)
+    b_out = np.empty(idx.shape, dtype=np.float32) if buf is not None else None
+    rc = _load().oracle_ps_apply_points(
+        W, shards, P, n, np.float32(lr), np.float32(mu),
+        buf.ctypes.data if buf is not None else None, idx, idx.size, w_out,
+        b_out.ctypes.data if b_out is not None else None)
+    if rc != 0:
+        raise RuntimeError("oracle_ps_apply_points failed")
+    return w_out, b_out
+
+
+# --------------------------------------------------------------------------
+# Hybrid communication (Sec. 3.2, Table 1, Alg. 1)
+# --------------------------------------------------------------------------
+
+def hybcomm_traffic(M: int, N: int, B: int, roles, scheme: int) -> np.ndarray:
+    """Per-node network traffic of one layer sync, in units of 1/P2 values.
+
+    roles[j] is a bit set (ROLE_WORKER, ROLE_SERVER) for node j; scheme is
+    PS, SFB or ADAM.  Every message is enumerated and counted at both ends."""
+    roles = np.ascontiguousarray(roles, dtype=np.int32)
+    out = np.empty(roles.size, dtype=np.int64)
+    rc = _load().oracle_hybcomm_traffic(M, N, B, roles, roles.size, scheme, out)
+    if rc != 0:
+        raise ValueError("invalid cluster or overflow")
+    return out
+
+
+def hybcomm_choose(M: int, N: int, B: int, P: int) -> int:
+    """SFB (1) or PS (0) for an M x N FC layer, batch B, P worker+server nodes."""
+    rc = _load().oracle_hybcomm_choose(M, N, B, P)
+    if rc < 0:
+        raise ValueError("invalid arguments")
+    return rc
+
+
+def best_scheme(is_fc: bool, M: int, N: int, B: int, P: int) -> int:
+    """Alg. 1: only fully-connected layers can use SFB; all others use PS."""
+    return hybcomm_choose(M, N, B, P) if is_fc else PS
+
+
+# --------------------------------------------------------------------------
+# One iteration's synchronisation of a whole network (Sec. 3, Alg. 2)
+# --------------------------------------------------------------------------
+
+def sync_iteration(layers, B: int, P: int, lr: float, mu: float):
+    """Apply one iteration's synchronisation to every layer.
+
+    ``layers`` is a list of dicts in forward order with keys
+    ``fc`` (bool), ``W`` (array), ``U``/``V`` (K x M / K x N, for FC layers),
+    ``shards`` (P x n) and ``buf`` (n, or None).  Layers are processed from the
+    last to the first (backpropagation order); each FC layer goes through
+    ``best_scheme``.  SFB layers take a plain SGD step; PS layers take the
+    momentum step.  Returns a list (forward order) of dicts with ``scheme``,
+    ``W`` and ``buf``."""
+    out = [None] * len(layers)
+    for l in range(len(layers) - 1, -1, -1):
+        L = layers[l]
+        W = L["W"]
+        if L["fc"]:
+            M, N = W.shape
+            scheme = best_scheme(True, M, N, B, P)
+        else:
+            scheme = PS
+        if scheme == SFB:
+            out[l] = {"scheme": SFB, "W": sf_apply(W, L["U"], L["V"], lr),
+                      "buf": None if L.get("buf") is None else np.array(L["buf"], copy=True)}
+        else:
+            w2, b2 = ps_apply(W.reshape(-1), L["shards"], lr, mu if L.get("buf") is not None else 0.0,
+                              L.get("buf"))
+            out[l] = {"scheme": PS, "W": w2.reshape(W.shape), "buf": b2}
+    return out
