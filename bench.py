@@ -1,0 +1,231 @@
+#!/usr/bin/env python3
+"""Benchmark: one node's per-iteration gradient synchronisation on one MI355X.
+
+A "step" is one full VGG19-22K iteration sync (P = 16 workers, per-worker
+batch B = 32): the three FC weights through sufficient-factor reconstruction
++ SGD (K = 512), the 16 conv kernels and 19 bias vectors through P-shard
+aggregation + momentum SGD, each FC layer's scheme chosen by Alg. 1, all
+issued in backpropagation order on a pool of HIP streams.  Inputs are seeded
+synthetic tensors already resident in HBM.
+
+Prints ONE JSON line: per-iteration sync ms (value), the SF-reconstruction
+kernel's TFLOP/s and the PS kernel's GB/s against MI355X peaks, and the CPU
+oracle's time on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--streams S] [--cpu-baseline off]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "per-iteration sync ms; SFB TFLOP/s + PS apply GB/s vs roofline at P=16"
+PEAK_FP32_MFMA_TFLOPS = 157.3     # MI355X dense fp32 matrix peak
+PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
+
+
+def _parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=5, help="workload (5 = VGG19-22K full iteration)")
+    ap.add_argument("--streams", type=int, default=4)
+    ap.add_argument("--kernel-steps", type=int, default=None,
+                    help="iterations timed per tensor for the roofline (default: --steps)")
+    ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
+    ap.add_argument("--cpu-fraction", type=float, default=1.0,
+                    help="fraction of each tensor the CPU oracle runs on")
+    return ap.parse_args()
+
+
+def _sf_flops(spec, K):
+    M, N = spec.shape
+    return 2.0 * M * N * K
+
+
+def _sf_bytes(spec, K):
+    M, N = spec.shape
+    return 4.0 * (2 * M * N + K * (M + N))
+
+
+def _ps_bytes(spec, P, momentum: bool):
+    return float(spec.numel) * (4 * P + (16 if momentum else 8))
+
+
+def _cpu_baseline(wl, host, fraction):
+    """The oracle (as is) on the first `fraction` of every tensor of the
+    workload, scaled to one whole iteration."""
+    import oracle
+    t_sfb = t_ps = 0.0
+    sfb_frac_work = ps_frac_work = 0.0
+    sfb_total = ps_total = 0.0
+    for h in host:
+        spec = h["spec"]
+        if spec.kind == "fc":
+            M, N = spec.shape
+            rows = max(1, int(round(M * fraction)))
+            t0 = time.perf_counter()
+            oracle.sf_apply(h["W"].numpy(), h["U"].numpy(), h["V"].numpy(), wl.lr, rows=(0, rows))
+            t_sfb += time.perf_counter() - t0
+            sfb_frac_work += rows * N
+            sfb_total += M * N
+        else:
+            n = spec.numel
+            cnt = max(1, int(round(n * fraction)))
+            t0 = time.perf_counter()
+            oracle.ps_apply(h["W"].numpy().reshape(-1), h["shards"].numpy(), wl.lr, wl.momentum,
+                            h["buf"].numpy(), elems=(0, cnt))
+            t_ps += time.perf_counter() - t0
+            ps_frac_work += cnt
+            ps_total += n
+    est_s = t_sfb * sfb_total / max(sfb_frac_work, 1) + t_ps * ps_total / max(ps_frac_work, 1)
+    return {
+        "value": est_s * 1e3,
+        "unit": "ms",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"first {fraction:.4g} of the rows of each SFB layer and of the elements of each "
+                   f"PS tensor of the same iteration ({t_sfb + t_ps:.1f} s measured: SFB {t_sfb:.2f} s, "
+                   f"PS {t_ps:.2f} s), scaled by work to one whole iteration"),
+    }
+
+
+def main():
+    args = _parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        msg = ("bench.py measures one GPU: this build has no multi-GPU path "
+               f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}). Run with --gpus 1.")
+        print(msg, file=sys.stderr, flush=True)
+        print(json.dumps({"metric": METRIC, "error": msg, "n_gpus": args.gpus}), flush=True)
+        sys.exit(2)
+
+    import torch
+
+    from paper_1706_03292_amd import api
+    from paper_1706_03292_amd import inputs as I
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a HIP device", file=sys.stderr)
+        sys.exit(1)
+    d = torch.device("cuda", 0)
+    torch.cuda.set_device(d)
+    wl = I.workload(args.config)
+    t0 = time.perf_counter()
+    host = I.make_tensors(wl)
+    devt = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in host]
+    torch.cuda.synchronize()
+    print(f"[bench] inputs for config {wl.config} ({wl.name}) ready in {time.perf_counter() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+
+    pool = api.StreamPool(args.streams, device=d)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    stream = torch.cuda.current_stream(d)
+
+    # Warm-up, then exactly K timed steps bracketed by synchronisations.
+    for _ in range(args.warmup):
+        schemes = it(stream)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_start = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        schemes = it(stream)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_start) * 1e3 / args.steps
+    event_ms = ev0.elapsed_time(ev1) / args.steps
+    print(f"[bench] timed {args.steps} steps: {wall_ms:.3f} ms/step (events {event_ms:.3f})",
+          file=sys.stderr, flush=True)
+
+    # Per-kernel durations for the roofline: the same iteration, same streams,
+    # with the library's per-tensor timing events on the streams the kernels run on.
+    ksteps = args.kernel_steps or args.steps
+    pool.set_timing(True)
+    sums = [0.0] * len(devt)
+    for _ in range(ksteps):
+        it(stream)
+        for i, ms in enumerate(pool.tensor_times(len(devt))):
+            sums[i] += ms
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    avg = [s / ksteps for s in sums]
+
+    sfb_flops = sfb_ms = sfb_bytes = 0.0
+    ps_bytes = ps_ms = 0.0
+    layers = []
+    big_ps = None
+    for h, sch, ms in zip(host, schemes, avg):
+        spec = h["spec"]
+        if sch == api.SFB:
+            f = _sf_flops(spec, wl.K)
+            sfb_flops += f
+            sfb_bytes += _sf_bytes(spec, wl.K)
+            sfb_ms += ms
+            layers.append({"tensor": spec.name, "scheme": "SFB", "ms": round(ms, 4),
+                           "tflops": round(f / ms / 1e9, 2)})
+        else:
+            b = _ps_bytes(spec, wl.P, "buf" in h)
+            ps_bytes += b
+            ps_ms += ms
+            if big_ps is None or spec.numel > big_ps[0]:
+                big_ps = (spec.numel, spec.name, b, ms)
+    sfb_tflops = sfb_flops / sfb_ms / 1e9 if sfb_ms else None
+    ps_gbs = ps_bytes / ps_ms / 1e6 if ps_ms else None
+    big_gbs = big_ps[2] / big_ps[3] / 1e6 if big_ps else None
+
+    result = {
+        "metric": METRIC,
+        "value": round(wall_ms, 4),
+        "unit": "ms",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall_ms, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: {sum(s.numel for s in wl.specs)} params, "
+                               f"{len(wl.specs)} tensors, K={wl.K}, lr={wl.lr}, momentum={wl.momentum}",
+                   "P": wl.P, "B": wl.B, "streams": args.streams},
+        "roofline": {"bound": "mfma", "kernel": "sf_apply (fp32 MFMA)",
+                     "achieved": round(sfb_tflops, 2) if sfb_tflops else None,
+                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(sfb_tflops / PEAK_FP32_MFMA_TFLOPS, 4) if sfb_tflops else None,
+                     "traffic": None,
+                     "work": f"2*M*N*K flops over the {sum(1 for s in schemes if s == api.SFB)} SFB "
+                             f"launches of one step ({sfb_flops / 1e9:.1f} GFLOP) / their summed "
+                             f"average durations ({sfb_ms:.4f} ms)"},
+        "roofline_ps": {"bound": "hbm", "kernel": "ps_apply",
+                        "achieved": round(ps_gbs, 1) if ps_gbs else None,
+                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                        "frac": round(ps_gbs / PEAK_HBM_GBS, 4) if ps_gbs else None,
+                        "traffic": None,
+                        "largest_tensor": {"tensor": big_ps[1], "gbs": round(big_gbs, 1),
+                                           "ms": round(big_ps[3], 4)} if big_ps else None,
+                        "work": f"(4P+16) bytes per element over all PS launches of one step "
+                                f"({ps_bytes / 1e9:.3f} GB) / summed average durations ({ps_ms:.4f} ms)"},
+        "event_ms_per_step": round(event_ms, 4),
+        "sfb_tflops": round(sfb_tflops, 2) if sfb_tflops else None,
+        "ps_gbs": round(ps_gbs, 1) if ps_gbs else None,
+        "layers_sfb": layers,
+    }
+    if args.cpu_baseline == "on":
+        print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
+        result["cpu_baseline"] = _cpu_baseline(wl, host, args.cpu_fraction)
+    pool.close()
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

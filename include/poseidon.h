@@ -1,0 +1,206 @@
+/*
+ * poseidon.h -- C ABI of libposeidon.so: one node's per-layer gradient
+ * synchronisation compute from Poseidon (Zhang et al., "Poseidon: An Efficient
+ * Communication Architecture for Distributed Deep Learning on GPU Clusters",
+ * arXiv 1706.03292), for AMD Instinct MI355X (gfx950).
+ *
+ * The paper synchronises each layer either through a parameter server (dense
+ * gradients pushed to server shards, summed and applied there) or by
+ * sufficient-factor broadcasting (the rank-1 factors u, v of each sample's
+ * fully-connected gradient are broadcast and every node rebuilds the
+ * gradient), choosing per layer by the bytes each scheme would move (hybrid
+ * communication).  This library performs the node-local arithmetic of both
+ * schemes on payloads that are already in device memory, and the choice.
+ *
+ * General conventions
+ *  - All array arguments are device pointers to fp32 data owned by the caller.
+ *    The library keeps no pointer past a call and allocates no device memory.
+ *  - Work is enqueued asynchronously on `stream` (0 = the null stream).
+ *    Argument errors are detected and reported synchronously, before anything
+ *    is enqueued; a fault inside a kernel surfaces at the next synchronisation
+ *    of the stream, as for any HIP kernel.
+ *  - Empty work (a zero dimension) is a successful no-op.
+ *  - Any 4-byte alignment is accepted; 16-byte aligned arrays whose row length
+ *    is a multiple of 4 take the vectorised fast path.
+ *  - Outputs must not overlap inputs (checked: overlapping ranges are an
+ *    argument error).
+ *  - The functions are thread-safe and keep no mutable global state, except the
+ *    stream pool object, which belongs to its creator and must not be used by
+ *    two threads at once.
+ *  - Results are deterministic: the same inputs give bit-identical outputs.
+ */
+#ifndef POSEIDON_H
+#define POSEIDON_H
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define POSEIDON_OK               0
+#define POSEIDON_ERR_INVALID_ARG (-1)  /* bad size, NULL with nonzero size, P < 1, overlap */
+#define POSEIDON_ERR_HIP         (-2)  /* a HIP runtime call or kernel launch failed */
+#define POSEIDON_ERR_PAYLOAD     (-3)  /* the chosen scheme's payload was not supplied */
+
+/* Synchronisation schemes (Alg. 1 returns one of these). */
+#define POSEIDON_PS   0
+#define POSEIDON_SFB  1
+
+/* Tensor kinds: only fully-connected weights can be synchronised by SFB;
+ * convolution kernels, biases and normalisation vectors always use the
+ * parameter server (Sec. 3.2, Alg. 1). */
+#define POSEIDON_KIND_FC     0
+#define POSEIDON_KIND_OTHER  1
+
+/*
+ * Sufficient-factor reconstruction fused with the SGD step (Sec. 2.1
+ * "Sufficient Factor Broadcasting"; Eq. 2; Eq. 1), the work of a syncer's
+ * Move(CPU2GPU) for an SFB layer (Sec. 4.1, Table 2):
+ *
+ *     W[m][n] <- W[m][n] - lr * sum_{k<K} U[k][m] * V[k][n]
+ *
+ * W : M x N row-major, updated in place (M = fan-out, the length of u;
+ *     N = fan-in, the length of v).
+ * U : K x M row-major; row k is the factor u_k.  V : K x N row-major; row k is
+ *     v_k.  K = P * B is the number of factor pairs gathered from the P
+ *     workers of per-worker batch B, this node's own included; the rows of
+ *     worker p are contiguous.
+ * The sum is accumulated in fp32 on the matrix cores and W is read and written
+ * exactly once.  lr is applied as given (no 1/(P*B) scaling).
+ * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (negative size, NULL pointer
+ * with nonzero size, W overlapping U or V) or POSEIDON_ERR_HIP.
+ */
+int poseidon_sf_apply(float* W, const float* U, const float* V,
+                      int64_t M, int64_t N, int64_t K, float lr,
+                      hipStream_t stream);
+
+/*
+ * Parameter-server aggregation and apply: the KV store's Receive of all P
+ * workers' updates followed by their application (Sec. 2.1 "Parameter
+ * Server"; Sec. 4.1 "KV Store", "Managing Consistency"), with heavy-ball
+ * momentum:
+ *
+ *     s_i   = sum_{p<P} shards[p*n + i]          (p in increasing order)
+ *     buf_i <- momentum * buf_i + s_i
+ *     W_i   <- W_i - lr * buf_i
+ *
+ * shards : P x n, shard p at offset p*n.  W, buf : n values, updated in place.
+ * buf == NULL is allowed only with momentum == 0 and gives W_i -= lr * s_i.
+ * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (P < 1, n < 0, NULL pointer
+ * with n > 0, momentum != 0 without buf, overlapping arrays) or
+ * POSEIDON_ERR_HIP.
+ */
+int poseidon_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
+                      float lr, float momentum, float* buf,
+                      hipStream_t stream);
+
+/*
+ * Coordinator.BestScheme for a fully-connected M x N layer (Alg. 1; Table 1)
+ * on a cluster of P nodes that are each both worker and server (P1 = P2 = P),
+ * per-worker batch B:
+ *
+ *     SFB  iff  2 B (P-1) (M+N)  <=  2 M N (P1 + P2 - 2) / P2
+ *
+ * evaluated exactly in integers (both sides multiplied by P2).  A tie goes to
+ * SFB; P = 1 is a tie (nothing is sent either way).  Host-only; no device work.
+ * Returns POSEIDON_SFB, POSEIDON_PS, or POSEIDON_ERR_INVALID_ARG (negative
+ * M, N or B; P < 1; any argument above 2^31 - 1).
+ */
+int poseidon_hybcomm_choose(int64_t M, int64_t N, int64_t B, int64_t P);
+
+/*
+ * Table 1's per-node traffic of one synchronisation of an M x N FC layer, in
+ * values (not bytes), multiplied by P2 so that it stays an integer:
+ *   *ps_x_p2  = 2 M N (P1 + P2 - 2)   (a node that is both server and worker)
+ *   *sfb_x_p2 = 2 B (P1 - 1) (M + N) P2
+ * Host-only.  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG (negative
+ * sizes, P1 or P2 < 1, arguments above 2^31 - 1, NULL outputs, or a result
+ * that does not fit in int64).
+ */
+int poseidon_hybcomm_cost(int64_t M, int64_t N, int64_t B, int64_t P1, int64_t P2,
+                          int64_t* ps_x_p2, int64_t* sfb_x_p2);
+
+/*
+ * One parameter tensor of a network, as handed to poseidon_sync_iteration.
+ * W has M*N values (kind FC: M x N row-major; other kinds: any shape
+ * flattened, M*N = n).  U/V are the SF payload (K x M and K x N, K = P*B) and
+ * shards the dense payload (P x M*N); a tensor carries the payload of the
+ * scheme it will use and may set the other to NULL.  buf is the momentum
+ * buffer (M*N values) used by the PS apply, or NULL for plain SGD.
+ */
+typedef struct poseidon_tensor {
+    int32_t      kind;     /* POSEIDON_KIND_FC or POSEIDON_KIND_OTHER */
+    int32_t      reserved; /* must be 0 */
+    float*       W;
+    int64_t      M;
+    int64_t      N;
+    const float* U;
+    const float* V;
+    const float* shards;
+    float*       buf;
+} poseidon_tensor;
+
+/* The client library's GPU stream pool (Sec. 4.1 "Client Library"): a fixed
+ * set of non-blocking, default-priority HIP streams on the current device plus
+ * the events that fork them from and join them back to a caller stream. */
+typedef struct poseidon_stream_pool poseidon_stream_pool;
+
+/* Create a pool of num_streams (1..64) streams on the current device.
+ * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG or POSEIDON_ERR_HIP. */
+int poseidon_pool_create(int32_t num_streams, poseidon_stream_pool** pool);
+
+/* Destroy a pool (waits for its streams to drain).  NULL is a no-op. */
+int poseidon_pool_destroy(poseidon_stream_pool* pool);
+
+/*
+ * One iteration's synchronisation of a whole network (Sec. 3 "wait-free
+ * backpropagation"; Alg. 2 TRAIN/sync): tensors[] is given in forward order
+ * and issued from the last to the first (backpropagation order).  For each
+ * tensor the scheme is Alg. 1's (FC: poseidon_hybcomm_choose(M, N, B, P);
+ * other kinds: PS) and its update is enqueued on the next pool stream in turn:
+ * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
+ * poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf) (momentum is used
+ * only when buf != NULL).  Every pool stream first waits for the work already
+ * enqueued on `stream`, and `stream` then waits for every tensor's update, so
+ * the call behaves like one asynchronous operation on `stream` (the
+ * bulk-synchronous barrier of Sec. 4.1 "Managing Consistency").
+ * schemes (optional, count entries) receives each tensor's scheme.
+ * All arguments are validated before anything is enqueued.  Returns
+ * POSEIDON_OK, POSEIDON_ERR_INVALID_ARG, POSEIDON_ERR_PAYLOAD (the chosen
+ * scheme's payload is NULL) or POSEIDON_ERR_HIP.
+ */
+int poseidon_sync_iteration(poseidon_stream_pool* pool,
+                            const poseidon_tensor* tensors, int32_t count,
+                            int64_t B, int32_t P, float lr, float momentum,
+                            hipStream_t stream, int32_t* schemes);
+
+/*
+ * Per-tensor timing (the per-layer synchronisation times the paper's
+ * evaluation reasons about, Sec. 5).  While enabled (default: off), every
+ * update that poseidon_sync_iteration enqueues is bracketed by two timing
+ * events on the stream it runs on.  Returns POSEIDON_OK,
+ * POSEIDON_ERR_INVALID_ARG or POSEIDON_ERR_HIP.
+ */
+int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
+
+/*
+ * Elapsed milliseconds of each tensor's update in the last iteration run with
+ * timing enabled: ms[t] for tensors[t] of that call (count entries); -1 for a
+ * tensor with no work.  Blocks until that iteration's updates have finished.
+ * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (no timed iteration yet, count
+ * different from that iteration's) or POSEIDON_ERR_HIP.
+ */
+int poseidon_pool_tensor_times(poseidon_stream_pool* pool, float* ms, int32_t count);
+
+/* Library version, for the binding's load check: returns POSEIDON_ABI_VERSION. */
+#define POSEIDON_ABI_VERSION 1
+int poseidon_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* POSEIDON_H */

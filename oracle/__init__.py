@@ -76,6 +76,8 @@ def _load():
     lib.oracle_hybcomm_traffic.restype = ctypes.c_int
     lib.oracle_hybcomm_choose.argtypes = [_i64, _i64, _i64, _i64]
     lib.oracle_hybcomm_choose.restype = ctypes.c_int
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -255,3 +257,8 @@ def sync_iteration(layers, B: int, P: int, lr: float, mu: float):
                               L.get("buf"))
             out[l] = {"scheme": PS, "W": w2.reshape(W.shape), "buf": b2}
     return out
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return int(_load().oracle_num_threads())

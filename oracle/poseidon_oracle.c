@@ -28,6 +28,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <omp.h>
+
 /* ------------------------------------------------------------------------ */
 /* Sufficient-factor reconstruction (Sec. 2.1, "Sufficient Factor            */
 /* Broadcasting"; Fig. 2b): the gradient of a fully-connected layer over one */
@@ -340,4 +342,10 @@ int oracle_hybcomm_choose(int64_t M, int64_t N, int64_t B, int64_t P)
     free(ps);
     free(sfb);
     return rc;
+}
+
+/* Threads the parallel loops above use (for reporting the CPU baseline). */
+int oracle_num_threads(void)
+{
+    return omp_get_max_threads();
 }

@@ -1,0 +1,65 @@
+"""Loader for libposeidon.so (the HIP library behind include/poseidon.h).
+
+There is no fallback: if the library is not built the first call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libposeidon.so")
+ABI_VERSION = 1
+
+OK = 0
+ERR_INVALID_ARG = -1
+ERR_HIP = -2
+ERR_PAYLOAD = -3
+PS = 0
+SFB = 1
+KIND_FC = 0
+KIND_OTHER = 1
+
+EXPORTS = ("poseidon_sf_apply", "poseidon_ps_apply", "poseidon_hybcomm_choose",
+           "poseidon_hybcomm_cost", "poseidon_pool_create", "poseidon_pool_destroy",
+           "poseidon_sync_iteration", "poseidon_pool_set_timing", "poseidon_pool_tensor_times",
+           "poseidon_abi_version")
+
+
+class PoseidonTensor(ctypes.Structure):
+    """Mirror of ``poseidon_tensor`` in include/poseidon.h."""
+    _fields_ = [("kind", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("W", ctypes.c_void_p), ("M", ctypes.c_int64), ("N", ctypes.c_int64),
+                ("U", ctypes.c_void_p), ("V", ctypes.c_void_p),
+                ("shards", ctypes.c_void_p), ("buf", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_1706_03292_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
+    L.poseidon_sf_apply.argtypes = [vp, vp, vp, i64, i64, i64, f32, vp]
+    L.poseidon_ps_apply.argtypes = [vp, vp, i32, i64, f32, f32, vp, vp]
+    L.poseidon_hybcomm_choose.argtypes = [i64, i64, i64, i64]
+    L.poseidon_hybcomm_cost.argtypes = [i64, i64, i64, i64, i64,
+                                        ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    L.poseidon_pool_create.argtypes = [i32, ctypes.POINTER(vp)]
+    L.poseidon_pool_destroy.argtypes = [vp]
+    L.poseidon_sync_iteration.argtypes = [vp, ctypes.POINTER(PoseidonTensor), i32, i64, i32,
+                                          f32, f32, vp, ctypes.POINTER(i32)]
+    L.poseidon_pool_set_timing.argtypes = [vp, i32]
+    L.poseidon_pool_tensor_times.argtypes = [vp, ctypes.POINTER(f32), i32]
+    L.poseidon_abi_version.argtypes = []
+    for name in EXPORTS:
+        getattr(L, name).restype = ctypes.c_int
+    if L.poseidon_abi_version() != ABI_VERSION:
+        raise RuntimeError("libposeidon.so ABI version mismatch; rebuild it")
+    _lib = L
+    return L

@@ -1,0 +1,206 @@
+"""Python binding of libposeidon.so: argument marshalling only.
+
+Every function takes PyTorch tensors that already live on a HIP device,
+checks dtype/shape/contiguity/device, and hands raw pointers and the current
+stream to the C ABI (include/poseidon.h).  All arithmetic happens in the HIP
+kernels; nothing here computes on the host, and tensors on the CPU are
+rejected rather than handled.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib as L
+from ._lib import ERR_HIP, ERR_INVALID_ARG, ERR_PAYLOAD, KIND_FC, KIND_OTHER, PS, SFB  # noqa: F401
+
+
+class PoseidonError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        names = {L.ERR_INVALID_ARG: "invalid argument", L.ERR_HIP: "HIP error",
+                 L.ERR_PAYLOAD: "missing payload for the chosen scheme"}
+        super().__init__(f"{fn} failed: {names.get(status, status)} ({status})")
+        self.status = status
+
+
+def _check(fn: str, status: int) -> int:
+    if status < 0:
+        raise PoseidonError(fn, status)
+    return status
+
+
+def _dev_f32(name: str, t: torch.Tensor) -> torch.Tensor:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.dtype != torch.float32:
+        raise TypeError(f"{name} must be float32, got {t.dtype}")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on a HIP device (no host path exists)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream_handle(stream, device) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _same_device(*ts):
+    devs = {t.device for t in ts if t is not None}
+    if len(devs) > 1:
+        raise ValueError(f"tensors on different devices: {devs}")
+
+
+# --------------------------------------------------------------------------
+# Single-tensor entry points
+# --------------------------------------------------------------------------
+
+def sf_apply(W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, lr: float, stream=None) -> None:
+    """W[M,N] -= lr * U[K,M]^T @ V[K,N], in place (poseidon_sf_apply)."""
+    _dev_f32("W", W), _dev_f32("U", U), _dev_f32("V", V)
+    _same_device(W, U, V)
+    if W.dim() != 2 or U.dim() != 2 or V.dim() != 2:
+        raise ValueError("W, U, V must be 2-D")
+    M, N = W.shape
+    K = U.shape[0]
+    if U.shape != (K, M) or V.shape != (K, N):
+        raise ValueError(f"shapes: W {tuple(W.shape)}, U {tuple(U.shape)}, V {tuple(V.shape)}")
+    with torch.cuda.device(W.device):
+        _check("poseidon_sf_apply", L.lib().poseidon_sf_apply(
+            W.data_ptr(), U.data_ptr(), V.data_ptr(), M, N, K, float(lr),
+            _stream_handle(stream, W.device)))
+
+
+def ps_apply(W: torch.Tensor, shards: torch.Tensor, lr: float, momentum: float = 0.0,
+             buf: torch.Tensor | None = None, stream=None) -> None:
+    """buf = momentum*buf + shards.sum(0); W -= lr*buf, in place (poseidon_ps_apply).
+
+    shards is P x n (or P x shape-of-W); without buf, momentum must be 0."""
+    _dev_f32("W", W), _dev_f32("shards", shards)
+    if buf is not None:
+        _dev_f32("buf", buf)
+    _same_device(W, shards, buf)
+    n = W.numel()
+    P = shards.shape[0] if shards.dim() >= 1 else 0
+    if shards.numel() != P * n or (buf is not None and buf.numel() != n):
+        raise ValueError(f"shards must be P x {n} and buf must have {n} values")
+    with torch.cuda.device(W.device):
+        _check("poseidon_ps_apply", L.lib().poseidon_ps_apply(
+            W.data_ptr(), shards.data_ptr(), P, n, float(lr), float(momentum),
+            buf.data_ptr() if buf is not None else None, _stream_handle(stream, W.device)))
+
+
+def hybcomm_choose(M: int, N: int, B: int, P: int) -> int:
+    """Alg. 1 for an FC layer on P worker+server nodes: SFB (1) or PS (0)."""
+    return _check("poseidon_hybcomm_choose", L.lib().poseidon_hybcomm_choose(M, N, B, P))
+
+
+def hybcomm_cost(M: int, N: int, B: int, P1: int, P2: int) -> tuple[int, int]:
+    """Table 1 per-node values x P2: (PS server&worker, SFB worker)."""
+    ps, sfb = ctypes.c_int64(), ctypes.c_int64()
+    _check("poseidon_hybcomm_cost", L.lib().poseidon_hybcomm_cost(
+        M, N, B, P1, P2, ctypes.byref(ps), ctypes.byref(sfb)))
+    return ps.value, sfb.value
+
+
+# --------------------------------------------------------------------------
+# Whole-iteration synchronisation on a stream pool
+# --------------------------------------------------------------------------
+
+class StreamPool:
+    """The library's pool of HIP streams on the current device."""
+
+    def __init__(self, num_streams: int = 4, device=None):
+        self._h = ctypes.c_void_p()
+        dev = torch.device("cuda", torch.cuda.current_device()) if device is None else torch.device(device)
+        self.device = dev
+        with torch.cuda.device(dev):
+            _check("poseidon_pool_create", L.lib().poseidon_pool_create(num_streams, ctypes.byref(self._h)))
+        self.num_streams = num_streams
+
+    @property
+    def handle(self):
+        return self._h
+
+    def set_timing(self, enable: bool) -> None:
+        """Bracket every update of the following iterations with timing events."""
+        _check("poseidon_pool_set_timing", L.lib().poseidon_pool_set_timing(self._h, int(bool(enable))))
+
+    def tensor_times(self, count: int) -> list[float]:
+        """Per-tensor ms of the last timed iteration (-1: no work); waits for it."""
+        ms = (ctypes.c_float * max(1, count))()
+        with torch.cuda.device(self.device):
+            _check("poseidon_pool_tensor_times", L.lib().poseidon_pool_tensor_times(self._h, ms, count))
+        return list(ms[:count])
+
+    def close(self):
+        if self._h:
+            with torch.cuda.device(self.device):
+                L.lib().poseidon_pool_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def _ptr(t):
+    return t.data_ptr() if t is not None else None
+
+
+class SyncIteration:
+    """One iteration's synchronisation of a list of tensors (forward order).
+
+    Each entry is a dict with ``W`` and either ``U``/``V`` (SF payload) or
+    ``shards`` (dense payload), an optional ``buf``, and ``fc`` (bool, or taken
+    from ``spec.kind == 'fc'``).  The descriptor array is built once; calling
+    the object enqueues the whole iteration (poseidon_sync_iteration)."""
+
+    def __init__(self, pool: StreamPool, tensors: list, B: int, P: int, lr: float,
+                 momentum: float = 0.0):
+        self.pool, self.B, self.P = pool, int(B), int(P)
+        self.lr, self.momentum = float(lr), float(momentum)
+        self._keep = []
+        arr = (L.PoseidonTensor * len(tensors))()
+        for i, t in enumerate(tensors):
+            fc = t["fc"] if "fc" in t else (t["spec"].kind == "fc")
+            W = _dev_f32("W", t["W"])
+            U, V, G, buf = t.get("U"), t.get("V"), t.get("shards"), t.get("buf")
+            for name, x in (("U", U), ("V", V), ("shards", G), ("buf", buf)):
+                if x is not None:
+                    _dev_f32(name, x)
+            _same_device(W, U, V, G, buf)
+            if W.device != pool.device:
+                raise ValueError("tensors must live on the pool's device")
+            if fc:
+                if W.dim() != 2:
+                    raise ValueError("an FC weight must be 2-D")
+                M, N = W.shape
+                K = self.B * self.P
+                if U is not None and (U.shape != (K, M) or V is None or V.shape != (K, N)):
+                    raise ValueError("U/V must be (P*B) x M and (P*B) x N")
+            else:
+                M, N = W.numel(), 1
+            n = W.numel()
+            if G is not None and G.numel() != self.P * n:
+                raise ValueError("shards must be P x n")
+            if buf is not None and buf.numel() != n:
+                raise ValueError("buf must have n values")
+            arr[i] = L.PoseidonTensor(KIND_FC if fc else KIND_OTHER, 0, W.data_ptr(), M, N,
+                                      _ptr(U), _ptr(V), _ptr(G), _ptr(buf))
+            self._keep.append((W, U, V, G, buf))
+        self._arr = arr
+        self._schemes = (ctypes.c_int32 * max(1, len(tensors)))()
+        self.count = len(tensors)
+
+    def __call__(self, stream=None) -> list[int]:
+        with torch.cuda.device(self.pool.device):
+            _check("poseidon_sync_iteration", L.lib().poseidon_sync_iteration(
+                self.pool.handle, self._arr, self.count, self.B, self.P, self.lr, self.momentum,
+                _stream_handle(stream, self.pool.device), self._schemes))
+        return list(self._schemes[:self.count])

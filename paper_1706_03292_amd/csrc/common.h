@@ -1,0 +1,39 @@
+// Internal helpers shared by the HIP sources of libposeidon.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "poseidon.h"
+
+namespace poseidon {
+
+// Native 4-wide vector (lowers to dwordx4 loads/stores).
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// True when the byte ranges [a, a+abytes) and [b, b+bbytes) overlap.
+inline bool overlaps(const void* a, int64_t abytes, const void* b, int64_t bbytes)
+{
+    if (!a || !b || abytes <= 0 || bbytes <= 0) return false;
+    const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
+    return a0 < b0 + static_cast<uintptr_t>(bbytes) && b0 < a0 + static_cast<uintptr_t>(abytes);
+}
+
+// Number of compute units of the current device (cached per device).
+int device_cu_count();
+
+// Internal launchers (arguments already validated; nonzero sizes).
+hipError_t launch_sf_apply(float* W, const float* U, const float* V,
+                           int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream);
+hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
+                           float lr, float momentum, float* buf, hipStream_t stream);
+
+// Argument checks of the public entry points (no device work).
+int check_sf_args(const float* W, const float* U, const float* V,
+                  int64_t M, int64_t N, int64_t K);
+int check_ps_args(const float* W, const float* shards, int32_t P, int64_t n,
+                  float momentum, const float* buf);
+
+}  // namespace poseidon

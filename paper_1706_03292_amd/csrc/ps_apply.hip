@@ -1,0 +1,202 @@
+// Parameter-server aggregation + momentum SGD apply (Sec. 2.1 "Parameter
+// Server"; Sec. 4.1 "KV Store", "Managing Consistency").
+//
+//   s_i = sum_{p<P} G[p*n + i]   (p increasing, fp32)
+//   buf_i = fma(mu, buf_i, s_i);  W_i = fma(-lr, buf_i, W_i)
+//
+// The kernel is bound by HBM bandwidth: per element it reads P shard values
+// plus W and buf and writes W and buf (4P + 16 bytes), against ~P + 3 flops.
+// Each thread owns 16-byte groups of four consecutive elements, issues all of
+// a group's shard loads before the dependent adds (bytes in flight), streams
+// the single-use shards with non-temporal loads, and walks the array with a
+// grid-stride loop sized to keep every CU busy.  A scalar variant covers sizes
+// that are not a multiple of four or arrays that are not 16-byte aligned.
+#include "common.h"
+
+namespace poseidon {
+namespace {
+
+constexpr int PS_THREADS = 256;
+constexpr int PS_CHUNK = 8;       // shard loads in flight per step when P is a runtime value
+
+__device__ inline f4 fma4(float a, f4 b, f4 c)
+{
+    return f4{fmaf(a, b.x, c.x), fmaf(a, b.y, c.y), fmaf(a, b.z, c.z), fmaf(a, b.w, c.w)};
+}
+
+// Sum of the P shard values at vector index i, in increasing p.
+template <int PT>
+__device__ inline f4 shard_sum4(const f4* __restrict__ G4, int P, int64_t n4, int64_t i)
+{
+    if constexpr (PT > 0) {
+        f4 g[PT];
+#pragma unroll
+        for (int p = 0; p < PT; ++p)
+            g[p] = __builtin_nontemporal_load(G4 + static_cast<int64_t>(p) * n4 + i);
+        f4 s = g[0];
+#pragma unroll
+        for (int p = 1; p < PT; ++p)
+            s += g[p];
+        return s;
+    } else {
+        f4 s = __builtin_nontemporal_load(G4 + i);
+        int p = 1;
+        for (; p + PS_CHUNK <= P; p += PS_CHUNK) {
+            f4 g[PS_CHUNK];
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                g[c] = __builtin_nontemporal_load(G4 + static_cast<int64_t>(p + c) * n4 + i);
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                s += g[c];
+        }
+        for (; p < P; ++p)
+            s += __builtin_nontemporal_load(G4 + static_cast<int64_t>(p) * n4 + i);
+        return s;
+    }
+}
+
+template <int PT>
+__device__ inline float shard_sum1(const float* __restrict__ G, int P, int64_t n, int64_t i)
+{
+    if constexpr (PT > 0) {
+        float g[PT];
+#pragma unroll
+        for (int p = 0; p < PT; ++p)
+            g[p] = __builtin_nontemporal_load(G + static_cast<int64_t>(p) * n + i);
+        float s = g[0];
+#pragma unroll
+        for (int p = 1; p < PT; ++p)
+            s += g[p];
+        return s;
+    } else {
+        float s = __builtin_nontemporal_load(G + i);
+        int p = 1;
+        for (; p + PS_CHUNK <= P; p += PS_CHUNK) {
+            float g[PS_CHUNK];
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                g[c] = __builtin_nontemporal_load(G + static_cast<int64_t>(p + c) * n + i);
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                s += g[c];
+        }
+        for (; p < P; ++p)
+            s += __builtin_nontemporal_load(G + static_cast<int64_t>(p) * n + i);
+        return s;
+    }
+}
+
+template <int PT, bool MOM>
+__global__ __launch_bounds__(PS_THREADS) void ps_apply_vec4(
+    float* __restrict__ W, const float* __restrict__ G, int P, int64_t n4,
+    float lr, float mu, float* __restrict__ buf)
+{
+    const f4* G4 = reinterpret_cast<const f4*>(G);
+    f4* W4 = reinterpret_cast<f4*>(W);
+    f4* B4 = reinterpret_cast<f4*>(buf);
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS + threadIdx.x; i < n4; i += stride) {
+        const f4 s = shard_sum4<PT>(G4, P, n4, i);
+        f4 w = W4[i];
+        if constexpr (MOM) {
+            const f4 b = fma4(mu, B4[i], s);
+            B4[i] = b;
+            w = fma4(-lr, b, w);
+        } else {
+            w = fma4(-lr, s, w);
+        }
+        W4[i] = w;
+    }
+}
+
+template <int PT, bool MOM>
+__global__ __launch_bounds__(PS_THREADS) void ps_apply_scalar(
+    float* __restrict__ W, const float* __restrict__ G, int P, int64_t n,
+    float lr, float mu, float* __restrict__ buf)
+{
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS + threadIdx.x; i < n; i += stride) {
+        const float s = shard_sum1<PT>(G, P, n, i);
+        float w = W[i];
+        if constexpr (MOM) {
+            const float b = fmaf(mu, buf[i], s);
+            buf[i] = b;
+            w = fmaf(-lr, b, w);
+        } else {
+            w = fmaf(-lr, s, w);
+        }
+        W[i] = w;
+    }
+}
+
+template <int PT, bool MOM>
+hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, float mu,
+                     float* buf, bool vec, hipStream_t stream)
+{
+    const int64_t items = vec ? n / 4 : n;
+    const int64_t want = (items + PS_THREADS - 1) / PS_THREADS;
+    const int64_t cap = static_cast<int64_t>(device_cu_count()) * 8;
+    const int grid = static_cast<int>(want < cap ? want : cap);
+    if (vec)
+        ps_apply_vec4<PT, MOM><<<grid, PS_THREADS, 0, stream>>>(W, G, P, items, lr, mu, buf);
+    else
+        ps_apply_scalar<PT, MOM><<<grid, PS_THREADS, 0, stream>>>(W, G, P, items, lr, mu, buf);
+    return hipGetLastError();
+}
+
+template <bool MOM>
+hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, float mu,
+                      float* buf, bool vec, hipStream_t stream)
+{
+    switch (P) {
+    case 1:  return launch_pt<1, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    case 2:  return launch_pt<2, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    case 4:  return launch_pt<4, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    case 8:  return launch_pt<8, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    case 16: return launch_pt<16, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    case 32: return launch_pt<32, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    default: return launch_pt<0, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
+                           float lr, float momentum, float* buf, hipStream_t stream)
+{
+    const bool vec = (n % 4 == 0) && aligned16(W) && aligned16(shards) && (!buf || aligned16(buf));
+    if (buf)
+        return launch_mom<true>(W, shards, P, n, lr, momentum, buf, vec, stream);
+    return launch_mom<false>(W, shards, P, n, lr, 0.0f, nullptr, vec, stream);
+}
+
+int check_ps_args(const float* W, const float* shards, int32_t P, int64_t n,
+                  float momentum, const float* buf)
+{
+    if (P < 1 || n < 0)
+        return POSEIDON_ERR_INVALID_ARG;
+    if (n == 0)
+        return POSEIDON_OK;
+    if (!W || !shards || (!buf && momentum != 0.0f))
+        return POSEIDON_ERR_INVALID_ARG;
+    if (n > (INT64_MAX / 4) / P)
+        return POSEIDON_ERR_INVALID_ARG;
+    const int64_t wb = n * 4, gb = n * 4 * static_cast<int64_t>(P);
+    if (overlaps(W, wb, shards, gb) || overlaps(buf, wb, shards, gb) || overlaps(W, wb, buf, wb))
+        return POSEIDON_ERR_INVALID_ARG;
+    return POSEIDON_OK;
+}
+
+}  // namespace poseidon
+
+extern "C" int poseidon_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
+                                 float lr, float momentum, float* buf, hipStream_t stream)
+{
+    const int rc = poseidon::check_ps_args(W, shards, P, n, momentum, buf);
+    if (rc != POSEIDON_OK || n == 0)
+        return rc;
+    return poseidon::launch_ps_apply(W, shards, P, n, lr, momentum, buf, stream) == hipSuccess
+               ? POSEIDON_OK
+               : POSEIDON_ERR_HIP;
+}

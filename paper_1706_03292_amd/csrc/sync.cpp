@@ -1,0 +1,247 @@
+// One iteration's synchronisation of a network on a pool of HIP streams
+// (Sec. 3 "wait-free backpropagation"; Sec. 4.1 "Client Library", "Managing
+// Consistency"; Alg. 2).  The host walks the tensors in backpropagation
+// order, asks Alg. 1 for each one's scheme, and enqueues the matching update
+// on the next stream of the pool; a fork event and one join event per stream
+// make the whole iteration a single asynchronous operation on the caller's
+// stream (the bulk-synchronous barrier).
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <vector>
+
+#include "common.h"
+
+struct poseidon_stream_pool {
+    int device = -1;
+    std::vector<hipStream_t> streams;
+    std::vector<hipEvent_t> joined;   // one per stream: its last update of the iteration
+    hipEvent_t fork = nullptr;        // work enqueued on the caller's stream before the iteration
+    bool timing = false;
+    std::vector<hipEvent_t> t_start;  // per tensor of the last timed iteration
+    std::vector<hipEvent_t> t_stop;
+    std::vector<char> t_ran;
+    int32_t t_count = -1;             // tensors in the last timed iteration (-1: none)
+};
+
+namespace poseidon {
+
+int device_cu_count()
+{
+    static std::atomic<int> cache[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return 256;
+    if (dev >= 0 && dev < 64) {
+        const int c = cache[dev].load(std::memory_order_relaxed);
+        if (c > 0)
+            return c;
+    }
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+        cus = 256;
+    if (dev >= 0 && dev < 64)
+        cache[dev].store(cus, std::memory_order_relaxed);
+    return cus;
+}
+
+}  // namespace poseidon
+
+namespace {
+
+void destroy_pool(poseidon_stream_pool* pool)
+{
+    for (hipStream_t s : pool->streams)
+        if (s) {
+            (void)hipStreamSynchronize(s);
+            (void)hipStreamDestroy(s);
+        }
+    for (hipEvent_t e : pool->joined)
+        if (e)
+            (void)hipEventDestroy(e);
+    if (pool->fork)
+        (void)hipEventDestroy(pool->fork);
+    for (hipEvent_t e : pool->t_start)
+        (void)hipEventDestroy(e);
+    for (hipEvent_t e : pool->t_stop)
+        (void)hipEventDestroy(e);
+    delete pool;
+}
+
+// Make sure the pool holds timing events for `count` tensors.
+bool reserve_timing(poseidon_stream_pool* pool, int32_t count)
+{
+    while (static_cast<int32_t>(pool->t_start.size()) < count) {
+        hipEvent_t a = nullptr, b = nullptr;
+        if (hipEventCreate(&a) != hipSuccess)
+            return false;
+        if (hipEventCreate(&b) != hipSuccess) {
+            (void)hipEventDestroy(a);
+            return false;
+        }
+        pool->t_start.push_back(a);
+        pool->t_stop.push_back(b);
+    }
+    pool->t_ran.assign(static_cast<size_t>(count), 0);
+    return true;
+}
+
+}  // namespace
+
+extern "C" int poseidon_pool_create(int32_t num_streams, poseidon_stream_pool** out)
+{
+    if (!out || num_streams < 1 || num_streams > 64)
+        return POSEIDON_ERR_INVALID_ARG;
+    *out = nullptr;
+    auto* pool = new poseidon_stream_pool;
+    bool ok = hipGetDevice(&pool->device) == hipSuccess &&
+              hipEventCreateWithFlags(&pool->fork, hipEventDisableTiming) == hipSuccess;
+    for (int32_t i = 0; ok && i < num_streams; ++i) {
+        hipStream_t s = nullptr;
+        hipEvent_t e = nullptr;
+        // Default priority on purpose: every stream of the library shares one.
+        ok = hipStreamCreateWithFlags(&s, hipStreamNonBlocking) == hipSuccess;
+        if (ok)
+            pool->streams.push_back(s);
+        ok = ok && hipEventCreateWithFlags(&e, hipEventDisableTiming) == hipSuccess;
+        if (ok)
+            pool->joined.push_back(e);
+    }
+    if (!ok) {
+        destroy_pool(pool);
+        return POSEIDON_ERR_HIP;
+    }
+    *out = pool;
+    return POSEIDON_OK;
+}
+
+extern "C" int poseidon_pool_destroy(poseidon_stream_pool* pool)
+{
+    if (pool)
+        destroy_pool(pool);
+    return POSEIDON_OK;
+}
+
+extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
+                                       const poseidon_tensor* tensors, int32_t count,
+                                       int64_t B, int32_t P, float lr, float momentum,
+                                       hipStream_t stream, int32_t* schemes)
+{
+    using namespace poseidon;
+    if (!pool || count < 0 || (count > 0 && !tensors) || B < 0 || P < 1)
+        return POSEIDON_ERR_INVALID_ARG;
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return POSEIDON_ERR_HIP;
+    if (dev != pool->device)
+        return POSEIDON_ERR_INVALID_ARG;
+    const int64_t K = B * static_cast<int64_t>(P);
+
+    // Validate everything and fix every scheme before enqueueing anything.
+    std::vector<int32_t> plan(static_cast<size_t>(count));
+    int32_t active = 0;
+    for (int32_t t = 0; t < count; ++t) {
+        const poseidon_tensor& x = tensors[t];
+        if ((x.kind != POSEIDON_KIND_FC && x.kind != POSEIDON_KIND_OTHER) || x.reserved != 0 ||
+            x.M < 0 || x.N < 0 || (x.N > 0 && x.M > INT64_MAX / x.N))
+            return POSEIDON_ERR_INVALID_ARG;
+        int32_t scheme = POSEIDON_PS;
+        if (x.kind == POSEIDON_KIND_FC) {
+            scheme = poseidon_hybcomm_choose(x.M, x.N, B, P);
+            if (scheme < 0)
+                return POSEIDON_ERR_INVALID_ARG;
+        }
+        const int64_t n = x.M * x.N;
+        int rc;
+        if (scheme == POSEIDON_SFB) {
+            if (n > 0 && K > 0 && (!x.U || !x.V))
+                return POSEIDON_ERR_PAYLOAD;
+            rc = check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
+            if (n > 0 && K > 0)
+                ++active;
+        } else {
+            if (n > 0 && !x.shards)
+                return POSEIDON_ERR_PAYLOAD;
+            rc = check_ps_args(x.W, x.shards, P, n, x.buf ? momentum : 0.0f, x.buf);
+            if (n > 0)
+                ++active;
+        }
+        if (rc != POSEIDON_OK)
+            return rc;
+        plan[static_cast<size_t>(t)] = scheme;
+    }
+    if (schemes)
+        for (int32_t t = 0; t < count; ++t)
+            schemes[t] = plan[static_cast<size_t>(t)];
+    if (pool->timing) {
+        if (!reserve_timing(pool, count))
+            return POSEIDON_ERR_HIP;
+        pool->t_count = count;
+    }
+    if (active == 0)
+        return POSEIDON_OK;
+
+    const int32_t S = static_cast<int32_t>(pool->streams.size());
+    const int32_t used = active < S ? active : S;
+    if (hipEventRecord(pool->fork, stream) != hipSuccess)
+        return POSEIDON_ERR_HIP;
+    for (int32_t s = 0; s < used; ++s)
+        if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
+            return POSEIDON_ERR_HIP;
+
+    // Backpropagation order: the last tensor's gradient is ready first.
+    int32_t q = 0;
+    for (int32_t t = count - 1; t >= 0; --t) {
+        const poseidon_tensor& x = tensors[t];
+        const int64_t n = x.M * x.N;
+        const bool sfb = plan[static_cast<size_t>(t)] == POSEIDON_SFB;
+        if (n == 0 || (sfb && K == 0))
+            continue;
+        hipStream_t s = pool->streams[q % used];
+        if (pool->timing && hipEventRecord(pool->t_start[t], s) != hipSuccess)
+            return POSEIDON_ERR_HIP;
+        const hipError_t err =
+            sfb ? launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s)
+                : launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
+        if (err != hipSuccess)
+            return POSEIDON_ERR_HIP;
+        if (pool->timing) {
+            if (hipEventRecord(pool->t_stop[t], s) != hipSuccess)
+                return POSEIDON_ERR_HIP;
+            pool->t_ran[static_cast<size_t>(t)] = 1;
+        }
+        ++q;
+    }
+
+    for (int32_t s = 0; s < used; ++s) {
+        if (hipEventRecord(pool->joined[s], pool->streams[s]) != hipSuccess ||
+            hipStreamWaitEvent(stream, pool->joined[s], 0) != hipSuccess)
+            return POSEIDON_ERR_HIP;
+    }
+    return POSEIDON_OK;
+}
+
+extern "C" int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable)
+{
+    if (!pool)
+        return POSEIDON_ERR_INVALID_ARG;
+    pool->timing = enable != 0;
+    return POSEIDON_OK;
+}
+
+extern "C" int poseidon_pool_tensor_times(poseidon_stream_pool* pool, float* ms, int32_t count)
+{
+    if (!pool || pool->t_count < 0 || count != pool->t_count || (count > 0 && !ms))
+        return POSEIDON_ERR_INVALID_ARG;
+    for (int32_t t = 0; t < count; ++t) {
+        ms[t] = -1.0f;
+        if (!pool->t_ran[static_cast<size_t>(t)])
+            continue;
+        if (hipEventSynchronize(pool->t_stop[t]) != hipSuccess ||
+            hipEventElapsedTime(&ms[t], pool->t_start[t], pool->t_stop[t]) != hipSuccess)
+            return POSEIDON_ERR_HIP;
+    }
+    return POSEIDON_OK;
+}
+
+extern "C" int poseidon_abi_version(void) { return POSEIDON_ABI_VERSION; }

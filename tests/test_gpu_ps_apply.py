@@ -1,0 +1,149 @@
+"""GPU parity of poseidon_ps_apply (P-shard aggregation + momentum SGD) with
+the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from _helpers import BUF_TOL, W_TOL, assert_close, dev, log, misaligned, to_np
+from paper_1706_03292_amd import api
+from paper_1706_03292_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _draw(P, n, seed, buf_std=0.0):
+    W = I.randn(seed, (n,), 0.01)
+    G = I.randn(seed + 1, (P, n), 1e-3)
+    buf = I.randn(seed + 2, (n,), 1e-3) if buf_std else torch.zeros(n)
+    return W, G, buf
+
+
+CASES = [
+    (4, 1 << 20),        # the 1M-parameter layer of the single-FC workload
+    (4, 1_000_003),      # ragged: n % 4 == 3
+    (1, 1), (2, 3), (3, 4), (5, 5), (8, 1023), (16, 4096 + 2),
+    (32, 9 * 1031), (33, 2049), (7, 65536 + 1), (16, 262144),
+]
+
+
+@pytest.mark.parametrize("P,n", CASES)
+@pytest.mark.parametrize("momentum", [0.9, 0.0])
+def test_ps_apply_matches_oracle(P, n, momentum):
+    d = dev()
+    W, G, buf = _draw(P, n, seed=P * 1000 + n % 997, buf_std=1e-3)
+    use_buf = momentum != 0.0
+    w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, momentum,
+                                   buf.numpy() if use_buf else None)
+    Wd, Gd = W.to(d), G.to(d)
+    bd = buf.to(d) if use_buf else None
+    log(f"ps_apply P={P} n={n} momentum={momentum}")
+    api.ps_apply(Wd, Gd, 0.01, momentum, bd)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), w_ref, W_TOL, f"W P={P} n={n}")
+    if use_buf:
+        assert_close(to_np(bd), b_ref, BUF_TOL, f"buf P={P} n={n}")
+
+
+@pytest.mark.parametrize("P,n", [(16, 1 << 16), (32, 12345), (3, 4097)])
+def test_ps_raw_sum_matches_oracle(P, n):
+    """W = 0, lr = -1, no momentum: W becomes the shard sum itself."""
+    d = dev()
+    _, G, _ = _draw(P, n, seed=P + n)
+    w_ref, _ = oracle.ps_apply(np.zeros(n, np.float32), G.numpy(), -1.0, 0.0, None)
+    Wd = torch.zeros(n, device=d)
+    log(f"ps_apply raw-sum P={P} n={n}")
+    api.ps_apply(Wd, G.to(d), -1.0, 0.0, None)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), w_ref, BUF_TOL, "sum")
+
+
+def test_ps_apply_with_buffer_and_zero_momentum():
+    d = dev()
+    P, n = 6, 5000
+    W, G, buf = _draw(P, n, seed=3, buf_std=1e-3)
+    w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, 0.0, buf.numpy())
+    Wd, bd = W.to(d), buf.to(d)
+    log("ps_apply buf with momentum 0")
+    api.ps_apply(Wd, G.to(d), 0.01, 0.0, bd)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), w_ref, W_TOL, "W")
+    assert_close(to_np(bd), b_ref, BUF_TOL, "buf")
+
+
+@pytest.mark.parametrize("P,n", [(16, 4096), (4, 1001)])
+def test_ps_apply_misaligned(P, n):
+    d = dev()
+    W, G, buf = _draw(P, n, seed=11, buf_std=1e-3)
+    w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, 0.9, buf.numpy())
+    Wd, Gd, bd = misaligned(W.to(d)), misaligned(G.to(d)), misaligned(buf.to(d))
+    log(f"ps_apply misaligned P={P} n={n}")
+    api.ps_apply(Wd, Gd, 0.01, 0.9, bd)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), w_ref, W_TOL, "W")
+    assert_close(to_np(bd), b_ref, BUF_TOL, "buf")
+
+
+def test_ps_apply_shard_order_within_tolerance_and_deterministic():
+    d = dev()
+    P, n = 16, 1 << 18
+    W, G, buf = _draw(P, n, seed=21, buf_std=1e-3)
+    w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, 0.9, buf.numpy())
+    outs = []
+    perms = [np.arange(P), np.arange(P), np.random.default_rng(0).permutation(P)]
+    for perm in perms:
+        Wd, bd = W.to(d), buf.to(d)
+        log(f"ps_apply order {list(perm)[:4]}...")
+        api.ps_apply(Wd, G[torch.from_numpy(perm)].contiguous().to(d), 0.01, 0.9, bd)
+        torch.cuda.synchronize()
+        outs.append((Wd.cpu(), bd.cpu()))
+        assert_close(outs[-1][0].numpy(), w_ref, W_TOL, "W")
+        assert_close(outs[-1][1].numpy(), b_ref, BUF_TOL, "buf")
+    # same order twice: bit-identical
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+
+
+def test_ps_apply_repeated_iterations_track_oracle():
+    """Five iterations with fresh shards: W and buf evolve as the oracle's."""
+    d = dev()
+    P, n = 8, 100_003
+    W, _, buf = _draw(P, n, seed=31)
+    w_ref, b_ref = W.numpy(), buf.numpy()
+    Wd, bd = W.to(d), buf.to(d)
+    for it in range(5):
+        G = I.randn(500 + it, (P, n), 1e-3)
+        w_ref, b_ref = oracle.ps_apply(w_ref, G.numpy(), 0.01, 0.9, b_ref)
+        log(f"ps_apply iteration {it}")
+        api.ps_apply(Wd, G.to(d), 0.01, 0.9, bd)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), w_ref, W_TOL, "W")
+    assert_close(to_np(bd), b_ref, BUF_TOL, "buf")
+
+
+def test_ps_apply_errors():
+    d = dev()
+    W = torch.zeros(16, device=d)
+    G = torch.zeros(2, 16, device=d)
+    with pytest.raises(api.PoseidonError):
+        api.ps_apply(W, G, 0.1, 0.9, None)                 # momentum without a buffer
+    with pytest.raises(ValueError):
+        api.ps_apply(W, torch.zeros(2, 15, device=d), 0.1)
+    with pytest.raises(ValueError):
+        api.ps_apply(W.cpu(), G.cpu(), 0.1)                 # no host path
+
+
+def test_ps_apply_fc_sized_layer_sampled():
+    """The 4096 x 4096 layer through PS (P=8, momentum 0.9) at full size."""
+    d = dev()
+    wl = I.workload(2)
+    t = I.make_tensors(wl, only=["fc7.W.dense"])[0]
+    W, G, buf = t["W"].reshape(-1), t["shards"], t["buf"]
+    n = W.numel()
+    idx = np.concatenate([np.random.default_rng(0).integers(0, n, 20000), np.arange(n - 100, n)])
+    w_ref, b_ref = oracle.ps_apply_points(W.numpy(), G.numpy(), wl.lr, wl.momentum, buf.numpy(), idx)
+    Wd, bd = W.to(d), buf.to(d)
+    log("ps_apply 4096x4096 P=8")
+    api.ps_apply(Wd, G.to(d), wl.lr, wl.momentum, bd)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd)[idx], w_ref, W_TOL, "W")
+    assert_close(to_np(bd)[idx], b_ref, BUF_TOL, "buf")

@@ -1,0 +1,141 @@
+"""GPU parity of poseidon_sf_apply (SF reconstruction + SGD) with the oracle."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from _helpers import (DELTA_TOL, W_TOL, assert_close, dev, log, misaligned, sample_points,
+                      to_np)
+from paper_1706_03292_amd import api
+from paper_1706_03292_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _draw(M, N, K, seed, w_std=0.01, sf_scale=1.0):
+    W = I.randn(seed, (M, N), w_std)
+    U = I.randn(seed + 1, (K, M), sf_scale)
+    V = I.randn(seed + 2, (K, N), sf_scale)
+    return W, U, V
+
+
+# Small and medium shapes the full oracle finishes in seconds: several tiles in
+# each direction plus ragged tails in M, N and K, including every residue mod 4.
+SHAPES = [
+    (1024, 512, 64),     # the single-FC-layer workload
+    (300, 200, 37),
+    (129, 257, 3),
+    (33, 65, 1),
+    (1, 1, 1),
+    (1, 777, 5),
+    (777, 1, 5),
+    (250, 130, 16),
+    (261, 387, 18),
+    (1000, 2048, 1024),  # the Inception-shaped classifier, K = 32 x 32
+    (517, 515, 513),
+]
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES)
+def test_sf_apply_matches_oracle(M, N, K):
+    d = dev()
+    W, U, V = _draw(M, N, K, seed=10 * M + N + K)
+    ref = oracle.sf_apply(W.numpy(), U.numpy(), V.numpy(), 0.01)
+    Wd = W.to(d)
+    log(f"sf_apply M={M} N={N} K={K}")
+    api.sf_apply(Wd, U.to(d), V.to(d), 0.01)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), ref, W_TOL, f"W {M}x{N} K={K}")
+
+
+@pytest.mark.parametrize("M,N,K", SHAPES)
+def test_sf_raw_gradient_matches_oracle(M, N, K):
+    """W = 0 and lr = -1 make the kernel write the reconstructed gradient
+    itself, so it can be held to a much tighter bar than the W update."""
+    d = dev()
+    _, U, V = _draw(M, N, K, seed=7 * M + N + 3 * K)
+    ref = oracle.sf_delta(U.numpy(), V.numpy())
+    Wd = torch.zeros(M, N, device=d)
+    log(f"sf_apply raw-delta M={M} N={N} K={K}")
+    api.sf_apply(Wd, U.to(d), V.to(d), -1.0)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), ref, DELTA_TOL, f"dW {M}x{N} K={K}")
+
+
+@pytest.mark.parametrize("M,N,K", [(256, 384, 40), (203, 129, 17), (1024, 512, 64)])
+def test_sf_apply_misaligned_pointers(M, N, K):
+    d = dev()
+    W, U, V = _draw(M, N, K, seed=99 + M)
+    ref = oracle.sf_apply(W.numpy(), U.numpy(), V.numpy(), 0.01)
+    Wd, Ud, Vd = misaligned(W.to(d)), misaligned(U.to(d)), misaligned(V.to(d))
+    log(f"sf_apply misaligned M={M} N={N} K={K}")
+    api.sf_apply(Wd, Ud, Vd, 0.01)
+    torch.cuda.synchronize()
+    assert_close(to_np(Wd), ref, W_TOL, "misaligned")
+
+
+def test_sf_gpu_gradient_rank_at_most_K():
+    d = dev()
+    M, N, K = 64, 48, 8
+    _, U, V = _draw(M, N, K, seed=5)
+    Wd = torch.zeros(M, N, device=d)
+    log("sf_apply rank")
+    api.sf_apply(Wd, U.to(d), V.to(d), -1.0)
+    torch.cuda.synchronize()
+    s = np.linalg.svd(to_np(Wd).astype(np.float64), compute_uv=False)
+    assert s[K] / s[0] < 1e-5
+
+
+def test_sf_apply_deterministic_and_noop_cases():
+    d = dev()
+    M, N, K = 300, 520, 96
+    W, U, V = _draw(M, N, K, seed=77)
+    Ud, Vd = U.to(d), V.to(d)
+    a, b = W.to(d), W.to(d)
+    log("sf_apply determinism")
+    api.sf_apply(a, Ud, Vd, 0.01)
+    api.sf_apply(b, Ud, Vd, 0.01)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    # K = 0 and empty W leave everything untouched.
+    c = W.to(d)
+    api.sf_apply(c, torch.zeros(0, M, device=d), torch.zeros(0, N, device=d), 0.01)
+    torch.cuda.synchronize()
+    assert torch.equal(c.cpu(), W)
+    api.sf_apply(torch.zeros(0, N, device=d), torch.zeros(K, 0, device=d), Vd, 0.01)
+
+
+def test_sf_apply_rejects_cpu_and_bad_shapes():
+    d = dev()
+    W, U, V = _draw(8, 8, 2, seed=1)
+    with pytest.raises(ValueError):
+        api.sf_apply(W, U, V, 0.1)                       # host tensors: no host path
+    with pytest.raises(ValueError):
+        api.sf_apply(W.to(d), U.to(d)[:, :4].contiguous(), V.to(d), 0.1)
+    with pytest.raises(TypeError):
+        api.sf_apply(W.to(d).double(), U.to(d), V.to(d), 0.1)
+
+
+@pytest.mark.parametrize("name", ["fc6.W", "fc7.W", "fc8.W"])
+def test_sf_apply_vgg19_22k_full_size_sampled(name):
+    """The VGG19-22K FC layers at full size (P=16, B=32, K=512), checked at
+    sampled points, the corners and stretches of the ragged last row/column."""
+    d = dev()
+    wl = I.workload(5)
+    t = I.make_tensors(wl, only=[name])[0]
+    W, U, V = t["W"], t["U"], t["V"]
+    M, N = W.shape
+    rows, cols = sample_points(M, N, 4000, seed=M + N)
+    ref = oracle.sf_apply_points(W.numpy(), U.numpy(), V.numpy(), wl.lr, rows, cols)
+    Wd = W.to(d)
+    log(f"sf_apply full {name} {M}x{N} K={wl.K}")
+    api.sf_apply(Wd, U.to(d), V.to(d), wl.lr)
+    torch.cuda.synchronize()
+    got = to_np(Wd)[rows, cols]
+    assert_close(got, ref, W_TOL, name)
+    # and the raw gradient at the same points, tightly
+    Z = torch.zeros(M, N, device=d)
+    api.sf_apply(Z, U.to(d), V.to(d), -1.0)
+    torch.cuda.synchronize()
+    ref_d = oracle.sf_apply_points(np.zeros((M, N), np.float32), U.numpy(), V.numpy(), -1.0, rows, cols)
+    assert_close(to_np(Z)[rows, cols], ref_d, DELTA_TOL, name + " raw")

@@ -1,0 +1,133 @@
+"""GPU parity of poseidon_sync_iteration: whole-iteration synchronisation of
+the evaluation workloads on the stream pool, against the oracle's per-layer
+schemes (bit-exact) and updates (sampled at full size)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from _helpers import BUF_TOL, W_TOL, assert_close, dev, log, sample_points, to_np
+from paper_1706_03292_amd import api
+from paper_1706_03292_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle_check(host, devt, wl, schemes, full_limit=2_000_000, npts=3000):
+    """Compare every tensor's update with the oracle: in full when small,
+    else at sampled points."""
+    for h, g, sch in zip(host, devt, schemes):
+        spec = h["spec"]
+        want = oracle.best_scheme(spec.kind == I.FC, *(spec.shape if spec.kind == I.FC else (spec.numel, 1)),
+                                  wl.B, wl.P)
+        assert sch == want, f"{spec.name}: scheme {sch} != oracle {want}"
+        Wg = to_np(g["W"])
+        if sch == oracle.SFB:
+            M, N = spec.shape
+            if M * N <= full_limit:
+                ref = oracle.sf_apply(h["W"].numpy(), h["U"].numpy(), h["V"].numpy(), wl.lr)
+                assert_close(Wg, ref, W_TOL, spec.name)
+            else:
+                r, c = sample_points(M, N, npts, seed=M)
+                ref = oracle.sf_apply_points(h["W"].numpy(), h["U"].numpy(), h["V"].numpy(), wl.lr, r, c)
+                assert_close(Wg[r, c], ref, W_TOL, spec.name)
+        else:
+            n = spec.numel
+            W0 = h["W"].numpy().reshape(-1)
+            b0 = h["buf"].numpy() if h.get("buf") is not None else None
+            mu = wl.momentum if b0 is not None else 0.0
+            if n <= full_limit:
+                w_ref, b_ref = oracle.ps_apply(W0, h["shards"].numpy(), wl.lr, mu, b0)
+                assert_close(Wg.reshape(-1), w_ref, W_TOL, spec.name)
+                if b0 is not None:
+                    assert_close(to_np(g["buf"]), b_ref, BUF_TOL, spec.name + " buf")
+            else:
+                idx = np.concatenate([np.random.default_rng(n).integers(0, n, npts), np.arange(n - 64, n)])
+                w_ref, b_ref = oracle.ps_apply_points(W0, h["shards"].numpy(), wl.lr, mu, b0, idx)
+                assert_close(Wg.reshape(-1)[idx], w_ref, W_TOL, spec.name)
+                if b0 is not None:
+                    assert_close(to_np(g["buf"])[idx], b_ref, BUF_TOL, spec.name + " buf")
+
+
+def _to_dev(host, d):
+    out = []
+    for h in host:
+        g = {"spec": h["spec"]}
+        for k in ("W", "U", "V", "shards", "buf"):
+            if k in h:
+                g[k] = h[k].to(d)
+        out.append(g)
+    return out
+
+
+@pytest.mark.parametrize("cfg,streams", [(1, 1), (1, 4), (3, 4), (4, 4), (5, 4), (5, 1), (5, 8)])
+def test_sync_iteration_matches_oracle(cfg, streams):
+    d = dev()
+    wl = I.workload(cfg)
+    host = I.make_tensors(wl)
+    devt = _to_dev(host, d)
+    pool = api.StreamPool(streams)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    log(f"sync_iteration config {cfg} streams={streams} tensors={len(devt)}")
+    schemes = it()
+    torch.cuda.synchronize()
+    _oracle_check(host, devt, wl, schemes)
+    pool.close()
+
+
+def test_sync_iteration_two_iterations_with_fresh_payloads():
+    """Two iterations of the single-FC workload: W and the momentum buffer carry over."""
+    d = dev()
+    wl = I.workload(1)
+    host = I.make_tensors(wl)
+    devt = _to_dev(host, d)
+    pool = api.StreamPool(2)
+    ref = [dict(h) for h in host]
+    for step in range(2):
+        if step:
+            # fresh payloads, same parameters
+            for r, g in zip(ref, devt):
+                for k in ("U", "V", "shards"):
+                    if k in r:
+                        seed = 9000 + 10 * step + {"U": 1, "V": 2, "shards": 3}[k]
+                        r[k] = I.randn(seed, tuple(r[k].shape), 1.0 if k != "shards" else 1e-3)
+                        g[k].copy_(r[k].to(d))
+        it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+        log(f"sync_iteration two-step step={step}")
+        it()
+        torch.cuda.synchronize()
+        outs = oracle.sync_iteration([_oracle_layer(r) for r in ref], wl.B, wl.P, wl.lr, wl.momentum)
+        for r, o in zip(ref, outs):
+            r["W"] = torch.from_numpy(o["W"])
+            if o["buf"] is not None:
+                r["buf"] = torch.from_numpy(o["buf"])
+    for r, g in zip(ref, devt):
+        assert_close(to_np(g["W"]), r["W"].numpy(), W_TOL, r["spec"].name)
+        if "buf" in g:
+            assert_close(to_np(g["buf"]), r["buf"].numpy(), BUF_TOL, r["spec"].name + " buf")
+    pool.close()
+
+
+def _oracle_layer(r):
+    fc = r["spec"].kind == I.FC
+    return {"fc": fc, "W": r["W"].numpy(),
+            "U": r["U"].numpy() if "U" in r else None, "V": r["V"].numpy() if "V" in r else None,
+            "shards": r["shards"].numpy() if "shards" in r else None,
+            "buf": r["buf"].numpy() if r.get("buf") is not None else None}
+
+
+def test_sync_iteration_missing_payload_is_an_error():
+    d = dev()
+    pool = api.StreamPool(2)
+    W = torch.zeros(1024, 512, device=d)
+    # An FC layer that Alg. 1 sends to SFB but that carries only dense shards.
+    t = {"fc": True, "W": W, "shards": torch.zeros(4, 1024 * 512, device=d)}
+    it = api.SyncIteration(pool, [t], B=16, P=4, lr=0.01)
+    with pytest.raises(api.PoseidonError) as e:
+        it()
+    assert e.value.status == api.ERR_PAYLOAD
+    # ... and the same layer at a batch that makes PS cheaper runs through PS.
+    it = api.SyncIteration(pool, [t], B=512, P=4, lr=0.01)
+    assert it() == [api.PS]
+    torch.cuda.synchronize()
+    pool.close()
