@@ -43,6 +43,9 @@ def _parse():
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--cpu-fraction", type=float, default=1.0,
                     help="fraction of each tensor the CPU oracle runs on")
+    ap.add_argument("--calibration-copy-mib", type=int, default=512,
+                    help="size of one plain device copy run before the timed region, whose "
+                         "FETCH_SIZE/WRITE_SIZE counters calibrate the kernels' HBM traffic")
     return ap.parse_args()
 
 
@@ -125,6 +128,14 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] inputs for config {wl.config} ({wl.name}) ready in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)
+
+    if args.calibration_copy_mib > 0:
+        n = args.calibration_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, device=d)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     pool = api.StreamPool(args.streams, device=d)
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)

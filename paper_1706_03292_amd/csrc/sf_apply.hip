@@ -11,10 +11,19 @@
 // Tiling: a workgroup owns a BM x BN block of W and loops over K in steps of
 // BK.  U[k0:k0+BK, m0:m0+BM] and V[k0:k0+BK, n0:n0+BN] are staged through LDS,
 // double-buffered, with the next step's global loads in flight while the
-// matrix cores work on the current one.  Each wave owns a WM x WN sub-block
-// (WM/32 x WN/32 MFMA blocks).  The SGD update is the epilogue: W is read
-// once and written once, straight from the accumulators, so the kernel never
-// materialises the gradient.
+// matrix cores work on the current one, and each wave reads the operand
+// fragments of the next MFMA step while the current one runs.  Each wave owns a
+// WM x WN sub-block (WM/32 x WN/32 MFMA blocks).
+//
+// The SGD update is the epilogue: W is read once and written once, straight
+// from the accumulators, so the gradient is never materialised.  On tiles that
+// lie wholly inside W the epilogue's loads are issued before the last K step
+// (their latency hides behind its MFMAs) and carry no per-element branch.
+//
+// Tile order: the hardware hands consecutive workgroups to the 8 XCDs in turn,
+// and each XCD has its own L2.  Workgroup ids are remapped so that every XCD
+// owns one contiguous run of tiles, walked in groups of GROUP_M tile rows, so
+// the tiles an XCD runs at the same time share U and V panels in its L2.
 #include "common.h"
 
 namespace poseidon {
@@ -22,7 +31,9 @@ namespace {
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 
-constexpr int LDS_PAD = 4;   // floats of padding per LDS row (keeps 16-byte alignment)
+constexpr int LDS_PAD = 4;    // floats of padding per LDS row (keeps 16-byte alignment)
+constexpr int NUM_XCD = 8;    // MI355X: 8 accelerator complex dies, one L2 each
+constexpr int GROUP_M = 8;    // tile rows walked together inside an XCD's run
 
 template <int BM, int BN, int BK, int WM, int WN>
 struct SfTile {
@@ -40,10 +51,10 @@ struct SfTile {
     static_assert(A_V4 * THREADS * 4 == BK * BM && B_V4 * THREADS * 4 == BK * BN, "staging");
 };
 
-// Load one BK x (4*cols4) panel slice of a K-major operand X (row stride ld)
-// into registers: group j of this thread covers row r = g / cols4, columns
-// 4*(g % cols4) .. +3 with g = tid + j*THREADS.  Out-of-range rows/columns
-// read as 0, which adds nothing to the sum.
+// Load one BK x (4*COLS4) slice of a K-major operand X (row length ld = its
+// number of columns) into registers: group j of this thread covers row
+// g / COLS4 and columns 4*(g % COLS4) .. +3 with g = tid + j*THREADS.
+// Out-of-range rows/columns read as 0, which adds nothing to the sum.
 template <int NV4, int COLS4, int THREADS, bool VEC>
 __device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int64_t ld,
                                   int64_t rows, int64_t k0, int64_t c0, int tid)
@@ -77,10 +88,63 @@ __device__ inline void store_panel(float* lds, const f4 (&r)[NV4], int tid)
     }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool VEC>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void sf_apply_kernel(
+// Workgroup id -> (tile row, tile column): contiguous runs per XCD, GROUP_M
+// tile rows at a time inside a run.
+__device__ inline void tile_coords(int bid, int tiles, int tiles_m, int tiles_n, int& tm, int& tn)
+{
+    const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
+    const int x = bid % NUM_XCD, j = bid / NUM_XCD;
+    const int t = x * q + (x < r ? x : r) + j;
+    const int per_group = GROUP_M * tiles_n;
+    const int g = t / per_group;
+    const int first_m = g * GROUP_M;
+    const int rows = (tiles_m - first_m) < GROUP_M ? (tiles_m - first_m) : GROUP_M;
+    const int in = t - g * per_group;
+    tm = first_m + in % rows;
+    tn = in / rows;
+}
+
+// One BK-deep step of the contraction out of LDS: each wave reads its U and V
+// fragments for MFMA step kk+2 while the matrix cores work on step kk.
+template <int BK, int LDA, int LDB, int TM, int TN>
+__device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const float* b_s)
+{
+    float a[2][TM], b[2][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+        a[0][i] = a_s[32 * i];
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+        b[0][j] = b_s[32 * j];
+#pragma unroll
+    for (int kk = 0; kk < BK; kk += 2) {
+        const int c = (kk >> 1) & 1;
+        if (kk + 2 < BK) {
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                a[c ^ 1][i] = a_s[(kk + 2) * LDA + 32 * i];
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                b[c ^ 1][j] = b_s[(kk + 2) * LDB + 32 * j];
+        }
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[c][i], b[c][j], acc[i][j], 0, 0, 0);
+    }
+}
+
+// Buffer resource word 3 for raw (untyped) dword accesses on CDNA.  The raw
+// buffer builtins move 32-bit integers: values are bit-cast, never converted.
+constexpr int BUF_RSRC_WORD3 = 0x00020000;
+
+// EPI: MFMA blocks of W (16 values per lane each) read per epilogue chunk.
+template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int OCC, int EPI>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
-    int64_t M, int64_t N, int64_t K, float lr, int tiles_n)
+    int64_t M, int64_t N, int64_t K, float lr, int tiles_m, int tiles_n, int fast_epilogue)
 {
     using T = SfTile<BM, BN, BK, WM, WN>;
     __shared__ float As[2][BK * T::LDA];
@@ -89,12 +153,17 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void sf_apply_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    const int64_t m0 = static_cast<int64_t>(blockIdx.x / tiles_n) * BM;
-    const int64_t n0 = static_cast<int64_t>(blockIdx.x % tiles_n) * BN;
+    int tm, tn;
+    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
+    const int64_t m0 = static_cast<int64_t>(tm) * BM;
+    const int64_t n0 = static_cast<int64_t>(tn) * BN;
     const int wm = (wave / T::NWN) * WM;
     const int wn = (wave % T::NWN) * WN;
     const int lrow = lane >> 5;        // which of the two k of an MFMA step this lane supplies
     const int lcol = lane & 31;
+    // Interior tiles take the buffer-addressed epilogue (32-bit offsets from
+    // the tile's first element; the host guarantees they fit).
+    const bool interior = fast_epilogue && (m0 + BM <= M) && (n0 + BN <= N);
 
     f16v acc[T::TM][T::TN];
 #pragma unroll
@@ -108,88 +177,133 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void sf_apply_kernel(
     f4 ra[T::A_V4], rb[T::B_V4];
     const int64_t nkt = (K + BK - 1) / BK;
 
-    load_panel<T::A_V4, BM / 4, T::THREADS, VEC>(ra, U, M, K, 0, m0, tid);
-    load_panel<T::B_V4, BN / 4, T::THREADS, VEC>(rb, V, N, K, 0, n0, tid);
+    load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, 0, m0, tid);
+    load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, 0, n0, tid);
     store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[0], ra, tid);
     store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[0], rb, tid);
     __syncthreads();
 
-    for (int64_t kt = 0; kt < nkt; ++kt) {
+    const int a_off = lrow * T::LDA + wm + lcol;
+    const int b_off = lrow * T::LDB + wn + lcol;
+    for (int64_t kt = 0; kt + 1 < nkt; ++kt) {
         const int cur = static_cast<int>(kt & 1);
-        const bool more = kt + 1 < nkt;
-        if (more) {
-            load_panel<T::A_V4, BM / 4, T::THREADS, VEC>(ra, U, M, K, (kt + 1) * BK, m0, tid);
-            load_panel<T::B_V4, BN / 4, T::THREADS, VEC>(rb, V, N, K, (kt + 1) * BK, n0, tid);
-        }
-        const float* a_s = As[cur];
-        const float* b_s = Bs[cur];
-#pragma unroll
-        for (int kk = 0; kk < BK; kk += 2) {
-            float a[T::TM], b[T::TN];
-#pragma unroll
-            for (int i = 0; i < T::TM; ++i)
-                a[i] = a_s[(kk + lrow) * T::LDA + wm + 32 * i + lcol];
-#pragma unroll
-            for (int j = 0; j < T::TN; ++j)
-                b[j] = b_s[(kk + lrow) * T::LDB + wn + 32 * j + lcol];
-#pragma unroll
-            for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-                for (int j = 0; j < T::TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-        if (more) {
-            store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[cur ^ 1], ra, tid);
-            store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[cur ^ 1], rb, tid);
-        }
+        load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, (kt + 1) * BK, m0, tid);
+        load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, (kt + 1) * BK, n0, tid);
+        mma_step<BK, T::LDA, T::LDB>(acc, As[cur] + a_off, Bs[cur] + b_off);
+        store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[cur ^ 1], ra, tid);
+        store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[cur ^ 1], rb, tid);
         __syncthreads();
     }
+    const int last = static_cast<int>((nkt - 1) & 1);
 
     // Epilogue: accumulator register r of lane l holds block row
     // 8*(r/4) + 4*(l/32) + r%4, block column l%32.
+    if (interior) {
+        const int64_t first = m0 * N + n0;
+        const int64_t avail = (M * N - first) * 4;
+        const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
+            W + first, static_cast<short>(0), static_cast<int>(avail < 0x7fffffff ? avail : 0x7fffffff),
+            BUF_RSRC_WORD3);
+        const int voff = ((wm + 4 * lrow) * static_cast<int>(N) + wn + lcol) * 4;
+        const int n4 = static_cast<int>(N) * 4;
+        // W is read in chunks of up to EPI MFMA blocks (16 values per
+        // block and lane, all loads of a chunk in flight together).  With
+        // PREFETCH_W the first chunk's loads are issued before the last step's
+        // MFMAs so that their latency hides behind them.
+        constexpr int NB = T::TM * T::TN;
+        constexpr int CH = NB < EPI ? NB : EPI;
+        static_assert(NB % CH == 0, "epilogue chunking");
 #pragma unroll
-    for (int i = 0; i < T::TM; ++i) {
+        for (int c0 = 0; c0 < NB; c0 += CH) {
+            if (c0 == 0 && !PREFETCH_W)
+                mma_step<BK, T::LDA, T::LDB>(acc, As[last] + a_off, Bs[last] + b_off);
+            float wv[CH][16];
 #pragma unroll
-        for (int j = 0; j < T::TN; ++j) {
-            const int64_t col = n0 + wn + 32 * j + lcol;
+            for (int c = 0; c < CH; ++c) {
+                const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int64_t row = m0 + wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
-                if (row < M && col < N) {
-                    float* w = W + row * N + col;
-                    *w = fmaf(-lr, acc[i][j][r], *w);
+                for (int r = 0; r < 16; ++r)
+                    wv[c][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                        wr, voff, (32 * i + 8 * (r >> 2) + (r & 3)) * n4 + 128 * j, 0));
+            }
+            if (c0 == 0 && PREFETCH_W)
+                mma_step<BK, T::LDA, T::LDB>(acc, As[last] + a_off, Bs[last] + b_off);
+#pragma unroll
+            for (int c = 0; c < CH; ++c) {
+                const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    __builtin_amdgcn_raw_buffer_store_b32(
+                        __builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], wv[c][r])), wr, voff,
+                        (32 * i + 8 * (r >> 2) + (r & 3)) * n4 + 128 * j, 0);
+            }
+        }
+    } else {
+        mma_step<BK, T::LDA, T::LDB>(acc, As[last] + a_off, Bs[last] + b_off);
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j) {
+                const int64_t col = n0 + wn + 32 * j + lcol;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int64_t row = m0 + wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                    if (row < M && col < N) {
+                        float* w = W + row * N + col;
+                        *w = fmaf(-lr, acc[i][j][r], *w);
+                    }
                 }
             }
         }
     }
 }
 
-template <int BM, int BN, int BK, int WM, int WN>
-hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
-                      float lr, bool vec, hipStream_t stream)
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, bool VA, bool VB>
+void launch_kernel(int tiles, int tiles_m, int tiles_n, float* W, const float* U, const float* V,
+                   int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
 {
-    using T = SfTile<BM, BN, BK, WM, WN>;
+    // The buffer-addressed epilogue needs every byte offset inside a tile,
+    // ((BM-1)*N + BN) * 4, to fit in a signed 32-bit offset.
+    const int fast = (static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL;
+    sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI><<<tiles, SfTile<BM, BN, BK, WM, WN>::THREADS, 0, stream>>>(
+        W, U, V, M, N, K, lr, tiles_m, tiles_n, fast);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4>
+hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
+                      float lr, hipStream_t stream)
+{
     const int64_t tiles_m = (M + BM - 1) / BM;
     const int64_t tiles_n = (N + BN - 1) / BN;
     const int64_t tiles = tiles_m * tiles_n;
-    if (tiles > INT32_MAX || tiles_n > INT32_MAX)
+    if (tiles > INT32_MAX)
         return hipErrorInvalidValue;
-    if (vec)
-        sf_apply_kernel<BM, BN, BK, WM, WN, true><<<static_cast<int>(tiles), T::THREADS, 0, stream>>>(
-            W, U, V, M, N, K, lr, static_cast<int>(tiles_n));
+    const bool va = (M % 4 == 0) && aligned16(U);
+    const bool vb = (N % 4 == 0) && aligned16(V);
+    const int t = static_cast<int>(tiles), tmi = static_cast<int>(tiles_m), tni = static_cast<int>(tiles_n);
+    if (va && vb)
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+    else if (va)
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+    else if (vb)
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else
-        sf_apply_kernel<BM, BN, BK, WM, WN, false><<<static_cast<int>(tiles), T::THREADS, 0, stream>>>(
-            W, U, V, M, N, K, lr, static_cast<int>(tiles_n));
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     return hipGetLastError();
 }
 
 }  // namespace
 
+// Tile choice: 128 x 128 workgroup tiles (64 x 64 per wave, W prefetched,
+// 3 waves per SIMD) when the layer has at least two such tiles per CU;
+// otherwise 64 x 64 tiles so that small layers still fill the chip.
 hipError_t launch_sf_apply(float* W, const float* U, const float* V,
                            int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
 {
-    const bool vec = (M % 4 == 0) && (N % 4 == 0) && aligned16(U) && aligned16(V);
-    return launch_cfg<128, 128, 16, 64, 64>(W, U, V, M, N, K, lr, vec, stream);
+    const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
+        return launch_cfg<128, 128, 16, 64, 64, true, 3, 1>(W, U, V, M, N, K, lr, stream);
+    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1>(W, U, V, M, N, K, lr, stream);
 }
 
 int check_sf_args(const float* W, const float* U, const float* V,

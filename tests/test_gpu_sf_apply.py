@@ -33,6 +33,11 @@ SHAPES = [
     (261, 387, 18),
     (1000, 2048, 1024),  # the Inception-shaped classifier, K = 32 x 32
     (517, 515, 513),
+    # Large enough for the 128 x 128 workgroup tiles (>= 2 tiles per CU), with
+    # ragged tails, dimensions not divisible by 4 and a ragged K.
+    (2085, 4125, 40),
+    (2049, 4099, 17),
+    (4100, 2052, 100),
 ]
 
 
@@ -62,7 +67,7 @@ def test_sf_raw_gradient_matches_oracle(M, N, K):
     assert_close(to_np(Wd), ref, DELTA_TOL, f"dW {M}x{N} K={K}")
 
 
-@pytest.mark.parametrize("M,N,K", [(256, 384, 40), (203, 129, 17), (1024, 512, 64)])
+@pytest.mark.parametrize("M,N,K", [(256, 384, 40), (203, 129, 17), (1024, 512, 64), (2052, 4100, 24)])
 def test_sf_apply_misaligned_pointers(M, N, K):
     d = dev()
     W, U, V = _draw(M, N, K, seed=99 + M)
