@@ -63,6 +63,34 @@ def _ps_bytes(spec, P, momentum: bool):
     return float(spec.numel) * (4 * P + (16 if momentum else 8))
 
 
+def _kernel_source_hash(name: str) -> str:
+    import hashlib
+    path = os.path.join(ROOT, "paper_1706_03292_amd", "csrc", name)
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def _stored_traffic(kernel: str, source: str):
+    """HBM bytes per step of `kernel` from the committed rocprofv3 counter
+    summaries under profiles/ (lines 'traffic: kernel=... source_sha256=...
+    bytes_per_step=...'), or None when no summary matches the current source
+    of that kernel (the counters were taken on different code)."""
+    want = _kernel_source_hash(source)
+    pdir = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(pdir):
+        return None
+    for fn in sorted(os.listdir(pdir)):
+        if not fn.endswith((".md", ".txt")):
+            continue
+        for line in open(os.path.join(pdir, fn)):
+            line = line.strip().strip("`")
+            if not line.startswith("traffic:"):
+                continue
+            kv = dict(x.split("=", 1) for x in line[len("traffic:"):].split() if "=" in x)
+            if kv.get("kernel") == kernel and kv.get("source_sha256") == want:
+                return float(kv["bytes_per_step"])
+    return None
+
+
 def _cpu_baseline(wl, host, fraction):
     """The oracle (as is) on the first `fraction` of every tensor of the
     workload, scaled to one whole iteration."""
@@ -95,9 +123,10 @@ def _cpu_baseline(wl, host, fraction):
         "unit": "ms",
         "cores": oracle.num_threads(),
         "kind": "oracle",
-        "sample": (f"first {fraction:.4g} of the rows of each SFB layer and of the elements of each "
-                   f"PS tensor of the same iteration ({t_sfb + t_ps:.1f} s measured: SFB {t_sfb:.2f} s, "
-                   f"PS {t_ps:.2f} s), scaled by work to one whole iteration"),
+        "sample": ((f"the whole iteration once (all {len(host)} tensors)" if fraction >= 1.0 else
+                    f"the first {fraction:.4g} of the rows of each SFB layer and of the elements of each "
+                    f"PS tensor of the same iteration, scaled by work to one whole iteration")
+                   + f"; {t_sfb + t_ps:.1f} s measured: SFB {t_sfb:.2f} s, PS {t_ps:.2f} s"),
     }
 
 
@@ -170,11 +199,32 @@ def main():
     torch.cuda.synchronize()
     avg = [s / ksteps for s in sums]
 
+    # The PS kernels share the GPU with the SF reconstructions during the
+    # iteration (by design), so their bandwidth is measured in a phase of its
+    # own: every PS tensor of the step, one after another on one stream, with
+    # HIP events around each launch on that stream.
+    ps_iso_ms = [0.0] * len(devt)
+    for rep in range(ksteps + 1):
+        evs = []
+        for i in range(len(devt) - 1, -1, -1):
+            t = devt[i]
+            if t["spec"].kind == "fc":
+                continue
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            api.ps_apply(t["W"].view(-1), t["shards"], wl.lr, wl.momentum, t.get("buf"), stream=stream)
+            b.record(stream)
+            evs.append((i, a, b))
+        torch.cuda.synchronize()
+        if rep > 0:                       # first pass is a warm-up
+            for i, a, b in evs:
+                ps_iso_ms[i] += a.elapsed_time(b) / ksteps
+
     sfb_flops = sfb_ms = sfb_bytes = 0.0
-    ps_bytes = ps_ms = 0.0
+    ps_bytes = ps_ms = ps_ms_in_iter = 0.0
     layers = []
     big_ps = None
-    for h, sch, ms in zip(host, schemes, avg):
+    for h, sch, ms, ms_iso in zip(host, schemes, avg, ps_iso_ms):
         spec = h["spec"]
         if sch == api.SFB:
             f = _sf_flops(spec, wl.K)
@@ -186,9 +236,10 @@ def main():
         else:
             b = _ps_bytes(spec, wl.P, "buf" in h)
             ps_bytes += b
-            ps_ms += ms
+            ps_ms += ms_iso
+            ps_ms_in_iter += ms
             if big_ps is None or spec.numel > big_ps[0]:
-                big_ps = (spec.numel, spec.name, b, ms)
+                big_ps = (spec.numel, spec.name, b, ms_iso)
     sfb_tflops = sfb_flops / sfb_ms / 1e9 if sfb_ms else None
     ps_gbs = ps_bytes / ps_ms / 1e6 if ps_ms else None
     big_gbs = big_ps[2] / big_ps[3] / 1e6 if big_ps else None
@@ -213,7 +264,7 @@ def main():
                      "achieved": round(sfb_tflops, 2) if sfb_tflops else None,
                      "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(sfb_tflops / PEAK_FP32_MFMA_TFLOPS, 4) if sfb_tflops else None,
-                     "traffic": None,
+                     "traffic": _stored_traffic("sf_apply", "sf_apply.hip"),
                      "work": f"2*M*N*K flops over the {sum(1 for s in schemes if s == api.SFB)} SFB "
                              f"launches of one step ({sfb_flops / 1e9:.1f} GFLOP) / their summed "
                              f"average durations ({sfb_ms:.4f} ms)"},
@@ -221,11 +272,14 @@ def main():
                         "achieved": round(ps_gbs, 1) if ps_gbs else None,
                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(ps_gbs / PEAK_HBM_GBS, 4) if ps_gbs else None,
-                        "traffic": None,
+                        "traffic": _stored_traffic("ps_apply", "ps_apply.hip"),
                         "largest_tensor": {"tensor": big_ps[1], "gbs": round(big_gbs, 1),
                                            "ms": round(big_ps[3], 4)} if big_ps else None,
                         "work": f"(4P+16) bytes per element over all PS launches of one step "
-                                f"({ps_bytes / 1e9:.3f} GB) / summed average durations ({ps_ms:.4f} ms)"},
+                                f"({ps_bytes / 1e9:.3f} GB) / their summed average durations "
+                                f"({ps_ms:.4f} ms) when launched one after another on one stream "
+                                f"with nothing else running (inside the iteration they overlap the "
+                                f"SF reconstructions: summed {ps_ms_in_iter:.4f} ms)"},
         "event_ms_per_step": round(event_ms, 4),
         "sfb_tflops": round(sfb_tflops, 2) if sfb_tflops else None,
         "ps_gbs": round(ps_gbs, 1) if ps_gbs else None,

@@ -160,8 +160,11 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation"; Alg. 2 TRAIN/sync): tensors[] is given in forward order
  * and issued from the last to the first (backpropagation order).  For each
  * tensor the scheme is Alg. 1's (FC: poseidon_hybcomm_choose(M, N, B, P);
- * other kinds: PS) and its update is enqueued on the next pool stream in turn:
- * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
+ * other kinds: PS) and its update is enqueued on a pool stream: every SFB
+ * update on the first stream (they are bound by the matrix cores), the PS
+ * updates round-robin on the others (bound by memory bandwidth), so that the
+ * two kinds overlap; a one-stream pool runs everything in order.  SFB tensors
+ * take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
  * poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf) (momentum is used
  * only when buf != NULL).  Every pool stream first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so

@@ -181,6 +181,11 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
     if (active == 0)
         return POSEIDON_OK;
 
+    // Stream assignment: the compute-bound SF reconstructions go, in
+    // backpropagation order, to the pool's first stream; the bandwidth-bound
+    // PS applies go round-robin to the others, so the two kinds overlap on the
+    // GPU instead of queueing behind each other.  A one-stream pool serialises
+    // everything.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
     const int32_t used = active < S ? active : S;
     if (hipEventRecord(pool->fork, stream) != hipSuccess)
@@ -189,7 +194,6 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
         if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
             return POSEIDON_ERR_HIP;
 
-    // Backpropagation order: the last tensor's gradient is ready first.
     int32_t q = 0;
     for (int32_t t = count - 1; t >= 0; --t) {
         const poseidon_tensor& x = tensors[t];
@@ -197,7 +201,10 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
         const bool sfb = plan[static_cast<size_t>(t)] == POSEIDON_SFB;
         if (n == 0 || (sfb && K == 0))
             continue;
-        hipStream_t s = pool->streams[q % used];
+        int32_t si = 0;
+        if (used > 1 && !sfb)
+            si = 1 + (q++ % (used - 1));
+        hipStream_t s = pool->streams[si];
         if (pool->timing && hipEventRecord(pool->t_start[t], s) != hipSuccess)
             return POSEIDON_ERR_HIP;
         const hipError_t err =
@@ -210,7 +217,6 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
                 return POSEIDON_ERR_HIP;
             pool->t_ran[static_cast<size_t>(t)] = 1;
         }
-        ++q;
     }
 
     for (int32_t s = 0; s < used; ++s) {
