@@ -105,8 +105,10 @@ __device__ inline void tile_coords(int bid, int tiles, int tiles_m, int tiles_n,
 }
 
 // One BK-deep step of the contraction out of LDS: each wave reads its U and V
-// fragments for MFMA step kk+2 while the matrix cores work on step kk.
-template <int BK, int LDA, int LDB, int TM, int TN>
+// fragments for MFMA step kk+2 while the matrix cores work on step kk.  With
+// FENCE the order is pinned with scheduling barriers (the compiler otherwise
+// sinks the reads below the MFMAs and waits on them at once).
+template <int BK, int LDA, int LDB, int TM, int TN, bool FENCE>
 __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const float* b_s)
 {
     float a[2][TM], b[2][TN];
@@ -127,11 +129,15 @@ __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const flo
             for (int j = 0; j < TN; ++j)
                 b[c ^ 1][j] = b_s[(kk + 2) * LDB + 32 * j];
         }
+        if constexpr (FENCE)
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[c][i], b[c][j], acc[i][j], 0, 0, 0);
+        if constexpr (FENCE)
+            __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -140,11 +146,12 @@ __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const flo
 constexpr int BUF_RSRC_WORD3 = 0x00020000;
 
 // EPI: MFMA blocks of W (16 values per lane each) read per epilogue chunk.
-template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int OCC, int EPI>
+template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int OCC, int EPI,
+          bool FENCE, bool HUGE_N>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
-    int64_t M, int64_t N, int64_t K, float lr, int tiles_m, int tiles_n, int fast_epilogue)
+    int64_t M, int64_t N, int64_t K, float lr, int tiles_m, int tiles_n)
 {
     using T = SfTile<BM, BN, BK, WM, WN>;
     __shared__ float As[2][BK * T::LDA];
@@ -161,9 +168,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     const int wn = (wave % T::NWN) * WN;
     const int lrow = lane >> 5;        // which of the two k of an MFMA step this lane supplies
     const int lcol = lane & 31;
-    // Interior tiles take the buffer-addressed epilogue (32-bit offsets from
-    // the tile's first element; the host guarantees they fit).
-    const bool interior = fast_epilogue && (m0 + BM <= M) && (n0 + BN <= N);
+    const bool interior = (m0 + BM <= M) && (n0 + BN <= N);
 
     f16v acc[T::TM][T::TN];
 #pragma unroll
@@ -189,7 +194,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
         const int cur = static_cast<int>(kt & 1);
         load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, (kt + 1) * BK, m0, tid);
         load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, (kt + 1) * BK, n0, tid);
-        mma_step<BK, T::LDA, T::LDB>(acc, As[cur] + a_off, Bs[cur] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, FENCE>(acc, As[cur] + a_off, Bs[cur] + b_off);
         store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[cur ^ 1], ra, tid);
         store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[cur ^ 1], rb, tid);
         __syncthreads();
@@ -198,48 +203,95 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
 
     // Epilogue: accumulator register r of lane l holds block row
     // 8*(r/4) + 4*(l/32) + r%4, block column l%32.
-    if (interior) {
+    if constexpr (!HUGE_N) {
+        // Buffer-addressed epilogue: byte offsets from the tile's first
+        // element fit in 31 bits (the host picks HUGE_N otherwise).
         const int64_t first = m0 * N + n0;
         const int64_t avail = (M * N - first) * 4;
         const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
             W + first, static_cast<short>(0), static_cast<int>(avail < 0x7fffffff ? avail : 0x7fffffff),
             BUF_RSRC_WORD3);
-        const int voff = ((wm + 4 * lrow) * static_cast<int>(N) + wn + lcol) * 4;
-        const int n4 = static_cast<int>(N) * 4;
-        // W is read in chunks of up to EPI MFMA blocks (16 values per
-        // block and lane, all loads of a chunk in flight together).  With
-        // PREFETCH_W the first chunk's loads are issued before the last step's
-        // MFMAs so that their latency hides behind them.
+        const int ni = static_cast<int>(N);
+        const int voff = ((wm + 4 * lrow) * ni + wn + lcol) * 4;
+        const int n4 = ni * 4;
         constexpr int NB = T::TM * T::TN;
         constexpr int CH = NB < EPI ? NB : EPI;
         static_assert(NB % CH == 0, "epilogue chunking");
-#pragma unroll
-        for (int c0 = 0; c0 < NB; c0 += CH) {
-            if (c0 == 0 && !PREFETCH_W)
-                mma_step<BK, T::LDA, T::LDB>(acc, As[last] + a_off, Bs[last] + b_off);
-            float wv[CH][16];
+        // W is read in chunks of up to EPI MFMA blocks (16 values per block
+        // and lane, all loads of a chunk in flight together).  Interior tiles
+        // use one shared lane offset and uniform row offsets; with PREFETCH_W
+        // their first chunk is loaded before the last step's MFMAs so that the
+        // latency hides behind them.
+        float wv[CH][16];
+        if (PREFETCH_W && interior) {
 #pragma unroll
             for (int c = 0; c < CH; ++c) {
-                const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
+                const int i = c / T::TN, j = c % T::TN;
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     wv[c][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                        wr, voff, (32 * i + 8 * (r >> 2) + (r & 3)) * n4 + 128 * j, 0));
+                        wr, voff + 128 * j, (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0));
             }
-            if (c0 == 0 && PREFETCH_W)
-                mma_step<BK, T::LDA, T::LDB>(acc, As[last] + a_off, Bs[last] + b_off);
+        }
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, FENCE>(acc, As[last] + a_off, Bs[last] + b_off);
+        if (interior) {
 #pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
+            for (int c0 = 0; c0 < NB; c0 += CH) {
+                if (c0 > 0 || !PREFETCH_W) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    __builtin_amdgcn_raw_buffer_store_b32(
-                        __builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], wv[c][r])), wr, voff,
-                        (32 * i + 8 * (r >> 2) + (r & 3)) * n4 + 128 * j, 0);
+                    for (int c = 0; c < CH; ++c) {
+                        const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
+#pragma unroll
+                        for (int r = 0; r < 16; ++r)
+                            wv[c][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                wr, voff + 128 * j, (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0));
+                    }
+                }
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        __builtin_amdgcn_raw_buffer_store_b32(
+                            __builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], wv[c][r])), wr, voff + 128 * j,
+                            (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0);
+                }
+            }
+        } else {
+            // Ragged edge tile: every element gets its own lane offset; an
+            // element outside W loads the tile's first element instead (always
+            // inside W, value unused) and is not stored.
+            const int rows_left = static_cast<int>(M - m0 < BM ? M - m0 : BM);
+            const int cols_left = static_cast<int>(N - n0 < BN ? N - n0 : BN);
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j) {
+                    const int col = wn + 32 * j + lcol;
+                    float ev[16];
+                    int off[16];
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                        off[r] = (row < rows_left && col < cols_left) ? (row * ni + col) * 4 : 0;
+                        ev[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wr, off[r], 0, 0));
+                    }
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                        if (row < rows_left && col < cols_left)
+                            __builtin_amdgcn_raw_buffer_store_b32(
+                                __builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], ev[r])), wr, off[r], 0, 0);
+                    }
+                    // One MFMA block at a time: keeps the scheduler from
+                    // hoisting every block's loads and offsets together.
+                    __builtin_amdgcn_sched_barrier(0);
+                }
             }
         }
     } else {
-        mma_step<BK, T::LDA, T::LDB>(acc, As[last] + a_off, Bs[last] + b_off);
+        // Rows so long that tile offsets need 64 bits: plain guarded accesses.
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, FENCE>(acc, As[last] + a_off, Bs[last] + b_off);
 #pragma unroll
         for (int i = 0; i < T::TM; ++i) {
 #pragma unroll
@@ -258,18 +310,22 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, bool VA, bool VB>
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, bool FENCE, bool VA, bool VB>
 void launch_kernel(int tiles, int tiles_m, int tiles_n, float* W, const float* U, const float* V,
                    int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
 {
     // The buffer-addressed epilogue needs every byte offset inside a tile,
     // ((BM-1)*N + BN) * 4, to fit in a signed 32-bit offset.
-    const int fast = (static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL;
-    sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI><<<tiles, SfTile<BM, BN, BK, WM, WN>::THREADS, 0, stream>>>(
-        W, U, V, M, N, K, lr, tiles_m, tiles_n, fast);
+    constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
+    if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
+        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, FENCE, false><<<tiles, NT, 0, stream>>>(
+            W, U, V, M, N, K, lr, tiles_m, tiles_n);
+    else
+        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, FENCE, true><<<tiles, NT, 0, stream>>>(
+            W, U, V, M, N, K, lr, tiles_m, tiles_n);
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4>
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4, bool FENCE = false>
 hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
                       float lr, hipStream_t stream)
 {
@@ -282,28 +338,28 @@ hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64
     const bool vb = (N % 4 == 0) && aligned16(V);
     const int t = static_cast<int>(tiles), tmi = static_cast<int>(tiles_m), tni = static_cast<int>(tiles_n);
     if (va && vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else if (va)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else if (vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     return hipGetLastError();
 }
 
 }  // namespace
 
 // Tile choice: 128 x 128 workgroup tiles (64 x 64 per wave, W prefetched,
-// 3 waves per SIMD) when the layer has at least two such tiles per CU;
+// 4 waves per SIMD) when the layer has at least two such tiles per CU;
 // otherwise 64 x 64 tiles so that small layers still fill the chip.
 hipError_t launch_sf_apply(float* W, const float* U, const float* V,
                            int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
 {
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
     if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_cfg<128, 128, 16, 64, 64, true, 3, 1>(W, U, V, M, N, K, lr, stream);
-    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1>(W, U, V, M, N, K, lr, stream);
+        return launch_cfg<128, 128, 16, 64, 64, true, 4, 1, false>(W, U, V, M, N, K, lr, stream);
+    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, false>(W, U, V, M, N, K, lr, stream);
 }
 
 int check_sf_args(const float* W, const float* U, const float* V,
