@@ -187,46 +187,44 @@ def main():
           file=sys.stderr, flush=True)
 
     # Per-kernel durations for the roofline: the same iteration, same streams,
-    # with the library's per-tensor timing events on the streams the kernels run on.
+    # with the library's timing events around each launch on its own stream.
     ksteps = args.kernel_steps or args.steps
     pool.set_timing(True)
-    sums = [0.0] * len(devt)
+    sfb_t = {}
+    ps_batch_in_iter = 0.0
     for _ in range(ksteps):
         it(stream)
-        for i, ms in enumerate(pool.tensor_times(len(devt))):
-            sums[i] += ms
+        for r in pool.launch_times():
+            if r["scheme"] == api.SFB:
+                sfb_t[r["tensor"]] = sfb_t.get(r["tensor"], 0.0) + r["ms"] / ksteps
+            else:
+                ps_batch_in_iter += r["ms"] / ksteps
     pool.set_timing(False)
     torch.cuda.synchronize()
-    avg = [s / ksteps for s in sums]
 
-    # The PS kernels share the GPU with the SF reconstructions during the
-    # iteration (by design), so their bandwidth is measured in a phase of its
-    # own: every PS tensor of the step, one after another on one stream, with
-    # HIP events around each launch on that stream.
-    ps_iso_ms = [0.0] * len(devt)
+    # The PS pass shares the GPU with the SF reconstructions during the
+    # iteration (by design), so its bandwidth is measured in a phase of its
+    # own: the same batched pass over every PS tensor of the step, alone on one
+    # stream, between HIP events on that stream.
+    ps_list = [(t["W"], t["shards"], t.get("buf")) for t in reversed(devt) if t["spec"].kind != "fc"]
+    ps_iso = []
     for rep in range(ksteps + 1):
-        evs = []
-        for i in range(len(devt) - 1, -1, -1):
-            t = devt[i]
-            if t["spec"].kind == "fc":
-                continue
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            api.ps_apply(t["W"].view(-1), t["shards"], wl.lr, wl.momentum, t.get("buf"), stream=stream)
-            b.record(stream)
-            evs.append((i, a, b))
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream)
+        b.record(stream)
         torch.cuda.synchronize()
-        if rep > 0:                       # first pass is a warm-up
-            for i, a, b in evs:
-                ps_iso_ms[i] += a.elapsed_time(b) / ksteps
+        if rep > 0:                       # the first pass is a warm-up
+            ps_iso.append(a.elapsed_time(b))
+    ps_ms = sum(ps_iso) / len(ps_iso)
 
     sfb_flops = sfb_ms = sfb_bytes = 0.0
-    ps_bytes = ps_ms = ps_ms_in_iter = 0.0
+    ps_bytes = 0.0
     layers = []
-    big_ps = None
-    for h, sch, ms, ms_iso in zip(host, schemes, avg, ps_iso_ms):
+    for i, (h, sch) in enumerate(zip(host, schemes)):
         spec = h["spec"]
         if sch == api.SFB:
+            ms = sfb_t[i]
             f = _sf_flops(spec, wl.K)
             sfb_flops += f
             sfb_bytes += _sf_bytes(spec, wl.K)
@@ -234,15 +232,10 @@ def main():
             layers.append({"tensor": spec.name, "scheme": "SFB", "ms": round(ms, 4),
                            "tflops": round(f / ms / 1e9, 2)})
         else:
-            b = _ps_bytes(spec, wl.P, "buf" in h)
-            ps_bytes += b
-            ps_ms += ms_iso
-            ps_ms_in_iter += ms
-            if big_ps is None or spec.numel > big_ps[0]:
-                big_ps = (spec.numel, spec.name, b, ms_iso)
+            ps_bytes += _ps_bytes(spec, wl.P, "buf" in h)
     sfb_tflops = sfb_flops / sfb_ms / 1e9 if sfb_ms else None
     ps_gbs = ps_bytes / ps_ms / 1e6 if ps_ms else None
-    big_gbs = big_ps[2] / big_ps[3] / 1e6 if big_ps else None
+    n_ps = sum(1 for s_ in schemes if s_ == api.PS)
 
     result = {
         "metric": METRIC,
@@ -268,18 +261,15 @@ def main():
                      "work": f"2*M*N*K flops over the {sum(1 for s in schemes if s == api.SFB)} SFB "
                              f"launches of one step ({sfb_flops / 1e9:.1f} GFLOP) / their summed "
                              f"average durations ({sfb_ms:.4f} ms)"},
-        "roofline_ps": {"bound": "hbm", "kernel": "ps_apply",
+        "roofline_ps": {"bound": "hbm", "kernel": "ps_apply_batch",
                         "achieved": round(ps_gbs, 1) if ps_gbs else None,
                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(ps_gbs / PEAK_HBM_GBS, 4) if ps_gbs else None,
                         "traffic": _stored_traffic("ps_apply", "ps_apply.hip"),
-                        "largest_tensor": {"tensor": big_ps[1], "gbs": round(big_gbs, 1),
-                                           "ms": round(big_ps[3], 4)} if big_ps else None,
-                        "work": f"(4P+16) bytes per element over all PS launches of one step "
-                                f"({ps_bytes / 1e9:.3f} GB) / their summed average durations "
-                                f"({ps_ms:.4f} ms) when launched one after another on one stream "
-                                f"with nothing else running (inside the iteration they overlap the "
-                                f"SF reconstructions: summed {ps_ms_in_iter:.4f} ms)"},
+                        "work": f"(4P+16) bytes per element over the {n_ps} PS tensors of one step "
+                                f"({ps_bytes / 1e9:.3f} GB) / the average duration of their batched "
+                                f"pass alone on one stream ({ps_ms:.4f} ms); inside the iteration the "
+                                f"same pass overlaps the SF reconstructions and takes {ps_batch_in_iter:.4f} ms"},
         "event_ms_per_step": round(event_ms, 4),
         "sfb_tflops": round(sfb_tflops, 2) if sfb_tflops else None,
         "ps_gbs": round(ps_gbs, 1) if ps_gbs else None,

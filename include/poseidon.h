@@ -97,6 +97,28 @@ int poseidon_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
                       float lr, float momentum, float* buf,
                       hipStream_t stream);
 
+/* One dense tensor of a batched parameter-server apply. */
+typedef struct poseidon_ps_tensor {
+    float*       W;       /* n values, updated in place */
+    const float* shards;  /* P x n, shard p at offset p*n */
+    float*       buf;     /* momentum buffer (n values) or NULL for plain SGD */
+    int64_t      n;
+} poseidon_ps_tensor;
+
+/*
+ * poseidon_ps_apply for many tensors at once: a KV store applying every pair
+ * it received in one pass (Sec. 4.1 "KV Store").  Each tensor is updated
+ * exactly as by poseidon_ps_apply(W, shards, P, n, lr, buf ? momentum : 0,
+ * buf); tensors with n = 0 are skipped.  The work is issued as one launch per
+ * group of up to 48 tensors of the same kind (with / without buffer), so that
+ * small tensors do not each pay a kernel launch.  All tensors are validated
+ * before anything is enqueued.  Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG
+ * (as for poseidon_ps_apply, for any tensor; count < 0; NULL tensors with
+ * count > 0) or POSEIDON_ERR_HIP.
+ */
+int poseidon_ps_apply_batch(const poseidon_ps_tensor* tensors, int32_t count, int32_t P,
+                            float lr, float momentum, hipStream_t stream);
+
 /*
  * Coordinator.BestScheme for a fully-connected M x N layer (Alg. 1; Table 1)
  * on a cluster of P nodes that are each both worker and server (P1 = P2 = P),
@@ -160,11 +182,12 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation"; Alg. 2 TRAIN/sync): tensors[] is given in forward order
  * and issued from the last to the first (backpropagation order).  For each
  * tensor the scheme is Alg. 1's (FC: poseidon_hybcomm_choose(M, N, B, P);
- * other kinds: PS) and its update is enqueued on a pool stream: every SFB
- * update on the first stream (they are bound by the matrix cores), the PS
- * updates round-robin on the others (bound by memory bandwidth), so that the
- * two kinds overlap; a one-stream pool runs everything in order.  SFB tensors
- * take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
+ * other kinds: PS).  The SFB updates (bound by the matrix cores) are
+ * enqueued one per tensor on the pool's first stream; the PS updates (bound
+ * by memory bandwidth) are enqueued as one batched pass over all PS tensors
+ * (poseidon_ps_apply_batch, backpropagation order) on the second stream, so
+ * that the two kinds overlap; a one-stream pool runs everything in order.
+ * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
  * poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf) (momentum is used
  * only when buf != NULL).  Every pool stream first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so
@@ -181,22 +204,30 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
                             hipStream_t stream, int32_t* schemes);
 
 /*
- * Per-tensor timing (the per-layer synchronisation times the paper's
- * evaluation reasons about, Sec. 5).  While enabled (default: off), every
- * update that poseidon_sync_iteration enqueues is bracketed by two timing
- * events on the stream it runs on.  Returns POSEIDON_OK,
- * POSEIDON_ERR_INVALID_ARG or POSEIDON_ERR_HIP.
+ * Launch timing (the per-layer synchronisation times the paper's evaluation
+ * reasons about, Sec. 5).  While enabled (default: off), every launch that
+ * poseidon_sync_iteration enqueues is bracketed by two timing events on the
+ * stream it runs on.  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG.
  */
 int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 
+/* One launch of the last iteration run with timing enabled. */
+typedef struct poseidon_launch_record {
+    int32_t scheme;   /* POSEIDON_SFB (one tensor) or POSEIDON_PS (the batch of all PS tensors) */
+    int32_t tensor;   /* index into that call's tensors[] for SFB, -1 for the PS batch */
+    int32_t stream;   /* pool stream index */
+    float   ms;       /* time between the events around the launch */
+} poseidon_launch_record;
+
 /*
- * Elapsed milliseconds of each tensor's update in the last iteration run with
- * timing enabled: ms[t] for tensors[t] of that call (count entries); -1 for a
- * tensor with no work.  Blocks until that iteration's updates have finished.
- * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (no timed iteration yet, count
- * different from that iteration's) or POSEIDON_ERR_HIP.
+ * Copies the launch records of the last timed iteration, in issue order, into
+ * records[0 .. *count), waiting for those launches to finish.  *count is set
+ * even when capacity is too small (then POSEIDON_ERR_INVALID_ARG).  Returns
+ * POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (no timed iteration yet, capacity too
+ * small, NULL pointers) or POSEIDON_ERR_HIP.
  */
-int poseidon_pool_tensor_times(poseidon_stream_pool* pool, float* ms, int32_t count);
+int poseidon_pool_launch_times(poseidon_stream_pool* pool, poseidon_launch_record* records,
+                               int32_t capacity, int32_t* count);
 
 /* Library version, for the binding's load check: returns POSEIDON_ABI_VERSION. */
 #define POSEIDON_ABI_VERSION 1

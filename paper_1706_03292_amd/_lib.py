@@ -20,10 +20,10 @@ SFB = 1
 KIND_FC = 0
 KIND_OTHER = 1
 
-EXPORTS = ("poseidon_sf_apply", "poseidon_ps_apply", "poseidon_hybcomm_choose",
-           "poseidon_hybcomm_cost", "poseidon_pool_create", "poseidon_pool_destroy",
-           "poseidon_sync_iteration", "poseidon_pool_set_timing", "poseidon_pool_tensor_times",
-           "poseidon_abi_version")
+EXPORTS = ("poseidon_sf_apply", "poseidon_ps_apply", "poseidon_ps_apply_batch",
+           "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_pool_create",
+           "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_pool_set_timing",
+           "poseidon_pool_launch_times", "poseidon_abi_version")
 
 
 class PoseidonTensor(ctypes.Structure):
@@ -32,6 +32,18 @@ class PoseidonTensor(ctypes.Structure):
                 ("W", ctypes.c_void_p), ("M", ctypes.c_int64), ("N", ctypes.c_int64),
                 ("U", ctypes.c_void_p), ("V", ctypes.c_void_p),
                 ("shards", ctypes.c_void_p), ("buf", ctypes.c_void_p)]
+
+
+class PoseidonPsTensor(ctypes.Structure):
+    """Mirror of ``poseidon_ps_tensor`` in include/poseidon.h."""
+    _fields_ = [("W", ctypes.c_void_p), ("shards", ctypes.c_void_p), ("buf", ctypes.c_void_p),
+                ("n", ctypes.c_int64)]
+
+
+class PoseidonLaunchRecord(ctypes.Structure):
+    """Mirror of ``poseidon_launch_record`` in include/poseidon.h."""
+    _fields_ = [("scheme", ctypes.c_int32), ("tensor", ctypes.c_int32), ("stream", ctypes.c_int32),
+                ("ms", ctypes.c_float)]
 
 
 _lib = None
@@ -54,8 +66,10 @@ def lib() -> ctypes.CDLL:
     L.poseidon_pool_destroy.argtypes = [vp]
     L.poseidon_sync_iteration.argtypes = [vp, ctypes.POINTER(PoseidonTensor), i32, i64, i32,
                                           f32, f32, vp, ctypes.POINTER(i32)]
+    L.poseidon_ps_apply_batch.argtypes = [ctypes.POINTER(PoseidonPsTensor), i32, i32, f32, f32, vp]
     L.poseidon_pool_set_timing.argtypes = [vp, i32]
-    L.poseidon_pool_tensor_times.argtypes = [vp, ctypes.POINTER(f32), i32]
+    L.poseidon_pool_launch_times.argtypes = [vp, ctypes.POINTER(PoseidonLaunchRecord), i32,
+                                             ctypes.POINTER(i32)]
     L.poseidon_abi_version.argtypes = []
     for name in EXPORTS:
         getattr(L, name).restype = ctypes.c_int

@@ -93,6 +93,37 @@ def ps_apply(W: torch.Tensor, shards: torch.Tensor, lr: float, momentum: float =
             buf.data_ptr() if buf is not None else None, _stream_handle(stream, W.device)))
 
 
+def ps_apply_batch(tensors: list, lr: float, momentum: float = 0.0, stream=None) -> None:
+    """poseidon_ps_apply for many tensors in one pass (poseidon_ps_apply_batch).
+
+    ``tensors`` is a list of (W, shards, buf) with shards P x W.numel() (the
+    same P for all) and buf None or a W.numel()-vector; momentum is used only
+    for tensors that have a buffer."""
+    if not tensors:
+        return
+    arr = (L.PoseidonPsTensor * len(tensors))()
+    P = None
+    dev = None
+    for i, (W, shards, buf) in enumerate(tensors):
+        _dev_f32("W", W), _dev_f32("shards", shards)
+        if buf is not None:
+            _dev_f32("buf", buf)
+        _same_device(W, shards, buf)
+        dev = dev or W.device
+        if W.device != dev:
+            raise ValueError("all tensors must be on one device")
+        n = W.numel()
+        p = shards.shape[0] if shards.dim() >= 1 else 0
+        if P is None:
+            P = p
+        if p != P or shards.numel() != P * n or (buf is not None and buf.numel() != n):
+            raise ValueError(f"tensor {i}: shards must be {P} x {n} and buf must have {n} values")
+        arr[i] = L.PoseidonPsTensor(W.data_ptr(), shards.data_ptr(), buf.data_ptr() if buf is not None else None, n)
+    with torch.cuda.device(dev):
+        _check("poseidon_ps_apply_batch", L.lib().poseidon_ps_apply_batch(
+            arr, len(tensors), P, float(lr), float(momentum), _stream_handle(stream, dev)))
+
+
 def hybcomm_choose(M: int, N: int, B: int, P: int) -> int:
     """Alg. 1 for an FC layer on P worker+server nodes: SFB (1) or PS (0)."""
     return _check("poseidon_hybcomm_choose", L.lib().poseidon_hybcomm_choose(M, N, B, P))
@@ -129,12 +160,16 @@ class StreamPool:
         """Bracket every update of the following iterations with timing events."""
         _check("poseidon_pool_set_timing", L.lib().poseidon_pool_set_timing(self._h, int(bool(enable))))
 
-    def tensor_times(self, count: int) -> list[float]:
-        """Per-tensor ms of the last timed iteration (-1: no work); waits for it."""
-        ms = (ctypes.c_float * max(1, count))()
+    def launch_times(self, capacity: int = 256) -> list[dict]:
+        """Launch records of the last timed iteration (waits for it): dicts with
+        ``scheme`` (SFB/PS), ``tensor`` (index, -1 for the PS batch),
+        ``stream`` and ``ms``."""
+        recs = (L.PoseidonLaunchRecord * capacity)()
+        n = ctypes.c_int32()
         with torch.cuda.device(self.device):
-            _check("poseidon_pool_tensor_times", L.lib().poseidon_pool_tensor_times(self._h, ms, count))
-        return list(ms[:count])
+            _check("poseidon_pool_launch_times",
+                   L.lib().poseidon_pool_launch_times(self._h, recs, capacity, ctypes.byref(n)))
+        return [{"scheme": r.scheme, "tensor": r.tensor, "stream": r.stream, "ms": r.ms} for r in recs[:n.value]]
 
     def close(self):
         if self._h:

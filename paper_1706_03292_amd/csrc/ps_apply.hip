@@ -160,6 +160,107 @@ hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, 
     }
 }
 
+// ---------------------------------------------------------------------------
+// Many tensors in one launch.  The descriptors travel by value in the kernel
+// arguments; tensor t owns the workgroups [first_block[t], first_block[t+1]),
+// each of which updates PS_BLOCK_ELEMS consecutive elements of it (16-byte
+// groups when the tensor allows it, single elements otherwise).
+// ---------------------------------------------------------------------------
+
+constexpr int PS_BLOCK_ELEMS = 4096;   // elements per workgroup in a batch
+
+struct PsBatchItem {
+    float* W;
+    const float* G;
+    float* buf;
+    int64_t n;
+    int32_t first_block;
+    int32_t vec;
+};
+
+struct PsBatchArgs {
+    PsBatchItem item[PS_BATCH_MAX];
+    int32_t count;
+};
+
+template <int PT, bool MOM>
+__global__ __launch_bounds__(PS_THREADS) void ps_apply_batch_kernel(const PsBatchArgs args, int P, float lr,
+                                                                    float mu, int total_blocks)
+{
+    // Persistent: workgroup g handles work blocks g, g + gridDim.x, ... so that
+    // a small grid can stream through the whole batch next to other kernels.
+    int t = 0;
+    for (int b = blockIdx.x; b < total_blocks; b += gridDim.x) {
+        while (t + 1 < args.count && b >= args.item[t + 1].first_block)
+            ++t;
+        float* __restrict__ W = args.item[t].W;
+        const float* __restrict__ G = args.item[t].G;
+        float* __restrict__ buf = args.item[t].buf;
+        const int64_t n = args.item[t].n;
+        const int64_t base = static_cast<int64_t>(b - args.item[t].first_block) * PS_BLOCK_ELEMS;
+        if (args.item[t].vec) {
+            const int64_t n4 = n >> 2;
+            const f4* G4 = reinterpret_cast<const f4*>(G);
+            f4* W4 = reinterpret_cast<f4*>(W);
+            f4* B4 = reinterpret_cast<f4*>(buf);
+#pragma unroll
+            for (int u = 0; u < PS_BLOCK_ELEMS / 4 / PS_THREADS; ++u) {
+                const int64_t i = (base >> 2) + u * PS_THREADS + threadIdx.x;
+                if (i < n4) {
+                    const f4 s = shard_sum4<PT>(G4, P, n4, i);
+                    f4 w = W4[i];
+                    if constexpr (MOM) {
+                        const f4 bv = fma4(mu, B4[i], s);
+                        B4[i] = bv;
+                        w = fma4(-lr, bv, w);
+                    } else {
+                        w = fma4(-lr, s, w);
+                    }
+                    W4[i] = w;
+                }
+            }
+        } else {
+#pragma unroll 4
+            for (int u = 0; u < PS_BLOCK_ELEMS / PS_THREADS; ++u) {
+                const int64_t i = base + u * PS_THREADS + threadIdx.x;
+                if (i < n) {
+                    const float s = shard_sum1<PT>(G, P, n, i);
+                    float w = W[i];
+                    if constexpr (MOM) {
+                        const float bv = fmaf(mu, buf[i], s);
+                        buf[i] = bv;
+                        w = fmaf(-lr, bv, w);
+                    } else {
+                        w = fmaf(-lr, s, w);
+                    }
+                    W[i] = w;
+                }
+            }
+        }
+    }
+}
+
+template <int PT, bool MOM>
+void launch_batch_pt(const PsBatchArgs& a, int blocks, int grid, int32_t P, float lr, float mu, hipStream_t stream)
+{
+    ps_apply_batch_kernel<PT, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu, blocks);
+}
+
+template <bool MOM>
+void launch_batch_mom(const PsBatchArgs& a, int blocks, int grid, int32_t P, float lr, float mu,
+                      hipStream_t stream)
+{
+    switch (P) {
+    case 1:  launch_batch_pt<1, MOM>(a, blocks, grid, P, lr, mu, stream); break;
+    case 2:  launch_batch_pt<2, MOM>(a, blocks, grid, P, lr, mu, stream); break;
+    case 4:  launch_batch_pt<4, MOM>(a, blocks, grid, P, lr, mu, stream); break;
+    case 8:  launch_batch_pt<8, MOM>(a, blocks, grid, P, lr, mu, stream); break;
+    case 16: launch_batch_pt<16, MOM>(a, blocks, grid, P, lr, mu, stream); break;
+    case 32: launch_batch_pt<32, MOM>(a, blocks, grid, P, lr, mu, stream); break;
+    default: launch_batch_pt<0, MOM>(a, blocks, grid, P, lr, mu, stream); break;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
@@ -169,6 +270,55 @@ hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
     if (buf)
         return launch_mom<true>(W, shards, P, n, lr, momentum, buf, vec, stream);
     return launch_mom<false>(W, shards, P, n, lr, 0.0f, nullptr, vec, stream);
+}
+
+hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, float lr, float momentum,
+                                 hipStream_t stream, int max_grid)
+{
+    // Tensors without a momentum buffer and tensors with one are launched
+    // separately (the kernel is specialised on it); each launch carries up to
+    // PS_BATCH_MAX descriptors.
+    for (int pass = 0; pass < 2; ++pass) {
+        const bool mom = pass == 1;
+        PsBatchArgs a{};
+        int64_t blocks = 0;
+        auto flush = [&]() -> hipError_t {
+            if (a.count == 0)
+                return hipSuccess;
+            const int nb = static_cast<int>(blocks);
+            const int grid = (max_grid > 0 && max_grid < nb) ? max_grid : nb;
+            if (mom)
+                launch_batch_mom<true>(a, nb, grid, P, lr, momentum, stream);
+            else
+                launch_batch_mom<false>(a, nb, grid, P, lr, 0.0f, stream);
+            a = PsBatchArgs{};
+            blocks = 0;
+            return hipGetLastError();
+        };
+        for (int32_t i = 0; i < count; ++i) {
+            if (t[i].n == 0 || (t[i].buf != nullptr) != mom)
+                continue;
+            const int64_t nb = (t[i].n + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
+            if (a.count == PS_BATCH_MAX || blocks + nb > INT32_MAX) {
+                const hipError_t e = flush();
+                if (e != hipSuccess)
+                    return e;
+            }
+            PsBatchItem& it = a.item[a.count++];
+            it.W = t[i].W;
+            it.G = t[i].shards;
+            it.buf = t[i].buf;
+            it.n = t[i].n;
+            it.first_block = static_cast<int32_t>(blocks);
+            it.vec = (t[i].n % 4 == 0) && aligned16(t[i].W) && aligned16(t[i].shards) &&
+                     (!t[i].buf || aligned16(t[i].buf));
+            blocks += nb;
+        }
+        const hipError_t e = flush();
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
 }
 
 int check_ps_args(const float* W, const float* shards, int32_t P, int64_t n,
@@ -197,6 +347,24 @@ extern "C" int poseidon_ps_apply(float* W, const float* shards, int32_t P, int64
     if (rc != POSEIDON_OK || n == 0)
         return rc;
     return poseidon::launch_ps_apply(W, shards, P, n, lr, momentum, buf, stream) == hipSuccess
+               ? POSEIDON_OK
+               : POSEIDON_ERR_HIP;
+}
+
+extern "C" int poseidon_ps_apply_batch(const poseidon_ps_tensor* tensors, int32_t count, int32_t P,
+                                       float lr, float momentum, hipStream_t stream)
+{
+    if (count < 0 || (count > 0 && !tensors) || P < 1)
+        return POSEIDON_ERR_INVALID_ARG;
+    for (int32_t i = 0; i < count; ++i) {
+        const poseidon_ps_tensor& x = tensors[i];
+        const int rc = poseidon::check_ps_args(x.W, x.shards, P, x.n, x.buf ? momentum : 0.0f, x.buf);
+        if (rc != POSEIDON_OK)
+            return rc;
+    }
+    static_assert(sizeof(poseidon_ps_tensor) == sizeof(poseidon::PsTensor), "descriptor layout");
+    return poseidon::launch_ps_apply_batch(reinterpret_cast<const poseidon::PsTensor*>(tensors), count, P, lr,
+                                           momentum, stream, 0) == hipSuccess
                ? POSEIDON_OK
                : POSEIDON_ERR_HIP;
 }

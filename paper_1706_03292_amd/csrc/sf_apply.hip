@@ -358,7 +358,8 @@ hipError_t launch_sf_apply(float* W, const float* U, const float* V,
 {
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
     if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_cfg<128, 128, 16, 64, 64, true, 4, 1, false>(W, U, V, M, N, K, lr, stream);
+        return launch_cfg<128, 128, 16, 64, 64, true, POSEIDON_SF_WAVES_PER_SIMD, 1, false>(W, U, V, M, N, K, lr,
+                                                                                           stream);
     return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, false>(W, U, V, M, N, K, lr, stream);
 }
 

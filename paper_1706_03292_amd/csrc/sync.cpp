@@ -18,10 +18,11 @@ struct poseidon_stream_pool {
     std::vector<hipEvent_t> joined;   // one per stream: its last update of the iteration
     hipEvent_t fork = nullptr;        // work enqueued on the caller's stream before the iteration
     bool timing = false;
-    std::vector<hipEvent_t> t_start;  // per tensor of the last timed iteration
+    std::vector<hipEvent_t> t_start;  // per launch of the last timed iteration
     std::vector<hipEvent_t> t_stop;
-    std::vector<char> t_ran;
-    int32_t t_count = -1;             // tensors in the last timed iteration (-1: none)
+    std::vector<poseidon_launch_record> t_rec;
+    bool t_valid = false;             // a timed iteration has been enqueued
+    std::vector<poseidon::PsTensor> ps_work;   // host scratch reused across calls
 };
 
 namespace poseidon {
@@ -68,7 +69,7 @@ void destroy_pool(poseidon_stream_pool* pool)
     delete pool;
 }
 
-// Make sure the pool holds timing events for `count` tensors.
+// Make sure the pool holds timing events for `count` launches.
 bool reserve_timing(poseidon_stream_pool* pool, int32_t count)
 {
     while (static_cast<int32_t>(pool->t_start.size()) < count) {
@@ -82,7 +83,7 @@ bool reserve_timing(poseidon_stream_pool* pool, int32_t count)
         pool->t_start.push_back(a);
         pool->t_stop.push_back(b);
     }
-    pool->t_ran.assign(static_cast<size_t>(count), 0);
+    pool->t_rec.clear();
     return true;
 }
 
@@ -173,51 +174,78 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
             schemes[t] = plan[static_cast<size_t>(t)];
-    if (pool->timing) {
-        if (!reserve_timing(pool, count))
-            return POSEIDON_ERR_HIP;
-        pool->t_count = count;
+    // Launches of this iteration: one per SFB tensor, plus one batched PS
+    // launch covering every PS tensor.
+    int32_t sfb_count = 0;
+    pool->ps_work.clear();
+    for (int32_t t = count - 1; t >= 0; --t) {
+        const poseidon_tensor& x = tensors[t];
+        const int64_t n = x.M * x.N;
+        if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
+            if (n > 0 && K > 0)
+                ++sfb_count;
+        } else if (n > 0) {
+            pool->ps_work.push_back(PsTensor{x.W, x.shards, x.buf, n});
+        }
     }
-    if (active == 0)
+    const int32_t launches = sfb_count + (pool->ps_work.empty() ? 0 : 1);
+    if (pool->timing) {
+        if (!reserve_timing(pool, launches))
+            return POSEIDON_ERR_HIP;
+        pool->t_valid = true;
+    }
+    if (launches == 0)
         return POSEIDON_OK;
 
     // Stream assignment: the compute-bound SF reconstructions go, in
     // backpropagation order, to the pool's first stream; the bandwidth-bound
-    // PS applies go round-robin to the others, so the two kinds overlap on the
-    // GPU instead of queueing behind each other.  A one-stream pool serialises
-    // everything.
+    // PS applies, batched into one pass over all PS tensors (backpropagation
+    // order), to the second, so the two kinds overlap on the GPU instead of
+    // queueing behind each other.  A one-stream pool serialises everything.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
-    const int32_t used = active < S ? active : S;
+    const int32_t used = (launches < S ? launches : S) < 2 ? 1 : 2;
     if (hipEventRecord(pool->fork, stream) != hipSuccess)
         return POSEIDON_ERR_HIP;
     for (int32_t s = 0; s < used; ++s)
         if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
             return POSEIDON_ERR_HIP;
 
-    int32_t q = 0;
+    auto timed = [&](hipStream_t s, int32_t scheme, int32_t tensor, int32_t si, auto&& launch) -> bool {
+        const size_t r = pool->t_rec.size();
+        if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
+            return false;
+        if (launch() != hipSuccess)
+            return false;
+        if (pool->timing) {
+            if (hipEventRecord(pool->t_stop[r], s) != hipSuccess)
+                return false;
+            pool->t_rec.push_back(poseidon_launch_record{scheme, tensor, si, 0.0f});
+        }
+        return true;
+    };
+    auto issue_ps = [&]() -> bool {
+        if (pool->ps_work.empty())
+            return true;
+        const int32_t si = used > 1 ? 1 : 0;
+        hipStream_t s = pool->streams[si];
+        return timed(s, POSEIDON_PS, -1, si, [&] {
+            return launch_ps_apply_batch(pool->ps_work.data(), static_cast<int32_t>(pool->ps_work.size()), P, lr,
+                                         momentum, s,
+                                         sfb_count > 0 ? POSEIDON_PS_OVERLAP_WG_PER_CU * device_cu_count() : 0);
+        });
+    };
+    if (POSEIDON_PS_ISSUE_FIRST && !issue_ps())
+        return POSEIDON_ERR_HIP;
     for (int32_t t = count - 1; t >= 0; --t) {
         const poseidon_tensor& x = tensors[t];
-        const int64_t n = x.M * x.N;
-        const bool sfb = plan[static_cast<size_t>(t)] == POSEIDON_SFB;
-        if (n == 0 || (sfb && K == 0))
+        if (plan[static_cast<size_t>(t)] != POSEIDON_SFB || x.M * x.N == 0 || K == 0)
             continue;
-        int32_t si = 0;
-        if (used > 1 && !sfb)
-            si = 1 + (q++ % (used - 1));
-        hipStream_t s = pool->streams[si];
-        if (pool->timing && hipEventRecord(pool->t_start[t], s) != hipSuccess)
+        hipStream_t s = pool->streams[0];
+        if (!timed(s, POSEIDON_SFB, t, 0, [&] { return launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s); }))
             return POSEIDON_ERR_HIP;
-        const hipError_t err =
-            sfb ? launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s)
-                : launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
-        if (err != hipSuccess)
-            return POSEIDON_ERR_HIP;
-        if (pool->timing) {
-            if (hipEventRecord(pool->t_stop[t], s) != hipSuccess)
-                return POSEIDON_ERR_HIP;
-            pool->t_ran[static_cast<size_t>(t)] = 1;
-        }
     }
+    if (!POSEIDON_PS_ISSUE_FIRST && !issue_ps())
+        return POSEIDON_ERR_HIP;
 
     for (int32_t s = 0; s < used; ++s) {
         if (hipEventRecord(pool->joined[s], pool->streams[s]) != hipSuccess ||
@@ -235,17 +263,22 @@ extern "C" int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enab
     return POSEIDON_OK;
 }
 
-extern "C" int poseidon_pool_tensor_times(poseidon_stream_pool* pool, float* ms, int32_t count)
+extern "C" int poseidon_pool_launch_times(poseidon_stream_pool* pool, poseidon_launch_record* records,
+                                          int32_t capacity, int32_t* count)
 {
-    if (!pool || pool->t_count < 0 || count != pool->t_count || (count > 0 && !ms))
+    if (!pool || !count || capacity < 0 || (capacity > 0 && !records) || !pool->t_valid)
         return POSEIDON_ERR_INVALID_ARG;
-    for (int32_t t = 0; t < count; ++t) {
-        ms[t] = -1.0f;
-        if (!pool->t_ran[static_cast<size_t>(t)])
-            continue;
-        if (hipEventSynchronize(pool->t_stop[t]) != hipSuccess ||
-            hipEventElapsedTime(&ms[t], pool->t_start[t], pool->t_stop[t]) != hipSuccess)
+    const int32_t n = static_cast<int32_t>(pool->t_rec.size());
+    *count = n;
+    if (capacity < n)
+        return POSEIDON_ERR_INVALID_ARG;
+    for (int32_t r = 0; r < n; ++r) {
+        float ms = 0.0f;
+        if (hipEventSynchronize(pool->t_stop[r]) != hipSuccess ||
+            hipEventElapsedTime(&ms, pool->t_start[r], pool->t_stop[r]) != hipSuccess)
             return POSEIDON_ERR_HIP;
+        records[r] = pool->t_rec[static_cast<size_t>(r)];
+        records[r].ms = ms;
     }
     return POSEIDON_OK;
 }

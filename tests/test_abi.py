@@ -36,6 +36,8 @@ def test_struct_layout_matches_header():
     # int32 kind, int32 reserved, then 8-byte fields: W, M, N, U, V, shards, buf.
     assert ctypes.sizeof(L.PoseidonTensor) == 8 + 7 * 8
     assert L.PoseidonTensor.W.offset == 8 and L.PoseidonTensor.buf.offset == 56
+    assert ctypes.sizeof(L.PoseidonPsTensor) == 32 and L.PoseidonPsTensor.n.offset == 24
+    assert ctypes.sizeof(L.PoseidonLaunchRecord) == 16 and L.PoseidonLaunchRecord.ms.offset == 12
 
 
 def test_invalid_arguments_rejected_before_device_work():
@@ -59,6 +61,15 @@ def test_invalid_arguments_rejected_before_device_work():
     assert lib.poseidon_pool_create(65, ctypes.byref(ctypes.c_void_p())) == L.ERR_INVALID_ARG
     assert lib.poseidon_pool_destroy(None) == L.OK
     assert lib.poseidon_sync_iteration(None, None, 0, 32, 16, 0.1, 0.9, None, None) == L.ERR_INVALID_ARG
+    # batched PS: bad P, bad count, one bad tensor rejects the whole batch
+    t = (L.PoseidonPsTensor * 2)(L.PoseidonPsTensor(0x1000, 0x900000, None, 8),
+                                 L.PoseidonPsTensor(0x2000, 0x2000, None, 8))
+    assert lib.poseidon_ps_apply_batch(t, 2, 0, 0.1, 0.0, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_ps_apply_batch(t, -1, 2, 0.1, 0.0, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_ps_apply_batch(t, 2, 2, 0.1, 0.0, None) == L.ERR_INVALID_ARG   # overlap in #1
+    assert lib.poseidon_ps_apply_batch(None, 0, 2, 0.1, 0.0, None) == L.OK
+    n = ctypes.c_int32()
+    assert lib.poseidon_pool_launch_times(None, None, 0, ctypes.byref(n)) == L.ERR_INVALID_ARG
 
 
 def test_hybcomm_argument_checks():

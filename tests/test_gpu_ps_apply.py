@@ -147,3 +147,66 @@ def test_ps_apply_fc_sized_layer_sampled():
     torch.cuda.synchronize()
     assert_close(to_np(Wd)[idx], w_ref, W_TOL, "W")
     assert_close(to_np(bd)[idx], b_ref, BUF_TOL, "buf")
+
+
+def _batch_case(sizes, P, seed, with_buf):
+    host = []
+    for j, n in enumerate(sizes):
+        W = I.randn(seed + 3 * j, (n,), 0.01)
+        G = I.randn(seed + 3 * j + 1, (P, n), 1e-3)
+        buf = I.randn(seed + 3 * j + 2, (n,), 1e-3) if with_buf(j) else None
+        host.append((W, G, buf))
+    return host
+
+
+@pytest.mark.parametrize("P", [16, 32, 3])
+def test_ps_apply_batch_matches_oracle(P):
+    """One pass over many tensors: sizes from 1 to 300k, every residue mod 4,
+    with and without momentum buffers, more tensors than one launch carries."""
+    d = dev()
+    sizes = [1, 2, 3, 4, 5, 63, 64, 65, 4095, 4096, 4097, 9 * 1031, 21841, 100_003, 300_000]
+    sizes = sizes * 4                      # 60 tensors: more than one launch's descriptors
+    host = _batch_case(sizes, P, seed=7000 + P, with_buf=lambda j: j % 3 != 0)
+    devt = [(W.to(d), G.to(d), b.to(d) if b is not None else None) for W, G, b in host]
+    log(f"ps_apply_batch P={P} tensors={len(devt)}")
+    api.ps_apply_batch(devt, 0.01, 0.9)
+    torch.cuda.synchronize()
+    for (W, G, b), (Wd, _, bd) in zip(host, devt):
+        mu = 0.9 if b is not None else 0.0
+        w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, mu, b.numpy() if b is not None else None)
+        assert_close(to_np(Wd), w_ref, W_TOL, f"W n={W.numel()}")
+        if b is not None:
+            assert_close(to_np(bd), b_ref, BUF_TOL, f"buf n={W.numel()}")
+
+
+def test_ps_apply_batch_equals_single_calls_bitwise():
+    """The batched pass computes each tensor exactly as poseidon_ps_apply does."""
+    d = dev()
+    host = _batch_case([4096 * 3 + 1, 8192, 50_000, 7], 16, seed=8100, with_buf=lambda j: j != 1)
+    a = [(W.to(d), G.to(d), b.to(d) if b is not None else None) for W, G, b in host]
+    s = [(W.to(d), G.to(d), b.to(d) if b is not None else None) for W, G, b in host]
+    log("ps_apply_batch vs single")
+    api.ps_apply_batch(a, 0.01, 0.9)
+    for W, G, b in s:
+        api.ps_apply(W, G, 0.01, 0.9 if b is not None else 0.0, b)
+    torch.cuda.synchronize()
+    for (Wa, _, ba), (Ws, _, bs) in zip(a, s):
+        assert torch.equal(Wa, Ws)
+        if ba is not None:
+            assert torch.equal(ba, bs)
+
+
+def test_ps_apply_batch_misaligned_and_empty():
+    d = dev()
+    host = _batch_case([1001, 4096, 0, 17], 4, seed=8200, with_buf=lambda j: True)
+    devt = [(misaligned(W.to(d)) if W.numel() else W.to(d), misaligned(G.to(d)) if W.numel() else G.to(d),
+             misaligned(b.to(d)) if W.numel() else b.to(d)) for W, G, b in host]
+    log("ps_apply_batch misaligned")
+    api.ps_apply_batch(devt, 0.01, 0.9)
+    torch.cuda.synchronize()
+    for (W, G, b), (Wd, _, bd) in zip(host, devt):
+        if W.numel() == 0:
+            continue
+        w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, 0.9, b.numpy())
+        assert_close(to_np(Wd), w_ref, W_TOL, "W")
+        assert_close(to_np(bd), b_ref, BUF_TOL, "buf")

@@ -144,3 +144,25 @@ def test_sf_apply_vgg19_22k_full_size_sampled(name):
     torch.cuda.synchronize()
     ref_d = oracle.sf_apply_points(np.zeros((M, N), np.float32), U.numpy(), V.numpy(), -1.0, rows, cols)
     assert_close(to_np(Z)[rows, cols], ref_d, DELTA_TOL, name + " raw")
+
+
+def test_sf_apply_rows_too_long_for_32bit_offsets():
+    """N > 2^31 / (4 * 128): a 128-row tile spans more than 2 GiB, so the
+    kernel takes its 64-bit-addressed epilogue.  W starts at a constant so the
+    2.2 GB layer needs no random draw; points are checked against the oracle."""
+    d = dev()
+    M, N, K = 130, (1 << 22) + 37, 3
+    U = I.randn(4242, (K, M), 1.0)
+    V = I.randn(4243, (K, N), 1.0)
+    Wd = torch.full((M, N), 0.5, device=d)
+    log(f"sf_apply huge rows M={M} N={N} K={K}")
+    api.sf_apply(Wd, U.to(d), V.to(d), 0.01)
+    torch.cuda.synchronize()
+    rows, cols = sample_points(M, N, 3000, seed=7)
+    rows = np.concatenate([rows, np.full(64, 129), np.full(64, 128)])
+    cols = np.concatenate([cols, np.arange(N - 64, N), np.arange(64)])
+    W0 = np.full((1, 1), 0.5, np.float32)
+    ref = np.array([oracle.sf_apply_points(W0, U[:, r:r + 1].numpy(), V[:, c:c + 1].numpy(), 0.01,
+                                           [0], [0])[0] for r, c in zip(rows, cols)])
+    got = Wd[torch.from_numpy(rows).to(d), torch.from_numpy(cols).to(d)].cpu().numpy()
+    assert_close(got, ref, W_TOL, "huge rows")

@@ -131,3 +131,23 @@ def test_sync_iteration_missing_payload_is_an_error():
     assert it() == [api.PS]
     torch.cuda.synchronize()
     pool.close()
+
+
+def test_sync_iteration_launch_records():
+    """Timing mode: one record per SFB tensor on stream 0 and one PS batch."""
+    d = dev()
+    wl = I.workload(5)
+    host = I.make_tensors(wl, only=["fc7.W", "fc7.b", "conv5_4.W"])
+    devt = _to_dev(host, d)
+    pool = api.StreamPool(4)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    pool.set_timing(True)
+    log("sync_iteration timing records")
+    it()
+    recs = pool.launch_times()
+    fc = [i for i, h in enumerate(host) if h["spec"].name == "fc7.W"][0]
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in recs] == [(api.PS, -1, 1), (api.SFB, fc, 0)]
+    assert all(r["ms"] > 0 for r in recs)
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    pool.close()
