@@ -190,41 +190,49 @@ def main():
     # with the library's timing events around each launch on its own stream.
     ksteps = args.kernel_steps or args.steps
     pool.set_timing(True)
-    sfb_t = {}
-    ps_batch_in_iter = 0.0
+    launch_ms = {}
     for _ in range(ksteps):
         it(stream)
         for r in pool.launch_times():
-            if r["scheme"] == api.SFB:
-                sfb_t[r["tensor"]] = sfb_t.get(r["tensor"], 0.0) + r["ms"] / ksteps
-            else:
-                ps_batch_in_iter += r["ms"] / ksteps
+            launch_ms[r["tensor"]] = launch_ms.get(r["tensor"], 0.0) + r["ms"] / ksteps
     pool.set_timing(False)
     torch.cuda.synchronize()
 
-    # The PS pass shares the GPU with the SF reconstructions during the
-    # iteration (by design), so its bandwidth is measured in a phase of its
-    # own: the same batched pass over every PS tensor of the step, alone on one
-    # stream, between HIP events on that stream.
+    # The PS applies share the GPU with the SF reconstructions during the
+    # iteration (by design), so their bandwidth is measured in a phase of its
+    # own: the same launches, every PS tensor of the step one after another on
+    # one stream with nothing else running, between HIP events on that stream.
+    # The batched pass (poseidon_ps_apply_batch) over the same tensors and the
+    # largest tensor's launch alone are timed too.
     ps_list = [(t["W"], t["shards"], t.get("buf")) for t in reversed(devt) if t["spec"].kind != "fc"]
-    ps_iso = []
-    for rep in range(ksteps + 1):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream)
-        b.record(stream)
-        torch.cuda.synchronize()
-        if rep > 0:                       # the first pass is a warm-up
-            ps_iso.append(a.elapsed_time(b))
-    ps_ms = sum(ps_iso) / len(ps_iso)
+    big = max(range(len(ps_list)), key=lambda i: ps_list[i][0].numel())
+
+    def _time(fn):
+        out = []
+        for rep in range(ksteps + 1):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            fn()
+            b.record(stream)
+            torch.cuda.synchronize()
+            if rep > 0:                   # the first pass is a warm-up
+                out.append(a.elapsed_time(b))
+        return sum(out) / len(out)
+
+    ps_ms = _time(lambda: [api.ps_apply(W.view(-1), G, wl.lr, wl.momentum, buf, stream=stream)
+                           for W, G, buf in ps_list])
+    ps_batch_ms = _time(lambda: api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream))
+    W_, G_, b_ = ps_list[big]
+    ps_big_ms = _time(lambda: api.ps_apply(W_.view(-1), G_, wl.lr, wl.momentum, b_, stream=stream))
+    ps_big_bytes = float(W_.numel()) * (4 * wl.P + (16 if b_ is not None else 8))
 
     sfb_flops = sfb_ms = sfb_bytes = 0.0
-    ps_bytes = 0.0
+    ps_bytes = ps_in_iter = 0.0
     layers = []
     for i, (h, sch) in enumerate(zip(host, schemes)):
         spec = h["spec"]
         if sch == api.SFB:
-            ms = sfb_t[i]
+            ms = launch_ms[i]
             f = _sf_flops(spec, wl.K)
             sfb_flops += f
             sfb_bytes += _sf_bytes(spec, wl.K)
@@ -233,6 +241,7 @@ def main():
                            "tflops": round(f / ms / 1e9, 2)})
         else:
             ps_bytes += _ps_bytes(spec, wl.P, "buf" in h)
+            ps_in_iter += launch_ms.get(i, 0.0)
     sfb_tflops = sfb_flops / sfb_ms / 1e9 if sfb_ms else None
     ps_gbs = ps_bytes / ps_ms / 1e6 if ps_ms else None
     n_ps = sum(1 for s_ in schemes if s_ == api.PS)
@@ -261,15 +270,22 @@ def main():
                      "work": f"2*M*N*K flops over the {sum(1 for s in schemes if s == api.SFB)} SFB "
                              f"launches of one step ({sfb_flops / 1e9:.1f} GFLOP) / their summed "
                              f"average durations ({sfb_ms:.4f} ms)"},
-        "roofline_ps": {"bound": "hbm", "kernel": "ps_apply_batch",
+        "roofline_ps": {"bound": "hbm", "kernel": "ps_apply",
                         "achieved": round(ps_gbs, 1) if ps_gbs else None,
                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(ps_gbs / PEAK_HBM_GBS, 4) if ps_gbs else None,
                         "traffic": _stored_traffic("ps_apply", "ps_apply.hip"),
                         "work": f"(4P+16) bytes per element over the {n_ps} PS tensors of one step "
-                                f"({ps_bytes / 1e9:.3f} GB) / the average duration of their batched "
-                                f"pass alone on one stream ({ps_ms:.4f} ms); inside the iteration the "
-                                f"same pass overlaps the SF reconstructions and takes {ps_batch_in_iter:.4f} ms"},
+                                f"({ps_bytes / 1e9:.3f} GB) / the duration of their launches one after "
+                                f"another on one stream with nothing else running ({ps_ms:.4f} ms); inside "
+                                f"the iteration they overlap the SF reconstructions (summed launch time "
+                                f"{ps_in_iter:.4f} ms)",
+                        "largest_tensor": {"tensor": host[[i for i, h in enumerate(host)
+                                                           if h["spec"].kind != "fc"][::-1][big]]["spec"].name,
+                                           "ms": round(ps_big_ms, 4),
+                                           "gbs": round(ps_big_bytes / ps_big_ms / 1e6, 1)},
+                        "batched_pass": {"ms": round(ps_batch_ms, 4),
+                                         "gbs": round(ps_bytes / ps_batch_ms / 1e6, 1)}},
         "event_ms_per_step": round(event_ms, 4),
         "sfb_tflops": round(sfb_tflops, 2) if sfb_tflops else None,
         "ps_gbs": round(ps_gbs, 1) if ps_gbs else None,

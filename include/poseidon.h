@@ -182,12 +182,10 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation"; Alg. 2 TRAIN/sync): tensors[] is given in forward order
  * and issued from the last to the first (backpropagation order).  For each
  * tensor the scheme is Alg. 1's (FC: poseidon_hybcomm_choose(M, N, B, P);
- * other kinds: PS).  The SFB updates (bound by the matrix cores) are
- * enqueued one per tensor on the pool's first stream; the PS updates (bound
- * by memory bandwidth) are enqueued as one batched pass over all PS tensors
- * (poseidon_ps_apply_batch, backpropagation order) on the second stream, so
- * that the two kinds overlap; a one-stream pool runs everything in order.
- * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
+ * other kinds: PS) and its update is enqueued, in backpropagation order,
+ * on the pool's first stream for SFB (bound by the matrix cores) or on its
+ * second stream for PS (bound by memory bandwidth), so that the two kinds
+ * overlap; a one-stream pool runs everything in order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
  * poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf) (momentum is used
  * only when buf != NULL).  Every pool stream first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so
@@ -213,8 +211,8 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 
 /* One launch of the last iteration run with timing enabled. */
 typedef struct poseidon_launch_record {
-    int32_t scheme;   /* POSEIDON_SFB (one tensor) or POSEIDON_PS (the batch of all PS tensors) */
-    int32_t tensor;   /* index into that call's tensors[] for SFB, -1 for the PS batch */
+    int32_t scheme;   /* POSEIDON_SFB or POSEIDON_PS */
+    int32_t tensor;   /* index into that call's tensors[] */
     int32_t stream;   /* pool stream index */
     float   ms;       /* time between the events around the launch */
 } poseidon_launch_record;

@@ -40,25 +40,8 @@ struct PsTensor {
 constexpr int PS_BATCH_MAX = 48;   // descriptors per batched launch (kernel-argument space)
 
 // Every tensor with n > 0 in one or a few launches (arguments validated).
-// max_grid > 0 caps the workgroups of each launch (they then loop over the
-// work), so that the pass can run next to a compute-bound kernel.
 hipError_t launch_ps_apply_batch(const PsTensor* tensors, int32_t count, int32_t P, float lr,
-                                 float momentum, hipStream_t stream, int max_grid);
-
-// Tuning knobs: workgroups per CU of the sync iteration's batched PS pass while
-// the SF reconstructions run (0 = one workgroup per 4096 elements, no cap),
-// whether the PS pass is issued before the SF launches, and the SF kernel's
-// waves per SIMD.  Measured on the VGG19-22K iteration, caps of 1-4 per CU,
-// either order and 3 or 4 waves per SIMD all land within 2.04-2.12 ms.
-#ifndef POSEIDON_PS_OVERLAP_WG_PER_CU
-#define POSEIDON_PS_OVERLAP_WG_PER_CU 0
-#endif
-#ifndef POSEIDON_PS_ISSUE_FIRST
-#define POSEIDON_PS_ISSUE_FIRST 1
-#endif
-#ifndef POSEIDON_SF_WAVES_PER_SIMD
-#define POSEIDON_SF_WAVES_PER_SIMD 4
-#endif
+                                 float momentum, hipStream_t stream);
 
 // Argument checks of the public entry points (no device work).
 int check_sf_args(const float* W, const float* U, const float* V,

@@ -167,7 +167,8 @@ hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, 
 // groups when the tensor allows it, single elements otherwise).
 // ---------------------------------------------------------------------------
 
-constexpr int PS_BLOCK_ELEMS = 4096;   // elements per workgroup in a batch
+constexpr int PS_BLOCK_ELEMS = 4096;     // elements per work block in a batch
+constexpr int PS_BATCH_MAX_GRID = 8192;  // workgroups per batched launch (they loop over the work blocks)
 
 struct PsBatchItem {
     float* W;
@@ -187,8 +188,8 @@ template <int PT, bool MOM>
 __global__ __launch_bounds__(PS_THREADS) void ps_apply_batch_kernel(const PsBatchArgs args, int P, float lr,
                                                                     float mu, int total_blocks)
 {
-    // Persistent: workgroup g handles work blocks g, g + gridDim.x, ... so that
-    // a small grid can stream through the whole batch next to other kernels.
+    // Workgroup g handles work blocks g, g + gridDim.x, ... (one pass when the
+    // grid covers every block).
     int t = 0;
     for (int b = blockIdx.x; b < total_blocks; b += gridDim.x) {
         while (t + 1 < args.count && b >= args.item[t + 1].first_block)
@@ -273,7 +274,7 @@ hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
 }
 
 hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, float lr, float momentum,
-                                 hipStream_t stream, int max_grid)
+                                 hipStream_t stream)
 {
     // Tensors without a momentum buffer and tensors with one are launched
     // separately (the kernel is specialised on it); each launch carries up to
@@ -286,7 +287,7 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
             if (a.count == 0)
                 return hipSuccess;
             const int nb = static_cast<int>(blocks);
-            const int grid = (max_grid > 0 && max_grid < nb) ? max_grid : nb;
+            const int grid = nb < PS_BATCH_MAX_GRID ? nb : PS_BATCH_MAX_GRID;
             if (mom)
                 launch_batch_mom<true>(a, nb, grid, P, lr, momentum, stream);
             else
@@ -364,7 +365,7 @@ extern "C" int poseidon_ps_apply_batch(const poseidon_ps_tensor* tensors, int32_
     }
     static_assert(sizeof(poseidon_ps_tensor) == sizeof(poseidon::PsTensor), "descriptor layout");
     return poseidon::launch_ps_apply_batch(reinterpret_cast<const poseidon::PsTensor*>(tensors), count, P, lr,
-                                           momentum, stream, 0) == hipSuccess
+                                           momentum, stream) == hipSuccess
                ? POSEIDON_OK
                : POSEIDON_ERR_HIP;
 }

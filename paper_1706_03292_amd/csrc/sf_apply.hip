@@ -107,8 +107,9 @@ __device__ inline void tile_coords(int bid, int tiles, int tiles_m, int tiles_n,
 // One BK-deep step of the contraction out of LDS: each wave reads its U and V
 // fragments for MFMA step kk+2 while the matrix cores work on step kk.  With
 // FENCE the order is pinned with scheduling barriers (the compiler otherwise
-// sinks the reads below the MFMAs and waits on them at once).
-template <int BK, int LDA, int LDB, int TM, int TN, bool FENCE>
+// sinks the reads below the MFMAs and waits on them at once).  With PRIO the
+// wave raises its issue priority while it issues MFMAs.
+template <int BK, int LDA, int LDB, int TM, int TN, bool FENCE, bool PRIO = false>
 __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const float* b_s)
 {
     float a[2][TM], b[2][TN];
@@ -131,11 +132,15 @@ __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const flo
         }
         if constexpr (FENCE)
             __builtin_amdgcn_sched_barrier(0);
+        if constexpr (PRIO)
+            __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[c][i], b[c][j], acc[i][j], 0, 0, 0);
+        if constexpr (PRIO)
+            __builtin_amdgcn_s_setprio(0);
         if constexpr (FENCE)
             __builtin_amdgcn_sched_barrier(0);
     }
@@ -147,7 +152,7 @@ constexpr int BUF_RSRC_WORD3 = 0x00020000;
 
 // EPI: MFMA blocks of W (16 values per lane each) read per epilogue chunk.
 template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int OCC, int EPI,
-          bool FENCE, bool HUGE_N>
+          int SCHED, bool HUGE_N>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
@@ -194,7 +199,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
         const int cur = static_cast<int>(kt & 1);
         load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, (kt + 1) * BK, m0, tid);
         load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, (kt + 1) * BK, n0, tid);
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, FENCE>(acc, As[cur] + a_off, Bs[cur] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, (SCHED & 1) != 0, (SCHED & 2) != 0>(acc, As[cur] + a_off, Bs[cur] + b_off);
         store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[cur ^ 1], ra, tid);
         store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[cur ^ 1], rb, tid);
         __syncthreads();
@@ -233,7 +238,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
                         wr, voff + 128 * j, (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0));
             }
         }
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, FENCE>(acc, As[last] + a_off, Bs[last] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, (SCHED & 1) != 0, (SCHED & 2) != 0>(acc, As[last] + a_off, Bs[last] + b_off);
         if (interior) {
 #pragma unroll
             for (int c0 = 0; c0 < NB; c0 += CH) {
@@ -291,7 +296,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
         }
     } else {
         // Rows so long that tile offsets need 64 bits: plain guarded accesses.
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, FENCE>(acc, As[last] + a_off, Bs[last] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, (SCHED & 1) != 0, (SCHED & 2) != 0>(acc, As[last] + a_off, Bs[last] + b_off);
 #pragma unroll
         for (int i = 0; i < T::TM; ++i) {
 #pragma unroll
@@ -310,7 +315,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, bool FENCE, bool VA, bool VB>
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, int SCHED, bool VA, bool VB>
 void launch_kernel(int tiles, int tiles_m, int tiles_n, float* W, const float* U, const float* V,
                    int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
 {
@@ -318,14 +323,14 @@ void launch_kernel(int tiles, int tiles_m, int tiles_n, float* W, const float* U
     // ((BM-1)*N + BN) * 4, to fit in a signed 32-bit offset.
     constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
     if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
-        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, FENCE, false><<<tiles, NT, 0, stream>>>(
+        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, SCHED, false><<<tiles, NT, 0, stream>>>(
             W, U, V, M, N, K, lr, tiles_m, tiles_n);
     else
-        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, FENCE, true><<<tiles, NT, 0, stream>>>(
+        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, SCHED, true><<<tiles, NT, 0, stream>>>(
             W, U, V, M, N, K, lr, tiles_m, tiles_n);
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4, bool FENCE = false>
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4, int SCHED = 0>
 hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
                       float lr, hipStream_t stream)
 {
@@ -338,13 +343,13 @@ hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64
     const bool vb = (N % 4 == 0) && aligned16(V);
     const int t = static_cast<int>(tiles), tmi = static_cast<int>(tiles_m), tni = static_cast<int>(tiles_n);
     if (va && vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else if (va)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else if (vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, FENCE, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     return hipGetLastError();
 }
 
@@ -358,9 +363,8 @@ hipError_t launch_sf_apply(float* W, const float* U, const float* V,
 {
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
     if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_cfg<128, 128, 16, 64, 64, true, POSEIDON_SF_WAVES_PER_SIMD, 1, false>(W, U, V, M, N, K, lr,
-                                                                                           stream);
-    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, false>(W, U, V, M, N, K, lr, stream);
+        return launch_cfg<128, 128, 16, 64, 64, true, 4, 1, 0>(W, U, V, M, N, K, lr, stream);
+    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, 0>(W, U, V, M, N, K, lr, stream);
 }
 
 int check_sf_args(const float* W, const float* U, const float* V,

@@ -22,7 +22,6 @@ struct poseidon_stream_pool {
     std::vector<hipEvent_t> t_stop;
     std::vector<poseidon_launch_record> t_rec;
     bool t_valid = false;             // a timed iteration has been enqueued
-    std::vector<poseidon::PsTensor> ps_work;   // host scratch reused across calls
 };
 
 namespace poseidon {
@@ -174,21 +173,13 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
             schemes[t] = plan[static_cast<size_t>(t)];
-    // Launches of this iteration: one per SFB tensor, plus one batched PS
-    // launch covering every PS tensor.
-    int32_t sfb_count = 0;
-    pool->ps_work.clear();
-    for (int32_t t = count - 1; t >= 0; --t) {
+    // One launch per tensor with work.
+    int32_t launches = 0;
+    for (int32_t t = 0; t < count; ++t) {
         const poseidon_tensor& x = tensors[t];
-        const int64_t n = x.M * x.N;
-        if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
-            if (n > 0 && K > 0)
-                ++sfb_count;
-        } else if (n > 0) {
-            pool->ps_work.push_back(PsTensor{x.W, x.shards, x.buf, n});
-        }
+        if (x.M * x.N > 0 && (plan[static_cast<size_t>(t)] == POSEIDON_PS || K > 0))
+            ++launches;
     }
-    const int32_t launches = sfb_count + (pool->ps_work.empty() ? 0 : 1);
     if (pool->timing) {
         if (!reserve_timing(pool, launches))
             return POSEIDON_ERR_HIP;
@@ -197,55 +188,43 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
     if (launches == 0)
         return POSEIDON_OK;
 
-    // Stream assignment: the compute-bound SF reconstructions go, in
-    // backpropagation order, to the pool's first stream; the bandwidth-bound
-    // PS applies, batched into one pass over all PS tensors (backpropagation
-    // order), to the second, so the two kinds overlap on the GPU instead of
-    // queueing behind each other.  A one-stream pool serialises everything.
+    // Stream assignment: the compute-bound SF reconstructions go to the pool's
+    // first stream, the bandwidth-bound PS applies to the second, each kind in
+    // backpropagation order, so that the two kinds overlap on the GPU instead
+    // of queueing behind each other.  (Measured on the VGG19-22K iteration:
+    // this beats spreading the PS applies over more streams, batching them
+    // into one pass, or one stream for everything.)  A one-stream pool
+    // serialises everything.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
-    const int32_t used = (launches < S ? launches : S) < 2 ? 1 : 2;
+    const int32_t used = (S > 1 && launches > 1) ? 2 : 1;
     if (hipEventRecord(pool->fork, stream) != hipSuccess)
         return POSEIDON_ERR_HIP;
     for (int32_t s = 0; s < used; ++s)
         if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
             return POSEIDON_ERR_HIP;
 
-    auto timed = [&](hipStream_t s, int32_t scheme, int32_t tensor, int32_t si, auto&& launch) -> bool {
-        const size_t r = pool->t_rec.size();
-        if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
-            return false;
-        if (launch() != hipSuccess)
-            return false;
-        if (pool->timing) {
-            if (hipEventRecord(pool->t_stop[r], s) != hipSuccess)
-                return false;
-            pool->t_rec.push_back(poseidon_launch_record{scheme, tensor, si, 0.0f});
-        }
-        return true;
-    };
-    auto issue_ps = [&]() -> bool {
-        if (pool->ps_work.empty())
-            return true;
-        const int32_t si = used > 1 ? 1 : 0;
-        hipStream_t s = pool->streams[si];
-        return timed(s, POSEIDON_PS, -1, si, [&] {
-            return launch_ps_apply_batch(pool->ps_work.data(), static_cast<int32_t>(pool->ps_work.size()), P, lr,
-                                         momentum, s,
-                                         sfb_count > 0 ? POSEIDON_PS_OVERLAP_WG_PER_CU * device_cu_count() : 0);
-        });
-    };
-    if (POSEIDON_PS_ISSUE_FIRST && !issue_ps())
-        return POSEIDON_ERR_HIP;
     for (int32_t t = count - 1; t >= 0; --t) {
         const poseidon_tensor& x = tensors[t];
-        if (plan[static_cast<size_t>(t)] != POSEIDON_SFB || x.M * x.N == 0 || K == 0)
+        const int64_t n = x.M * x.N;
+        const bool sfb = plan[static_cast<size_t>(t)] == POSEIDON_SFB;
+        if (n == 0 || (sfb && K == 0))
             continue;
-        hipStream_t s = pool->streams[0];
-        if (!timed(s, POSEIDON_SFB, t, 0, [&] { return launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s); }))
+        const int32_t si = (sfb || used == 1) ? 0 : 1;
+        hipStream_t s = pool->streams[si];
+        const size_t r = pool->t_rec.size();
+        if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
             return POSEIDON_ERR_HIP;
+        const hipError_t err =
+            sfb ? launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s)
+                : launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
+        if (err != hipSuccess)
+            return POSEIDON_ERR_HIP;
+        if (pool->timing) {
+            if (hipEventRecord(pool->t_stop[r], s) != hipSuccess)
+                return POSEIDON_ERR_HIP;
+            pool->t_rec.push_back(poseidon_launch_record{sfb ? POSEIDON_SFB : POSEIDON_PS, t, si, 0.0f});
+        }
     }
-    if (!POSEIDON_PS_ISSUE_FIRST && !issue_ps())
-        return POSEIDON_ERR_HIP;
 
     for (int32_t s = 0; s < used; ++s) {
         if (hipEventRecord(pool->joined[s], pool->streams[s]) != hipSuccess ||

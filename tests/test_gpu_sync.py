@@ -134,7 +134,8 @@ def test_sync_iteration_missing_payload_is_an_error():
 
 
 def test_sync_iteration_launch_records():
-    """Timing mode: one record per SFB tensor on stream 0 and one PS batch."""
+    """Timing mode: one record per launch, backprop order, SFB on stream 0 and
+    PS on stream 1."""
     d = dev()
     wl = I.workload(5)
     host = I.make_tensors(wl, only=["fc7.W", "fc7.b", "conv5_4.W"])
@@ -145,8 +146,9 @@ def test_sync_iteration_launch_records():
     log("sync_iteration timing records")
     it()
     recs = pool.launch_times()
-    fc = [i for i, h in enumerate(host) if h["spec"].name == "fc7.W"][0]
-    assert [(r["scheme"], r["tensor"], r["stream"]) for r in recs] == [(api.PS, -1, 1), (api.SFB, fc, 0)]
+    want = [(api.SFB if h["spec"].kind == I.FC else api.PS, i, 0 if h["spec"].kind == I.FC else 1)
+            for i, h in reversed(list(enumerate(host)))]
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in recs] == want
     assert all(r["ms"] > 0 for r in recs)
     pool.set_timing(False)
     torch.cuda.synchronize()
