@@ -77,6 +77,30 @@ int poseidon_sf_apply(float* W, const float* U, const float* V,
                       int64_t M, int64_t N, int64_t K, float lr,
                       hipStream_t stream);
 
+/* One fully-connected layer of a grouped SF reconstruction. */
+typedef struct poseidon_sf_tensor {
+    float*       W;   /* M x N row-major, updated in place */
+    const float* U;   /* K x M row-major */
+    const float* V;   /* K x N row-major */
+    int64_t      M;
+    int64_t      N;
+} poseidon_sf_tensor;
+
+/*
+ * poseidon_sf_apply for several FC layers that share K (the same P workers and
+ * batch B) in one pass: each layer is updated exactly as by
+ * poseidon_sf_apply(W, U, V, M, N, K, lr).  Their tiles form one work list
+ * (in the order given), so the GPU is never left half idle between layers;
+ * layers whose rows are too long for the grouped kernel, and groups too small
+ * to fill the GPU, are launched one by one instead.  The W arrays must not
+ * overlap each other or any U, V.  All layers are validated before anything
+ * is enqueued.  Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (as for
+ * poseidon_sf_apply, for any layer; count < 0; NULL layers with count > 0;
+ * overlapping W) or POSEIDON_ERR_HIP.
+ */
+int poseidon_sf_apply_batch(const poseidon_sf_tensor* layers, int32_t count, int64_t K, float lr,
+                            hipStream_t stream);
+
 /*
  * Parameter-server aggregation and apply: the KV store's Receive of all P
  * workers' updates followed by their application (Sec. 2.1 "Parameter
@@ -182,10 +206,12 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation"; Alg. 2 TRAIN/sync): tensors[] is given in forward order
  * and issued from the last to the first (backpropagation order).  For each
  * tensor the scheme is Alg. 1's (FC: poseidon_hybcomm_choose(M, N, B, P);
- * other kinds: PS) and its update is enqueued, in backpropagation order,
- * on the pool's first stream for SFB (bound by the matrix cores) or on its
- * second stream for PS (bound by memory bandwidth), so that the two kinds
- * overlap; a one-stream pool runs everything in order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
+ * other kinds: PS).  All SFB updates (bound by the matrix cores) are
+ * enqueued as one grouped reconstruction (poseidon_sf_apply_batch, layers in
+ * backpropagation order) on the pool's first stream; the PS updates (bound
+ * by memory bandwidth) are enqueued one per tensor, in backpropagation order,
+ * on its second stream, so that the two kinds overlap; a one-stream pool runs
+ * everything in order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
  * poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf) (momentum is used
  * only when buf != NULL).  Every pool stream first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so
@@ -211,8 +237,8 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 
 /* One launch of the last iteration run with timing enabled. */
 typedef struct poseidon_launch_record {
-    int32_t scheme;   /* POSEIDON_SFB or POSEIDON_PS */
-    int32_t tensor;   /* index into that call's tensors[] */
+    int32_t scheme;   /* POSEIDON_SFB (the grouped SF launch) or POSEIDON_PS (one tensor) */
+    int32_t tensor;   /* index into that call's tensors[] for PS, -1 for the SF group */
     int32_t stream;   /* pool stream index */
     float   ms;       /* time between the events around the launch */
 } poseidon_launch_record;

@@ -20,7 +20,7 @@ SFB = 1
 KIND_FC = 0
 KIND_OTHER = 1
 
-EXPORTS = ("poseidon_sf_apply", "poseidon_ps_apply", "poseidon_ps_apply_batch",
+EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_batch", "poseidon_ps_apply", "poseidon_ps_apply_batch",
            "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_pool_create",
            "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_pool_set_timing",
            "poseidon_pool_launch_times", "poseidon_abi_version")
@@ -32,6 +32,12 @@ class PoseidonTensor(ctypes.Structure):
                 ("W", ctypes.c_void_p), ("M", ctypes.c_int64), ("N", ctypes.c_int64),
                 ("U", ctypes.c_void_p), ("V", ctypes.c_void_p),
                 ("shards", ctypes.c_void_p), ("buf", ctypes.c_void_p)]
+
+
+class PoseidonSfTensor(ctypes.Structure):
+    """Mirror of ``poseidon_sf_tensor`` in include/poseidon.h."""
+    _fields_ = [("W", ctypes.c_void_p), ("U", ctypes.c_void_p), ("V", ctypes.c_void_p),
+                ("M", ctypes.c_int64), ("N", ctypes.c_int64)]
 
 
 class PoseidonPsTensor(ctypes.Structure):
@@ -66,6 +72,7 @@ def lib() -> ctypes.CDLL:
     L.poseidon_pool_destroy.argtypes = [vp]
     L.poseidon_sync_iteration.argtypes = [vp, ctypes.POINTER(PoseidonTensor), i32, i64, i32,
                                           f32, f32, vp, ctypes.POINTER(i32)]
+    L.poseidon_sf_apply_batch.argtypes = [ctypes.POINTER(PoseidonSfTensor), i32, i64, f32, vp]
     L.poseidon_ps_apply_batch.argtypes = [ctypes.POINTER(PoseidonPsTensor), i32, i32, f32, f32, vp]
     L.poseidon_pool_set_timing.argtypes = [vp, i32]
     L.poseidon_pool_launch_times.argtypes = [vp, ctypes.POINTER(PoseidonLaunchRecord), i32,

@@ -74,6 +74,33 @@ def sf_apply(W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, lr: float, strea
             _stream_handle(stream, W.device)))
 
 
+def sf_apply_batch(layers: list, lr: float, stream=None) -> None:
+    """poseidon_sf_apply for several FC layers with the same K in one pass
+    (poseidon_sf_apply_batch).  ``layers`` is a list of (W, U, V)."""
+    if not layers:
+        return
+    arr = (L.PoseidonSfTensor * len(layers))()
+    K = None
+    dev = None
+    for i, (W, U, V) in enumerate(layers):
+        _dev_f32("W", W), _dev_f32("U", U), _dev_f32("V", V)
+        _same_device(W, U, V)
+        dev = dev or W.device
+        if W.device != dev:
+            raise ValueError("all layers must be on one device")
+        if W.dim() != 2 or U.dim() != 2 or V.dim() != 2:
+            raise ValueError("W, U, V must be 2-D")
+        M, N = W.shape
+        k = U.shape[0]
+        K = k if K is None else K
+        if k != K or U.shape != (K, M) or V.shape != (K, N):
+            raise ValueError(f"layer {i}: U must be {K} x {M} and V {K} x {N}")
+        arr[i] = L.PoseidonSfTensor(W.data_ptr(), U.data_ptr(), V.data_ptr(), M, N)
+    with torch.cuda.device(dev):
+        _check("poseidon_sf_apply_batch", L.lib().poseidon_sf_apply_batch(
+            arr, len(layers), K, float(lr), _stream_handle(stream, dev)))
+
+
 def ps_apply(W: torch.Tensor, shards: torch.Tensor, lr: float, momentum: float = 0.0,
              buf: torch.Tensor | None = None, stream=None) -> None:
     """buf = momentum*buf + shards.sum(0); W -= lr*buf, in place (poseidon_ps_apply).

@@ -30,6 +30,20 @@ hipError_t launch_sf_apply(float* W, const float* U, const float* V,
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
                            float lr, float momentum, float* buf, hipStream_t stream);
 
+// One FC layer of a grouped SF launch (same layout as poseidon_sf_tensor).
+struct SfTensor {
+    float* W;
+    const float* U;
+    const float* V;
+    int64_t M;
+    int64_t N;
+};
+constexpr int SF_BATCH_MAX = 16;   // layers per grouped launch (kernel-argument space)
+
+// Every layer with work, grouped into as few launches as possible (validated).
+hipError_t launch_sf_apply_batch(const SfTensor* layers, int32_t count, int64_t K, float lr,
+                                 hipStream_t stream);
+
 // One dense tensor of a batched PS apply (same layout as poseidon_ps_tensor).
 struct PsTensor {
     float* W;

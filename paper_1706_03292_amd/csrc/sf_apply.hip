@@ -22,8 +22,10 @@
 //
 // Tile order: the hardware hands consecutive workgroups to the 8 XCDs in turn,
 // and each XCD has its own L2.  Workgroup ids are remapped so that every XCD
-// owns one contiguous run of tiles, walked in groups of GROUP_M tile rows, so
+// owns one contiguous run of tiles, walked a group of tile rows at a time, so
 // the tiles an XCD runs at the same time share U and V panels in its L2.
+#include <vector>
+
 #include "common.h"
 
 namespace poseidon {
@@ -33,7 +35,6 @@ typedef float f16v __attribute__((ext_vector_type(16)));
 
 constexpr int LDS_PAD = 4;    // floats of padding per LDS row (keeps 16-byte alignment)
 constexpr int NUM_XCD = 8;    // MI355X: 8 accelerator complex dies, one L2 each
-constexpr int GROUP_M = 8;    // tile rows walked together inside an XCD's run
 
 template <int BM, int BN, int BK, int WM, int WN>
 struct SfTile {
@@ -54,10 +55,11 @@ struct SfTile {
 // Load one BK x (4*COLS4) slice of a K-major operand X (row length ld = its
 // number of columns) into registers: group j of this thread covers row
 // g / COLS4 and columns 4*(g % COLS4) .. +3 with g = tid + j*THREADS.
-// Out-of-range rows/columns read as 0, which adds nothing to the sum.
-template <int NV4, int COLS4, int THREADS, bool VEC>
+// Out-of-range rows/columns read as 0, which adds nothing to the sum.  vec
+// (uniform; a constant in the single-layer kernels) selects 16-byte loads.
+template <int NV4, int COLS4, int THREADS>
 __device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int64_t ld,
-                                  int64_t rows, int64_t k0, int64_t c0, int tid)
+                                  int64_t rows, int64_t k0, int64_t c0, int tid, bool vec)
 {
 #pragma unroll
     for (int j = 0; j < NV4; ++j) {
@@ -65,7 +67,7 @@ __device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int
         const int64_t k = k0 + g / COLS4;
         const int64_t c = c0 + 4 * (g % COLS4);
         const float* src = X + k * ld + c;
-        if constexpr (VEC) {
+        if (vec) {
             // ld % 4 == 0 and X 16-byte aligned: a group is wholly in or out.
             r[j] = (k < rows && c < ld) ? *reinterpret_cast<const f4*>(src) : f4{0.f, 0.f, 0.f, 0.f};
         } else {
@@ -88,28 +90,33 @@ __device__ inline void store_panel(float* lds, const f4 (&r)[NV4], int tid)
     }
 }
 
-// Workgroup id -> (tile row, tile column): contiguous runs per XCD, GROUP_M
-// tile rows at a time inside a run.
+// Workgroup id -> (tile row, tile column): contiguous runs per XCD, GM tile
+// rows at a time inside a run (GM = 0: plain row-major order, no remap).
+template <int GM>
 __device__ inline void tile_coords(int bid, int tiles, int tiles_m, int tiles_n, int& tm, int& tn)
 {
-    const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
-    const int x = bid % NUM_XCD, j = bid / NUM_XCD;
-    const int t = x * q + (x < r ? x : r) + j;
-    const int per_group = GROUP_M * tiles_n;
-    const int g = t / per_group;
-    const int first_m = g * GROUP_M;
-    const int rows = (tiles_m - first_m) < GROUP_M ? (tiles_m - first_m) : GROUP_M;
-    const int in = t - g * per_group;
-    tm = first_m + in % rows;
-    tn = in / rows;
+    if constexpr (GM == 0) {
+        tm = bid / tiles_n;
+        tn = bid % tiles_n;
+    } else {
+        const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
+        const int x = bid % NUM_XCD, j = bid / NUM_XCD;
+        const int t = x * q + (x < r ? x : r) + j;
+        const int per_group = GM * tiles_n;
+        const int g = t / per_group;
+        const int first_m = g * GM;
+        const int rows = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
+        const int in = t - g * per_group;
+        tm = first_m + in % rows;
+        tn = in / rows;
+    }
 }
 
 // One BK-deep step of the contraction out of LDS: each wave reads its U and V
-// fragments for MFMA step kk+2 while the matrix cores work on step kk.  With
-// FENCE the order is pinned with scheduling barriers (the compiler otherwise
-// sinks the reads below the MFMAs and waits on them at once).  With PRIO the
-// wave raises its issue priority while it issues MFMAs.
-template <int BK, int LDA, int LDB, int TM, int TN, bool FENCE, bool PRIO = false>
+// fragments for MFMA step kk+2 while the matrix cores work on step kk (the
+// compiler interleaves the reads with the MFMAs; pinning other orders with
+// scheduling barriers or priorities measured no faster).
+template <int BK, int LDA, int LDB, int TM, int TN>
 __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const float* b_s)
 {
     float a[2][TM], b[2][TN];
@@ -130,19 +137,11 @@ __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const flo
             for (int j = 0; j < TN; ++j)
                 b[c ^ 1][j] = b_s[(kk + 2) * LDB + 32 * j];
         }
-        if constexpr (FENCE)
-            __builtin_amdgcn_sched_barrier(0);
-        if constexpr (PRIO)
-            __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[c][i], b[c][j], acc[i][j], 0, 0, 0);
-        if constexpr (PRIO)
-            __builtin_amdgcn_s_setprio(0);
-        if constexpr (FENCE)
-            __builtin_amdgcn_sched_barrier(0);
     }
 }
 
@@ -150,13 +149,11 @@ __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const flo
 // buffer builtins move 32-bit integers: values are bit-cast, never converted.
 constexpr int BUF_RSRC_WORD3 = 0x00020000;
 
-// EPI: MFMA blocks of W (16 values per lane each) read per epilogue chunk.
-template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int OCC, int EPI,
-          int SCHED, bool HUGE_N>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
-    float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
-    int64_t M, int64_t N, int64_t K, float lr, int tiles_m, int tiles_n)
+// One BM x BN tile of W: the whole K loop and the fused update.  EPI: MFMA
+// blocks of W (16 values per lane each) read per epilogue chunk.
+template <int BM, int BN, int BK, int WM, int WN, bool PREFETCH_W, int EPI, bool HUGE_N>
+__device__ inline void sf_tile(float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
+                               int64_t M, int64_t N, int64_t K, float lr, int tm, int tn, bool va, bool vb)
 {
     using T = SfTile<BM, BN, BK, WM, WN>;
     __shared__ float As[2][BK * T::LDA];
@@ -165,8 +162,6 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = tid >> 6;
-    int tm, tn;
-    tile_coords(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
     const int64_t m0 = static_cast<int64_t>(tm) * BM;
     const int64_t n0 = static_cast<int64_t>(tn) * BN;
     const int wm = (wave / T::NWN) * WM;
@@ -187,8 +182,8 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     f4 ra[T::A_V4], rb[T::B_V4];
     const int64_t nkt = (K + BK - 1) / BK;
 
-    load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, 0, m0, tid);
-    load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, 0, n0, tid);
+    load_panel<T::A_V4, BM / 4, T::THREADS>(ra, U, M, K, 0, m0, tid, va);
+    load_panel<T::B_V4, BN / 4, T::THREADS>(rb, V, N, K, 0, n0, tid, vb);
     store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[0], ra, tid);
     store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[0], rb, tid);
     __syncthreads();
@@ -197,9 +192,9 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     const int b_off = lrow * T::LDB + wn + lcol;
     for (int64_t kt = 0; kt + 1 < nkt; ++kt) {
         const int cur = static_cast<int>(kt & 1);
-        load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, (kt + 1) * BK, m0, tid);
-        load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, (kt + 1) * BK, n0, tid);
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, (SCHED & 1) != 0, (SCHED & 2) != 0>(acc, As[cur] + a_off, Bs[cur] + b_off);
+        load_panel<T::A_V4, BM / 4, T::THREADS>(ra, U, M, K, (kt + 1) * BK, m0, tid, va);
+        load_panel<T::B_V4, BN / 4, T::THREADS>(rb, V, N, K, (kt + 1) * BK, n0, tid, vb);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As[cur] + a_off, Bs[cur] + b_off);
         store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[cur ^ 1], ra, tid);
         store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[cur ^ 1], rb, tid);
         __syncthreads();
@@ -238,7 +233,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
                         wr, voff + 128 * j, (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0));
             }
         }
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, (SCHED & 1) != 0, (SCHED & 2) != 0>(acc, As[last] + a_off, Bs[last] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As[last] + a_off, Bs[last] + b_off);
         if (interior) {
 #pragma unroll
             for (int c0 = 0; c0 < NB; c0 += CH) {
@@ -296,7 +291,7 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
         }
     } else {
         // Rows so long that tile offsets need 64 bits: plain guarded accesses.
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN, (SCHED & 1) != 0, (SCHED & 2) != 0>(acc, As[last] + a_off, Bs[last] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As[last] + a_off, Bs[last] + b_off);
 #pragma unroll
         for (int i = 0; i < T::TM; ++i) {
 #pragma unroll
@@ -315,7 +310,71 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, int SCHED, bool VA, bool VB>
+template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int OCC, int EPI,
+          int GM, bool HUGE_N>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
+    float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
+    int64_t M, int64_t N, int64_t K, float lr, int tiles_m, int tiles_n)
+{
+    int tm, tn;
+    tile_coords<GM>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
+    sf_tile<BM, BN, BK, WM, WN, PREFETCH_W, EPI, HUGE_N>(W, U, V, M, N, K, lr, tm, tn, VEC_A, VEC_B);
+}
+
+// ---------------------------------------------------------------------------
+// Several layers in one launch (same K): one tile list, so the chip is filled
+// by the tiles of the next layer while the last ones of a layer finish,
+// instead of every layer ending in a partly idle round.  Layer descriptors
+// travel by value in the kernel arguments; the XCD-aware order runs over the
+// combined list (layer by layer, in the order given), and inside a layer tile
+// rows are walked 8 at a time.
+// ---------------------------------------------------------------------------
+struct SfBatchItem {
+    float* W;
+    const float* U;
+    const float* V;
+    int64_t M;
+    int64_t N;
+    int32_t first_tile;
+    int32_t tiles_m;
+    int32_t tiles_n;
+    int32_t vec;   // bit 0: U rows 16-byte loadable, bit 1: V rows
+};
+
+struct SfBatchArgs {
+    SfBatchItem item[SF_BATCH_MAX];
+    int32_t count;
+    int32_t total_tiles;
+};
+
+template <int BM, int BN, int BK, int WM, int WN, bool PREFETCH_W, int OCC, int EPI>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K,
+                                                                           float lr)
+{
+    const int tiles = args.total_tiles;
+    const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
+    const int x = blockIdx.x % NUM_XCD, j = blockIdx.x / NUM_XCD;
+    const int t = x * q + (x < r ? x : r) + j;
+    int l = 0;
+    while (l + 1 < args.count && t >= args.item[l + 1].first_tile)
+        ++l;
+    const int local = t - args.item[l].first_tile;
+    const int tiles_m = args.item[l].tiles_m, tiles_n = args.item[l].tiles_n;
+    constexpr int G = 8;
+    const int per_group = G * tiles_n;
+    const int g = local / per_group;
+    const int first_m = g * G;
+    const int rows = (tiles_m - first_m) < G ? (tiles_m - first_m) : G;
+    const int in = local - g * per_group;
+    sf_tile<BM, BN, BK, WM, WN, PREFETCH_W, EPI, false>(args.item[l].W, args.item[l].U, args.item[l].V,
+                                                       args.item[l].M, args.item[l].N, K, lr, first_m + in % rows,
+                                                       in / rows, (args.item[l].vec & 1) != 0,
+                                                       (args.item[l].vec & 2) != 0);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, int GM, bool VA, bool VB>
 void launch_kernel(int tiles, int tiles_m, int tiles_n, float* W, const float* U, const float* V,
                    int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
 {
@@ -323,14 +382,14 @@ void launch_kernel(int tiles, int tiles_m, int tiles_n, float* W, const float* U
     // ((BM-1)*N + BN) * 4, to fit in a signed 32-bit offset.
     constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
     if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
-        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, SCHED, false><<<tiles, NT, 0, stream>>>(
+        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, GM, false><<<tiles, NT, 0, stream>>>(
             W, U, V, M, N, K, lr, tiles_m, tiles_n);
     else
-        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, SCHED, true><<<tiles, NT, 0, stream>>>(
+        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, GM, true><<<tiles, NT, 0, stream>>>(
             W, U, V, M, N, K, lr, tiles_m, tiles_n);
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4, int SCHED = 0>
+template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4, int GM = 8>
 hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
                       float lr, hipStream_t stream)
 {
@@ -343,13 +402,13 @@ hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64
     const bool vb = (N % 4 == 0) && aligned16(V);
     const int t = static_cast<int>(tiles), tmi = static_cast<int>(tiles_m), tni = static_cast<int>(tiles_n);
     if (va && vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else if (va)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else if (vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     else
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, SCHED, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
+        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
     return hipGetLastError();
 }
 
@@ -363,8 +422,63 @@ hipError_t launch_sf_apply(float* W, const float* U, const float* V,
 {
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
     if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_cfg<128, 128, 16, 64, 64, true, 4, 1, 0>(W, U, V, M, N, K, lr, stream);
-    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, 0>(W, U, V, M, N, K, lr, stream);
+        return launch_cfg<128, 128, 16, 64, 64, true, 4, 1, 8>(W, U, V, M, N, K, lr, stream);
+    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, 8>(W, U, V, M, N, K, lr, stream);
+}
+
+// Grouped launch: every layer whose tile offsets fit 32 bits joins one tile
+// list (128 x 128 tiles) when the group has at least two tiles per CU; the
+// others, and groups too small to fill the chip, take per-layer launches.
+hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, float lr, hipStream_t stream)
+{
+    constexpr int BM = 128, BN = 128;
+    std::vector<int32_t> grouped;
+    int64_t tiles = 0;
+    for (int32_t i = 0; i < count; ++i) {
+        if (t[i].M == 0 || t[i].N == 0 || K == 0)
+            continue;
+        const int64_t tl = ((t[i].M + BM - 1) / BM) * ((t[i].N + BN - 1) / BN);
+        if ((static_cast<int64_t>(BM) * t[i].N + BN) * 4 < 0x7fffffffLL && tiles + tl <= INT32_MAX) {
+            grouped.push_back(i);
+            tiles += tl;
+        } else {
+            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream);
+            if (e != hipSuccess)
+                return e;
+        }
+    }
+    if (tiles < 2 * static_cast<int64_t>(device_cu_count())) {
+        for (int32_t i : grouped) {
+            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream);
+            if (e != hipSuccess)
+                return e;
+        }
+        return hipSuccess;
+    }
+    for (size_t g0 = 0; g0 < grouped.size(); g0 += SF_BATCH_MAX) {
+        SfBatchArgs a{};
+        int32_t first = 0;
+        for (size_t g = g0; g < grouped.size() && g < g0 + SF_BATCH_MAX; ++g) {
+            const SfTensor& x = t[grouped[g]];
+            SfBatchItem& it = a.item[a.count++];
+            it.W = x.W;
+            it.U = x.U;
+            it.V = x.V;
+            it.M = x.M;
+            it.N = x.N;
+            it.tiles_m = static_cast<int32_t>((x.M + BM - 1) / BM);
+            it.tiles_n = static_cast<int32_t>((x.N + BN - 1) / BN);
+            it.first_tile = first;
+            it.vec = ((x.M % 4 == 0) && aligned16(x.U) ? 1 : 0) | ((x.N % 4 == 0) && aligned16(x.V) ? 2 : 0);
+            first += it.tiles_m * it.tiles_n;
+        }
+        a.total_tiles = first;
+        sf_apply_batch_kernel<BM, BN, 16, 64, 64, true, 4, 1><<<first, 256, 0, stream>>>(a, K, lr);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
 }
 
 int check_sf_args(const float* W, const float* U, const float* V,
@@ -393,6 +507,33 @@ extern "C" int poseidon_sf_apply(float* W, const float* U, const float* V,
     if (rc != POSEIDON_OK || M == 0 || N == 0 || K == 0)
         return rc;
     return poseidon::launch_sf_apply(W, U, V, M, N, K, lr, stream) == hipSuccess
+               ? POSEIDON_OK
+               : POSEIDON_ERR_HIP;
+}
+
+extern "C" int poseidon_sf_apply_batch(const poseidon_sf_tensor* layers, int32_t count, int64_t K, float lr,
+                                       hipStream_t stream)
+{
+    if (count < 0 || (count > 0 && !layers) || K < 0)
+        return POSEIDON_ERR_INVALID_ARG;
+    for (int32_t i = 0; i < count; ++i) {
+        const poseidon_sf_tensor& x = layers[i];
+        const int rc = poseidon::check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
+        if (rc != POSEIDON_OK)
+            return rc;
+        for (int32_t j = 0; j < count; ++j) {   // no W may overlap another layer's W, U or V
+            if (j == i)
+                continue;
+            const poseidon_sf_tensor& y = layers[j];
+            const int64_t wb = x.M * x.N * 4;
+            if (poseidon::overlaps(x.W, wb, y.W, y.M * y.N * 4) || poseidon::overlaps(x.W, wb, y.U, K * y.M * 4) ||
+                poseidon::overlaps(x.W, wb, y.V, K * y.N * 4))
+                return POSEIDON_ERR_INVALID_ARG;
+        }
+    }
+    static_assert(sizeof(poseidon_sf_tensor) == sizeof(poseidon::SfTensor), "descriptor layout");
+    return poseidon::launch_sf_apply_batch(reinterpret_cast<const poseidon::SfTensor*>(layers), count, K, lr,
+                                           stream) == hipSuccess
                ? POSEIDON_OK
                : POSEIDON_ERR_HIP;
 }

@@ -22,6 +22,7 @@ struct poseidon_stream_pool {
     std::vector<hipEvent_t> t_stop;
     std::vector<poseidon_launch_record> t_rec;
     bool t_valid = false;             // a timed iteration has been enqueued
+    std::vector<poseidon::SfTensor> sf_work;   // host scratch reused across calls
 };
 
 namespace poseidon {
@@ -173,13 +174,22 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
             schemes[t] = plan[static_cast<size_t>(t)];
-    // One launch per tensor with work.
-    int32_t launches = 0;
-    for (int32_t t = 0; t < count; ++t) {
+    // Launches: every SFB tensor in one grouped SF launch (backpropagation
+    // order of the tile list), every PS tensor on its own.
+    pool->sf_work.clear();
+    int32_t ps_launches = 0;
+    for (int32_t t = count - 1; t >= 0; --t) {
         const poseidon_tensor& x = tensors[t];
-        if (x.M * x.N > 0 && (plan[static_cast<size_t>(t)] == POSEIDON_PS || K > 0))
-            ++launches;
+        if (x.M * x.N == 0)
+            continue;
+        if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
+            if (K > 0)
+                pool->sf_work.push_back(SfTensor{x.W, x.U, x.V, x.M, x.N});
+        } else {
+            ++ps_launches;
+        }
     }
+    const int32_t launches = ps_launches + (pool->sf_work.empty() ? 0 : 1);
     if (pool->timing) {
         if (!reserve_timing(pool, launches))
             return POSEIDON_ERR_HIP;
@@ -189,12 +199,9 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
         return POSEIDON_OK;
 
     // Stream assignment: the compute-bound SF reconstructions go to the pool's
-    // first stream, the bandwidth-bound PS applies to the second, each kind in
+    // first stream, the bandwidth-bound PS applies to the second, in
     // backpropagation order, so that the two kinds overlap on the GPU instead
-    // of queueing behind each other.  (Measured on the VGG19-22K iteration:
-    // this beats spreading the PS applies over more streams, batching them
-    // into one pass, or one stream for everything.)  A one-stream pool
-    // serialises everything.
+    // of queueing behind each other.  A one-stream pool serialises everything.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
     const int32_t used = (S > 1 && launches > 1) ? 2 : 1;
     if (hipEventRecord(pool->fork, stream) != hipSuccess)
@@ -203,27 +210,38 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
         if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
             return POSEIDON_ERR_HIP;
 
+    auto timed = [&](hipStream_t s, int32_t scheme, int32_t tensor, int32_t si, auto&& launch) -> bool {
+        const size_t r = pool->t_rec.size();
+        if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
+            return false;
+        if (launch() != hipSuccess)
+            return false;
+        if (pool->timing) {
+            if (hipEventRecord(pool->t_stop[r], s) != hipSuccess)
+                return false;
+            pool->t_rec.push_back(poseidon_launch_record{scheme, tensor, si, 0.0f});
+        }
+        return true;
+    };
+    if (!pool->sf_work.empty()) {
+        hipStream_t s = pool->streams[0];
+        if (!timed(s, POSEIDON_SFB, -1, 0, [&] {
+                return launch_sf_apply_batch(pool->sf_work.data(), static_cast<int32_t>(pool->sf_work.size()), K,
+                                             lr, s);
+            }))
+            return POSEIDON_ERR_HIP;
+    }
     for (int32_t t = count - 1; t >= 0; --t) {
         const poseidon_tensor& x = tensors[t];
         const int64_t n = x.M * x.N;
-        const bool sfb = plan[static_cast<size_t>(t)] == POSEIDON_SFB;
-        if (n == 0 || (sfb && K == 0))
+        if (n == 0 || plan[static_cast<size_t>(t)] != POSEIDON_PS)
             continue;
-        const int32_t si = (sfb || used == 1) ? 0 : 1;
+        const int32_t si = used == 1 ? 0 : 1;
         hipStream_t s = pool->streams[si];
-        const size_t r = pool->t_rec.size();
-        if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
+        if (!timed(s, POSEIDON_PS, t, si, [&] {
+                return launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
+            }))
             return POSEIDON_ERR_HIP;
-        const hipError_t err =
-            sfb ? launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s)
-                : launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
-        if (err != hipSuccess)
-            return POSEIDON_ERR_HIP;
-        if (pool->timing) {
-            if (hipEventRecord(pool->t_stop[r], s) != hipSuccess)
-                return POSEIDON_ERR_HIP;
-            pool->t_rec.push_back(poseidon_launch_record{sfb ? POSEIDON_SFB : POSEIDON_PS, t, si, 0.0f});
-        }
     }
 
     for (int32_t s = 0; s < used; ++s) {

@@ -37,6 +37,7 @@ def test_struct_layout_matches_header():
     assert ctypes.sizeof(L.PoseidonTensor) == 8 + 7 * 8
     assert L.PoseidonTensor.W.offset == 8 and L.PoseidonTensor.buf.offset == 56
     assert ctypes.sizeof(L.PoseidonPsTensor) == 32 and L.PoseidonPsTensor.n.offset == 24
+    assert ctypes.sizeof(L.PoseidonSfTensor) == 40 and L.PoseidonSfTensor.N.offset == 32
     assert ctypes.sizeof(L.PoseidonLaunchRecord) == 16 and L.PoseidonLaunchRecord.ms.offset == 12
 
 
@@ -70,6 +71,12 @@ def test_invalid_arguments_rejected_before_device_work():
     assert lib.poseidon_ps_apply_batch(None, 0, 2, 0.1, 0.0, None) == L.OK
     n = ctypes.c_int32()
     assert lib.poseidon_pool_launch_times(None, None, 0, ctypes.byref(n)) == L.ERR_INVALID_ARG
+    # grouped SF: negative K, a W overlapping another layer's U, empty
+    sf = (L.PoseidonSfTensor * 2)(L.PoseidonSfTensor(0x100000, 0x200000, 0x300000, 8, 8),
+                                  L.PoseidonSfTensor(0x400000, 0x100010, 0x500000, 8, 8))
+    assert lib.poseidon_sf_apply_batch(sf, 2, -1, 0.1, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_sf_apply_batch(sf, 2, 4, 0.1, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_sf_apply_batch(None, 0, 4, 0.1, None) == L.OK
 
 
 def test_hybcomm_argument_checks():

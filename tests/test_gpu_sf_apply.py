@@ -166,3 +166,40 @@ def test_sf_apply_rows_too_long_for_32bit_offsets():
                                            [0], [0])[0] for r, c in zip(rows, cols)])
     got = Wd[torch.from_numpy(rows).to(d), torch.from_numpy(cols).to(d)].cpu().numpy()
     assert_close(got, ref, W_TOL, "huge rows")
+
+
+def test_sf_apply_batch_matches_oracle_and_single_calls():
+    """Grouped launch over layers of different shapes (ragged, M % 4 != 0,
+    unaligned V): every layer as the oracle computes it, and bit-identical to
+    poseidon_sf_apply on the same layer (same K order in every tile)."""
+    d = dev()
+    shapes = [(2085, 4125), (129, 257), (4100, 2052), (21841 // 8, 1024 + 3)]
+    K = 40
+    host = [_draw(M, N, K, seed=900 + 17 * i) for i, (M, N) in enumerate(shapes)]
+    a = [(W.to(d), U.to(d), V.to(d)) for W, U, V in host]
+    a[1] = (a[1][0], a[1][1], misaligned(a[1][2]))
+    b = [(W.clone(), U, V) for W, U, V in a]
+    log(f"sf_apply_batch layers={len(a)} K={K}")
+    api.sf_apply_batch(a, 0.01)
+    for W, U, V in b:
+        api.sf_apply(W, U, V, 0.01)
+    torch.cuda.synchronize()
+    for (W0, U0, V0), (Wa, _, _), (Wb, _, _) in zip(host, a, b):
+        ref = oracle.sf_apply(W0.numpy(), U0.numpy(), V0.numpy(), 0.01)
+        assert_close(to_np(Wa), ref, W_TOL, f"batch {tuple(W0.shape)}")
+        assert torch.equal(Wa, Wb), f"batch != single for {tuple(W0.shape)}"
+
+
+def test_sf_apply_batch_small_group_and_errors():
+    d = dev()
+    host = [_draw(300, 200, 37, seed=1200), _draw(64, 96, 37, seed=1300)]
+    a = [(W.to(d), U.to(d), V.to(d)) for W, U, V in host]
+    log("sf_apply_batch small group")
+    api.sf_apply_batch(a, 0.01)        # too small to fill the GPU: per-layer launches
+    torch.cuda.synchronize()
+    for (W0, U0, V0), (Wa, _, _) in zip(host, a):
+        assert_close(to_np(Wa), oracle.sf_apply(W0.numpy(), U0.numpy(), V0.numpy(), 0.01), W_TOL, "small")
+    with pytest.raises(ValueError):
+        api.sf_apply_batch([a[0], (a[1][0], a[1][1][:5].contiguous(), a[1][2][:5].contiguous())], 0.01)
+    with pytest.raises(api.PoseidonError):
+        api.sf_apply_batch([a[0], a[0]], 0.01)          # the same W twice
