@@ -35,7 +35,8 @@ def _parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=50,
+                    help="untimed steps first (the first few dozen steps of a fresh process run a few %% slower)")
     ap.add_argument("--config", type=int, default=5, help="workload (5 = VGG19-22K full iteration)")
     ap.add_argument("--streams", type=int, default=4)
     ap.add_argument("--kernel-steps", type=int, default=None,
@@ -194,12 +195,10 @@ def main():
     for _ in range(ksteps):
         it(stream)
         for r in pool.launch_times():
-            key = "sf_group" if r["scheme"] == api.SFB else r["tensor"]
-            launch_ms[key] = launch_ms.get(key, 0.0) + r["ms"] / ksteps
+            launch_ms[r["tensor"]] = launch_ms.get(r["tensor"], 0.0) + r["ms"] / ksteps
     pool.set_timing(False)
     torch.cuda.synchronize()
 
-    # The same SF layers launched one by one (context for the grouped launch).
     fc_list = [(t["W"], t["U"], t["V"]) for t in reversed(devt) if t["spec"].kind == "fc"]
 
     # The PS applies share the GPU with the SF reconstructions during the
@@ -231,24 +230,26 @@ def main():
     ps_big_bytes = float(W_.numel()) * (4 * wl.P + (16 if b_ is not None else 8))
 
     sfb_flops = sfb_bytes = 0.0
-    ps_bytes = ps_in_iter = 0.0
+    ps_bytes = ps_in_iter = sfb_ms = 0.0
     layers = []
     fc_idx = [i for i, h in enumerate(host) if h["spec"].kind == "fc"][::-1]
     for (W, U, V), i in zip(fc_list, fc_idx):
         spec = host[i]["spec"]
         ms = _time(lambda: api.sf_apply(W, U, V, wl.lr, stream=stream))
         f = _sf_flops(spec, wl.K)
-        layers.append({"tensor": spec.name, "scheme": "SFB", "alone_ms": round(ms, 4),
-                       "alone_tflops": round(f / ms / 1e9, 2)})
+        it_ms = launch_ms.get(i, 0.0)
+        layers.append({"tensor": spec.name, "scheme": "SFB",
+                       "ms": round(it_ms, 4), "tflops": round(f / it_ms / 1e9, 2) if it_ms else None,
+                       "alone_ms": round(ms, 4), "alone_tflops": round(f / ms / 1e9, 2)})
     for i, (h, sch) in enumerate(zip(host, schemes)):
         spec = h["spec"]
         if sch == api.SFB:
             sfb_flops += _sf_flops(spec, wl.K)
             sfb_bytes += _sf_bytes(spec, wl.K)
+            sfb_ms += launch_ms.get(i, 0.0)
         else:
             ps_bytes += _ps_bytes(spec, wl.P, "buf" in h)
             ps_in_iter += launch_ms.get(i, 0.0)
-    sfb_ms = launch_ms.get("sf_group", 0.0)
     sfb_tflops = sfb_flops / sfb_ms / 1e9 if sfb_ms else None
     ps_gbs = ps_bytes / ps_ms / 1e6 if ps_ms else None
     n_ps = sum(1 for s_ in schemes if s_ == api.PS)
@@ -269,14 +270,14 @@ def main():
         "config": {"workload": f"{wl.name}: {sum(s.numel for s in wl.specs)} params, "
                                f"{len(wl.specs)} tensors, K={wl.K}, lr={wl.lr}, momentum={wl.momentum}",
                    "P": wl.P, "B": wl.B, "streams": args.streams},
-        "roofline": {"bound": "mfma", "kernel": "sf_apply_batch (fp32 MFMA, all FC layers in one launch)",
+        "roofline": {"bound": "mfma", "kernel": "sf_apply (fp32 MFMA; one launch per FC layer)",
                      "achieved": round(sfb_tflops, 2) if sfb_tflops else None,
                      "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(sfb_tflops / PEAK_FP32_MFMA_TFLOPS, 4) if sfb_tflops else None,
                      "traffic": _stored_traffic("sf_apply", "sf_apply.hip"),
                      "work": f"2*M*N*K flops of the {sum(1 for s in schemes if s == api.SFB)} SFB "
-                             f"layers of one step ({sfb_flops / 1e9:.1f} GFLOP) / the average duration of "
-                             f"their grouped launch inside the iteration ({sfb_ms:.4f} ms)"},
+                             f"layers of one step ({sfb_flops / 1e9:.1f} GFLOP) / the summed average "
+                             f"durations of their launches inside the iteration ({sfb_ms:.4f} ms)"},
         "roofline_ps": {"bound": "hbm", "kernel": "ps_apply",
                         "achieved": round(ps_gbs, 1) if ps_gbs else None,
                         "peak": PEAK_HBM_GBS, "unit": "GB/s",

@@ -206,14 +206,13 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation"; Alg. 2 TRAIN/sync): tensors[] is given in forward order
  * and issued from the last to the first (backpropagation order).  For each
  * tensor the scheme is Alg. 1's (FC: poseidon_hybcomm_choose(M, N, B, P);
- * other kinds: PS).  All SFB updates (bound by the matrix cores) are
- * enqueued as one grouped reconstruction (poseidon_sf_apply_batch, layers in
- * backpropagation order) on the pool's first stream; the PS updates (bound
- * by memory bandwidth) are enqueued one per tensor, in backpropagation order,
- * on its second stream, so that the two kinds overlap; a one-stream pool runs
- * everything in order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS tensors take
- * poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf) (momentum is used
- * only when buf != NULL).  Every pool stream first waits for the work already
+ * other kinds: PS).  Every tensor with work is one launch, in
+ * backpropagation order: the SFB updates (bound by the matrix cores) on the
+ * pool's first stream, the PS updates (bound by memory bandwidth) on its
+ * second, so that the two kinds overlap; a one-stream pool runs everything in
+ * order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS
+ * tensors take poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf)
+ * (momentum is used only when buf != NULL).  Every pool stream first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so
  * the call behaves like one asynchronous operation on `stream` (the
  * bulk-synchronous barrier of Sec. 4.1 "Managing Consistency").
@@ -237,8 +236,8 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 
 /* One launch of the last iteration run with timing enabled. */
 typedef struct poseidon_launch_record {
-    int32_t scheme;   /* POSEIDON_SFB (the grouped SF launch) or POSEIDON_PS (one tensor) */
-    int32_t tensor;   /* index into that call's tensors[] for PS, -1 for the SF group */
+    int32_t scheme;   /* POSEIDON_SFB or POSEIDON_PS */
+    int32_t tensor;   /* index into that call's tensors[] */
     int32_t stream;   /* pool stream index */
     float   ms;       /* time between the events around the launch */
 } poseidon_launch_record;

@@ -32,6 +32,7 @@ namespace poseidon {
 namespace {
 
 typedef float f16v __attribute__((ext_vector_type(16)));
+typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));   // 16 bytes, 4-byte aligned
 
 constexpr int LDS_PAD = 4;    // floats of padding per LDS row (keeps 16-byte alignment)
 constexpr int NUM_XCD = 8;    // MI355X: 8 accelerator complex dies, one L2 each
@@ -55,11 +56,14 @@ struct SfTile {
 // Load one BK x (4*COLS4) slice of a K-major operand X (row length ld = its
 // number of columns) into registers: group j of this thread covers row
 // g / COLS4 and columns 4*(g % COLS4) .. +3 with g = tid + j*THREADS.
-// Out-of-range rows/columns read as 0, which adds nothing to the sum.  vec
-// (uniform; a constant in the single-layer kernels) selects 16-byte loads.
-template <int NV4, int COLS4, int THREADS>
+// Out-of-range rows/columns read as 0, which adds nothing to the sum.  Every
+// group is one 16-byte load: with VEC (ld % 4 == 0, X 16-byte aligned) a group
+// is wholly in or out; otherwise rows start at any 4-byte boundary (global
+// loads of several dwords need only 4-byte alignment) and only a group that
+// runs past the end of its row is read element by element.
+template <int NV4, int COLS4, int THREADS, bool VEC>
 __device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int64_t ld,
-                                  int64_t rows, int64_t k0, int64_t c0, int tid, bool vec)
+                                  int64_t rows, int64_t k0, int64_t c0, int tid)
 {
 #pragma unroll
     for (int j = 0; j < NV4; ++j) {
@@ -67,11 +71,12 @@ __device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int
         const int64_t k = k0 + g / COLS4;
         const int64_t c = c0 + 4 * (g % COLS4);
         const float* src = X + k * ld + c;
-        if (vec) {
-            // ld % 4 == 0 and X 16-byte aligned: a group is wholly in or out.
-            r[j] = (k < rows && c < ld) ? *reinterpret_cast<const f4*>(src) : f4{0.f, 0.f, 0.f, 0.f};
+        const bool kin = k < rows;
+        if constexpr (VEC) {
+            r[j] = (kin && c < ld) ? *reinterpret_cast<const f4*>(src) : f4{0.f, 0.f, 0.f, 0.f};
+        } else if (kin && c + 3 < ld) {
+            r[j] = *reinterpret_cast<const f4u*>(src);
         } else {
-            const bool kin = k < rows;
             r[j].x = (kin && c + 0 < ld) ? src[0] : 0.f;
             r[j].y = (kin && c + 1 < ld) ? src[1] : 0.f;
             r[j].z = (kin && c + 2 < ld) ? src[2] : 0.f;
@@ -150,14 +155,18 @@ __device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const flo
 constexpr int BUF_RSRC_WORD3 = 0x00020000;
 
 // One BM x BN tile of W: the whole K loop and the fused update.  EPI: MFMA
-// blocks of W (16 values per lane each) read per epilogue chunk.
-template <int BM, int BN, int BK, int WM, int WN, bool PREFETCH_W, int EPI, bool HUGE_N>
-__device__ inline void sf_tile(float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
-                               int64_t M, int64_t N, int64_t K, float lr, int tm, int tn, bool va, bool vb)
+// blocks of W (16 values per lane each) read per epilogue chunk.  The
+// double-buffered K slices live in the caller's LDS arrays (As: 2 x BK*LDA
+// floats, Bs: 2 x BK*LDB; buffer b starts at b*BK*LD), so that several
+// inlined variants share one allocation.  Always inlined: as a called function it would keep both the
+// 16-byte and the scalar operand loads and pay the call convention.
+template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int EPI, bool HUGE_N>
+__device__ __forceinline__ void sf_tile(
+    float* As, float* Bs, float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
+    int64_t M, int64_t N, int64_t K, float lr, int tm, int tn)
 {
     using T = SfTile<BM, BN, BK, WM, WN>;
-    __shared__ float As[2][BK * T::LDA];
-    __shared__ float Bs[2][BK * T::LDB];
+    constexpr int SA = BK * T::LDA, SB = BK * T::LDB;   // floats per LDS buffer
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -182,21 +191,21 @@ __device__ inline void sf_tile(float* __restrict__ W, const float* __restrict__ 
     f4 ra[T::A_V4], rb[T::B_V4];
     const int64_t nkt = (K + BK - 1) / BK;
 
-    load_panel<T::A_V4, BM / 4, T::THREADS>(ra, U, M, K, 0, m0, tid, va);
-    load_panel<T::B_V4, BN / 4, T::THREADS>(rb, V, N, K, 0, n0, tid, vb);
-    store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[0], ra, tid);
-    store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[0], rb, tid);
+    load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, 0, m0, tid);
+    load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, 0, n0, tid);
+    store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As, ra, tid);
+    store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs, rb, tid);
     __syncthreads();
 
     const int a_off = lrow * T::LDA + wm + lcol;
     const int b_off = lrow * T::LDB + wn + lcol;
     for (int64_t kt = 0; kt + 1 < nkt; ++kt) {
         const int cur = static_cast<int>(kt & 1);
-        load_panel<T::A_V4, BM / 4, T::THREADS>(ra, U, M, K, (kt + 1) * BK, m0, tid, va);
-        load_panel<T::B_V4, BN / 4, T::THREADS>(rb, V, N, K, (kt + 1) * BK, n0, tid, vb);
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As[cur] + a_off, Bs[cur] + b_off);
-        store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As[cur ^ 1], ra, tid);
-        store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs[cur ^ 1], rb, tid);
+        load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, (kt + 1) * BK, m0, tid);
+        load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, (kt + 1) * BK, n0, tid);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + cur * SA + a_off, Bs + cur * SB + b_off);
+        store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As + (cur ^ 1) * SA, ra, tid);
+        store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs + (cur ^ 1) * SB, rb, tid);
         __syncthreads();
     }
     const int last = static_cast<int>((nkt - 1) & 1);
@@ -233,7 +242,7 @@ __device__ inline void sf_tile(float* __restrict__ W, const float* __restrict__ 
                         wr, voff + 128 * j, (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0));
             }
         }
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As[last] + a_off, Bs[last] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + last * SA + a_off, Bs + last * SB + b_off);
         if (interior) {
 #pragma unroll
             for (int c0 = 0; c0 < NB; c0 += CH) {
@@ -291,7 +300,7 @@ __device__ inline void sf_tile(float* __restrict__ W, const float* __restrict__ 
         }
     } else {
         // Rows so long that tile offsets need 64 bits: plain guarded accesses.
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As[last] + a_off, Bs[last] + b_off);
+        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + last * SA + a_off, Bs + last * SB + b_off);
 #pragma unroll
         for (int i = 0; i < T::TM; ++i) {
 #pragma unroll
@@ -317,9 +326,12 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
     int64_t M, int64_t N, int64_t K, float lr, int tiles_m, int tiles_n)
 {
+    using T = SfTile<BM, BN, BK, WM, WN>;
+    __shared__ float As[2 * BK * T::LDA];
+    __shared__ float Bs[2 * BK * T::LDB];
     int tm, tn;
     tile_coords<GM>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
-    sf_tile<BM, BN, BK, WM, WN, PREFETCH_W, EPI, HUGE_N>(W, U, V, M, N, K, lr, tm, tn, VEC_A, VEC_B);
+    sf_tile<BM, BN, BK, WM, WN, VEC_A, VEC_B, PREFETCH_W, EPI, HUGE_N>(As, Bs, W, U, V, M, N, K, lr, tm, tn);
 }
 
 // ---------------------------------------------------------------------------
@@ -368,10 +380,30 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_batch_kernel(const 
     const int first_m = g * G;
     const int rows = (tiles_m - first_m) < G ? (tiles_m - first_m) : G;
     const int in = local - g * per_group;
-    sf_tile<BM, BN, BK, WM, WN, PREFETCH_W, EPI, false>(args.item[l].W, args.item[l].U, args.item[l].V,
-                                                       args.item[l].M, args.item[l].N, K, lr, first_m + in % rows,
-                                                       in / rows, (args.item[l].vec & 1) != 0,
-                                                       (args.item[l].vec & 2) != 0);
+    using T = SfTile<BM, BN, BK, WM, WN>;
+    __shared__ float As[2 * BK * T::LDA];
+    __shared__ float Bs[2 * BK * T::LDB];
+    const SfBatchItem& it = args.item[l];
+    const int tm = first_m + in % rows, tn = in / rows;
+    // The operand-load variant is uniform per layer: four inlined copies.
+    switch (it.vec & 3) {
+    case 3:
+        sf_tile<BM, BN, BK, WM, WN, true, true, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K, lr,
+                                                                        tm, tn);
+        break;
+    case 2:
+        sf_tile<BM, BN, BK, WM, WN, false, true, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K, lr,
+                                                                         tm, tn);
+        break;
+    case 1:
+        sf_tile<BM, BN, BK, WM, WN, true, false, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K, lr,
+                                                                         tm, tn);
+        break;
+    default:
+        sf_tile<BM, BN, BK, WM, WN, false, false, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K,
+                                                                          lr, tm, tn);
+        break;
+    }
 }
 
 template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, int GM, bool VA, bool VB>

@@ -22,7 +22,6 @@ struct poseidon_stream_pool {
     std::vector<hipEvent_t> t_stop;
     std::vector<poseidon_launch_record> t_rec;
     bool t_valid = false;             // a timed iteration has been enqueued
-    std::vector<poseidon::SfTensor> sf_work;   // host scratch reused across calls
 };
 
 namespace poseidon {
@@ -174,22 +173,9 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
             schemes[t] = plan[static_cast<size_t>(t)];
-    // Launches: every SFB tensor in one grouped SF launch (backpropagation
-    // order of the tile list), every PS tensor on its own.
-    pool->sf_work.clear();
-    int32_t ps_launches = 0;
-    for (int32_t t = count - 1; t >= 0; --t) {
-        const poseidon_tensor& x = tensors[t];
-        if (x.M * x.N == 0)
-            continue;
-        if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
-            if (K > 0)
-                pool->sf_work.push_back(SfTensor{x.W, x.U, x.V, x.M, x.N});
-        } else {
-            ++ps_launches;
-        }
-    }
-    const int32_t launches = ps_launches + (pool->sf_work.empty() ? 0 : 1);
+    // One launch per tensor with work.  (A grouped launch of all SF layers
+    // measured slower than per-layer launches, alone and beside the PS work.)
+    const int32_t launches = active;
     if (pool->timing) {
         if (!reserve_timing(pool, launches))
             return POSEIDON_ERR_HIP;
@@ -223,25 +209,25 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
         }
         return true;
     };
-    if (!pool->sf_work.empty()) {
-        hipStream_t s = pool->streams[0];
-        if (!timed(s, POSEIDON_SFB, -1, 0, [&] {
-                return launch_sf_apply_batch(pool->sf_work.data(), static_cast<int32_t>(pool->sf_work.size()), K,
-                                             lr, s);
-            }))
-            return POSEIDON_ERR_HIP;
-    }
     for (int32_t t = count - 1; t >= 0; --t) {
         const poseidon_tensor& x = tensors[t];
         const int64_t n = x.M * x.N;
-        if (n == 0 || plan[static_cast<size_t>(t)] != POSEIDON_PS)
+        if (n == 0)
             continue;
-        const int32_t si = used == 1 ? 0 : 1;
-        hipStream_t s = pool->streams[si];
-        if (!timed(s, POSEIDON_PS, t, si, [&] {
-                return launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
-            }))
-            return POSEIDON_ERR_HIP;
+        if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
+            if (K == 0)
+                continue;
+            hipStream_t s = pool->streams[0];
+            if (!timed(s, POSEIDON_SFB, t, 0, [&] { return launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s); }))
+                return POSEIDON_ERR_HIP;
+        } else {
+            const int32_t si = used == 1 ? 0 : 1;
+            hipStream_t s = pool->streams[si];
+            if (!timed(s, POSEIDON_PS, t, si, [&] {
+                    return launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
+                }))
+                return POSEIDON_ERR_HIP;
+        }
     }
 
     for (int32_t s = 0; s < used; ++s) {

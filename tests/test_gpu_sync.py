@@ -134,8 +134,8 @@ def test_sync_iteration_missing_payload_is_an_error():
 
 
 def test_sync_iteration_launch_records():
-    """Timing mode: one record for the grouped SF launch (stream 0), then one per
-    PS tensor in backprop order (stream 1)."""
+    """Timing mode: one record per launch in backprop order, SF layers on
+    stream 0 and PS tensors on stream 1."""
     d = dev()
     wl = I.workload(5)
     host = I.make_tensors(wl, only=["fc7.W", "fc7.b", "conv5_4.W"])
@@ -146,8 +146,8 @@ def test_sync_iteration_launch_records():
     log("sync_iteration timing records")
     it()
     recs = pool.launch_times()
-    want = [(api.SFB, -1, 0)] + [(api.PS, i, 1) for i, h in reversed(list(enumerate(host)))
-                                 if h["spec"].kind != I.FC]
+    want = [(api.SFB, i, 0) if h["spec"].kind == I.FC else (api.PS, i, 1)
+            for i, h in reversed(list(enumerate(host)))]
     assert [(r["scheme"], r["tensor"], r["stream"]) for r in recs] == want
     assert all(r["ms"] > 0 for r in recs)
     pool.set_timing(False)
