@@ -38,10 +38,13 @@ def _parse():
     ap.add_argument("--warmup", type=int, default=50,
                     help="untimed steps first (the first few dozen steps of a fresh process run a few %% slower)")
     ap.add_argument("--config", type=int, default=5, help="workload (5 = VGG19-22K full iteration)")
-    ap.add_argument("--streams", type=int, default=4)
+    ap.add_argument("--streams", type=int, default=2)
     ap.add_argument("--kernel-steps", type=int, default=None,
                     help="iterations timed per tensor for the roofline (default: --steps)")
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
+    ap.add_argument("--wfbp", choices=["on", "off"], default="on",
+                    help="also time the iteration overlapped with a synthetic VGG19 backward pass")
+    ap.add_argument("--wfbp-steps", type=int, default=5)
     ap.add_argument("--cpu-fraction", type=float, default=1.0,
                     help="fraction of each tensor the CPU oracle runs on")
     ap.add_argument("--calibration-copy-mib", type=int, default=512,
@@ -90,6 +93,73 @@ def _stored_traffic(kernel: str, source: str):
             if kv.get("kernel") == kernel and kv.get("source_sha256") == want:
                 return float(kv["bytes_per_step"])
     return None
+
+
+def _wfbp_phase(wl, devt, it, pool, d, steps):
+    """Wait-free backpropagation on one GPU: a synthetic fp32 VGG19 backward
+    pass (vendor GEMMs on a compute stream) with the iteration's updates
+    started per layer as its backward finishes, against the backward pass
+    followed by the whole iteration."""
+    import torch
+
+    from paper_1706_03292_amd import api
+    from paper_1706_03292_amd import synthetic_backward as SB
+
+    # The backward pass runs on the default stream: with the pool's two
+    # streams that is three streams, each on a hardware queue of its own.
+    cs = torch.cuda.current_stream(d)
+    bw = SB.SyntheticBackward(wl, [t["W"] for t in devt], d)
+    events = {l.layer: torch.cuda.Event() for l in bw.layers}
+    ready = bw.ready_list(events, len(devt))
+
+    def timed(fn):
+        out = []
+        for rep in range(steps + 2):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(cs)
+            fn()
+            b.record(cs)
+            torch.cuda.synchronize()
+            if rep >= 2:
+                out.append(a.elapsed_time(b))
+        return sum(out) / len(out)
+
+    def serial():
+        bw.run(cs)
+        it(cs)
+
+    def wfbp():
+        bw.run(cs, events)
+        it(cs, ready=ready)
+
+    t_bw = timed(lambda: bw.run(cs))
+    t_sync = timed(lambda: it(cs))
+    t_serial = timed(serial)
+    t_wfbp = timed(wfbp)
+    hidden = t_serial - t_wfbp
+    # One more of each with the library's launch timing: the updates' own
+    # durations show whether they ran beside the backward pass.
+    launch = {}
+    for name, fn in (("serial", serial), ("wfbp", wfbp)):
+        pool.set_timing(True)
+        fn()
+        recs = pool.launch_times()
+        pool.set_timing(False)
+        launch[name] = {"sf_ms": round(sum(r["ms"] for r in recs if r["scheme"] == api.SFB), 3),
+                        "ps_ms": round(sum(r["ms"] for r in recs if r["scheme"] == api.PS), 3)}
+    torch.cuda.synchronize()
+    del bw
+    torch.cuda.empty_cache()
+    return {
+        "backward": "synthetic VGG19 backward at 224x224, B=%d, fp32 torch.mm (vendor library), %.2f TFLOP"
+                    % (wl.B, sum(l.flops for l in SB.plan(wl)) / 1e12),
+        "backward_ms": round(t_bw, 3), "sync_ms": round(t_sync, 3),
+        "serial_ms": round(t_serial, 3), "wfbp_ms": round(t_wfbp, 3),
+        "hidden_sync_ms": round(hidden, 3), "hidden_frac": round(hidden / t_sync, 3),
+        "stall_ms": round(max(0.0, t_wfbp - t_bw), 3), "busy_frac": round(t_bw / t_wfbp, 3),
+        "update_launch_ms": launch,
+        "steps": steps,
+    }
 
 
 def _cpu_baseline(wl, host, fraction):
@@ -299,6 +369,10 @@ def main():
         "ps_gbs": round(ps_gbs, 1) if ps_gbs else None,
         "layers_sfb": layers,
     }
+    if args.wfbp == "on" and wl.config == 5:
+        print("[bench] WFBP phase (synthetic backward)", file=sys.stderr, flush=True)
+        result["wfbp"] = _wfbp_phase(wl, devt, it, pool, d, args.wfbp_steps)
+        print(f"[bench] WFBP: {result['wfbp']}", file=sys.stderr, flush=True)
     if args.cpu_baseline == "on":
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = _cpu_baseline(wl, host, args.cpu_fraction)

@@ -194,7 +194,12 @@ typedef struct poseidon_tensor {
  * the events that fork them from and join them back to a caller stream. */
 typedef struct poseidon_stream_pool poseidon_stream_pool;
 
-/* Create a pool of num_streams (1..64) streams on the current device.
+/* Create a pool of num_streams (1..64) streams on the current device.  An
+ * iteration uses at most two of them.  HIP runs a process's streams on at most
+ * GPU_MAX_HW_QUEUES hardware queues (4 by default), and streams that share a
+ * queue run in order: for the two kinds of updates to overlap each other and
+ * the caller's work, keep the streams in use (these two and the caller's)
+ * within that number -- a two-stream pool is enough.
  * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG or POSEIDON_ERR_HIP. */
 int poseidon_pool_create(int32_t num_streams, poseidon_stream_pool** pool);
 
@@ -227,10 +232,33 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
                             hipStream_t stream, int32_t* schemes);
 
 /*
+ * The same iteration with wait-free backpropagation (Sec. 3.1; Alg. 2: the
+ * sync of layer l is scheduled as soon as BackwardThrough(l) has run): tensor
+ * t's update starts once the caller's event ready[t] has completed, not after
+ * everything enqueued on `stream`, so the updates of the upper layers run
+ * while the backward pass of the lower layers is still computing.  ready[t]
+ * marks the point after which W_t may change: the caller records it (with
+ * hipEventRecord, on any stream of the current device, BEFORE this call --
+ * an event never recorded counts as complete) after the last kernel that
+ * reads W_t or writes t's payload (U/V rows or shards) in this iteration;
+ * tensors of one layer may share an event.  Issue order, streams, schemes,
+ * payload rules and results are those of poseidon_sync_iteration (bitwise:
+ * the same launches); `stream` waits for every update at the end.
+ * ready: count non-NULL events, caller-owned, not retained after the call.
+ * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (also for NULL ready or a NULL
+ * entry), POSEIDON_ERR_PAYLOAD or POSEIDON_ERR_HIP.
+ */
+int poseidon_sync_iteration_wfbp(poseidon_stream_pool* pool,
+                                 const poseidon_tensor* tensors, int32_t count,
+                                 int64_t B, int32_t P, float lr, float momentum,
+                                 const hipEvent_t* ready, hipStream_t stream, int32_t* schemes);
+
+/*
  * Launch timing (the per-layer synchronisation times the paper's evaluation
  * reasons about, Sec. 5).  While enabled (default: off), every launch that
- * poseidon_sync_iteration enqueues is bracketed by two timing events on the
- * stream it runs on.  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG.
+ * poseidon_sync_iteration or poseidon_sync_iteration_wfbp enqueues is
+ * bracketed by two timing events on the stream it runs on (after any wait on a
+ * ready event).  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG.
  */
 int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 

@@ -22,7 +22,8 @@ KIND_OTHER = 1
 
 EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_batch", "poseidon_ps_apply", "poseidon_ps_apply_batch",
            "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_pool_create",
-           "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_pool_set_timing",
+           "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_sync_iteration_wfbp",
+           "poseidon_pool_set_timing",
            "poseidon_pool_launch_times", "poseidon_abi_version")
 
 
@@ -72,6 +73,8 @@ def lib() -> ctypes.CDLL:
     L.poseidon_pool_destroy.argtypes = [vp]
     L.poseidon_sync_iteration.argtypes = [vp, ctypes.POINTER(PoseidonTensor), i32, i64, i32,
                                           f32, f32, vp, ctypes.POINTER(i32)]
+    L.poseidon_sync_iteration_wfbp.argtypes = [vp, ctypes.POINTER(PoseidonTensor), i32, i64, i32,
+                                               f32, f32, ctypes.POINTER(vp), vp, ctypes.POINTER(i32)]
     L.poseidon_sf_apply_batch.argtypes = [ctypes.POINTER(PoseidonSfTensor), i32, i64, f32, vp]
     L.poseidon_ps_apply_batch.argtypes = [ctypes.POINTER(PoseidonPsTensor), i32, i32, f32, f32, vp]
     L.poseidon_pool_set_timing.argtypes = [vp, i32]

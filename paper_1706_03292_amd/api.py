@@ -260,9 +260,25 @@ class SyncIteration:
         self._schemes = (ctypes.c_int32 * max(1, len(tensors)))()
         self.count = len(tensors)
 
-    def __call__(self, stream=None) -> list[int]:
+    def __call__(self, stream=None, ready=None) -> list[int]:
+        """Enqueue the iteration on ``stream`` (default: the current stream).
+
+        ``ready`` (optional): one already-recorded event per tensor, in the
+        same order (``torch.cuda.Event`` or a raw hipEvent_t); tensor t's
+        update then waits for ready[t] instead of for the work on ``stream``
+        (wait-free backpropagation, poseidon_sync_iteration_wfbp)."""
+        h = _stream_handle(stream, self.pool.device)
         with torch.cuda.device(self.pool.device):
-            _check("poseidon_sync_iteration", L.lib().poseidon_sync_iteration(
-                self.pool.handle, self._arr, self.count, self.B, self.P, self.lr, self.momentum,
-                _stream_handle(stream, self.pool.device), self._schemes))
+            if ready is None:
+                _check("poseidon_sync_iteration", L.lib().poseidon_sync_iteration(
+                    self.pool.handle, self._arr, self.count, self.B, self.P, self.lr, self.momentum,
+                    h, self._schemes))
+            else:
+                if len(ready) != self.count:
+                    raise ValueError("ready needs one event per tensor")
+                evs = (ctypes.c_void_p * max(1, self.count))(
+                    *[int(e.cuda_event) if hasattr(e, "cuda_event") else int(e) for e in ready])
+                _check("poseidon_sync_iteration_wfbp", L.lib().poseidon_sync_iteration_wfbp(
+                    self.pool.handle, self._arr, self.count, self.B, self.P, self.lr, self.momentum,
+                    evs, h, self._schemes))
         return list(self._schemes[:self.count])

@@ -122,10 +122,13 @@ extern "C" int poseidon_pool_destroy(poseidon_stream_pool* pool)
     return POSEIDON_OK;
 }
 
-extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
-                                       const poseidon_tensor* tensors, int32_t count,
-                                       int64_t B, int32_t P, float lr, float momentum,
-                                       hipStream_t stream, int32_t* schemes)
+namespace {
+
+// The iteration of poseidon_sync_iteration (ready == NULL: every update waits
+// for the work enqueued on `stream` before the call) and of
+// poseidon_sync_iteration_wfbp (tensor t's update waits for ready[t] only).
+int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_t count, int64_t B, int32_t P,
+              float lr, float momentum, const hipEvent_t* ready, hipStream_t stream, int32_t* schemes)
 {
     using namespace poseidon;
     if (!pool || count < 0 || (count > 0 && !tensors) || B < 0 || P < 1)
@@ -168,6 +171,8 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
         }
         if (rc != POSEIDON_OK)
             return rc;
+        if (ready && !ready[t])
+            return POSEIDON_ERR_INVALID_ARG;
         plan[static_cast<size_t>(t)] = scheme;
     }
     if (schemes)
@@ -190,13 +195,24 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
     // of queueing behind each other.  A one-stream pool serialises everything.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
     const int32_t used = (S > 1 && launches > 1) ? 2 : 1;
-    if (hipEventRecord(pool->fork, stream) != hipSuccess)
-        return POSEIDON_ERR_HIP;
-    for (int32_t s = 0; s < used; ++s)
-        if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
+    hipEvent_t waited[2] = {nullptr, nullptr};   // last ready event each used stream waits on
+    if (!ready) {
+        if (hipEventRecord(pool->fork, stream) != hipSuccess)
             return POSEIDON_ERR_HIP;
+        for (int32_t s = 0; s < used; ++s)
+            if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
+                return POSEIDON_ERR_HIP;
+    }
 
+    // Tensor t's launch on pool stream si: with ready events it first waits
+    // for ready[t] (once per run of equal events), then the timing events, if
+    // on, bracket the launch alone.
     auto timed = [&](hipStream_t s, int32_t scheme, int32_t tensor, int32_t si, auto&& launch) -> bool {
+        if (ready && ready[tensor] != waited[si]) {
+            if (hipStreamWaitEvent(s, ready[tensor], 0) != hipSuccess)
+                return false;
+            waited[si] = ready[tensor];
+        }
         const size_t r = pool->t_rec.size();
         if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
             return false;
@@ -236,6 +252,27 @@ extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
             return POSEIDON_ERR_HIP;
     }
     return POSEIDON_OK;
+}
+
+}  // namespace
+
+extern "C" int poseidon_sync_iteration(poseidon_stream_pool* pool,
+                                       const poseidon_tensor* tensors, int32_t count,
+                                       int64_t B, int32_t P, float lr, float momentum,
+                                       hipStream_t stream, int32_t* schemes)
+{
+    return sync_impl(pool, tensors, count, B, P, lr, momentum, nullptr, stream, schemes);
+}
+
+extern "C" int poseidon_sync_iteration_wfbp(poseidon_stream_pool* pool,
+                                            const poseidon_tensor* tensors, int32_t count,
+                                            int64_t B, int32_t P, float lr, float momentum,
+                                            const hipEvent_t* ready, hipStream_t stream, int32_t* schemes)
+{
+    if (count > 0 && !ready)
+        return POSEIDON_ERR_INVALID_ARG;
+    static const hipEvent_t none = nullptr;
+    return sync_impl(pool, tensors, count, B, P, lr, momentum, count > 0 ? ready : &none, stream, schemes);
 }
 
 extern "C" int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable)

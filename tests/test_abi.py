@@ -62,6 +62,7 @@ def test_invalid_arguments_rejected_before_device_work():
     assert lib.poseidon_pool_create(65, ctypes.byref(ctypes.c_void_p())) == L.ERR_INVALID_ARG
     assert lib.poseidon_pool_destroy(None) == L.OK
     assert lib.poseidon_sync_iteration(None, None, 0, 32, 16, 0.1, 0.9, None, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_sync_iteration_wfbp(None, None, 0, 32, 16, 0.1, 0.9, None, None, None) == L.ERR_INVALID_ARG
     # batched PS: bad P, bad count, one bad tensor rejects the whole batch
     t = (L.PoseidonPsTensor * 2)(L.PoseidonPsTensor(0x1000, 0x900000, None, 8),
                                  L.PoseidonPsTensor(0x2000, 0x2000, None, 8))

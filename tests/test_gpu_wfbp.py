@@ -1,0 +1,233 @@
+"""Wait-free backpropagation (Sec. 3.1; Alg. 2): poseidon_sync_iteration_wfbp
+starts each tensor's update on its own ready event.  Checked here: results
+bit-identical to poseidon_sync_iteration, no update before its event (the
+payload written by the backward pass is the one applied), no weight changed
+before the backward pass read it, and updates overlapping later backward
+work.
+
+The backward work runs on the default stream and the pools have two streams,
+so that (with HIP's default of four hardware queues per process) every
+stream has a hardware queue of its own: two streams that share a queue run
+in order, which would hide any overlap."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from _helpers import W_TOL, BUF_TOL, assert_close, dev, log, to_np
+from paper_1706_03292_amd import api
+from paper_1706_03292_amd import inputs as I
+from paper_1706_03292_amd import synthetic_backward as SB
+
+pytestmark = pytest.mark.gpu
+
+
+def _to_dev(host, d):
+    return [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in host]
+
+
+def test_wfbp_equals_sync_iteration_bitwise():
+    """VGG19-22K with a synthetic backward at 56 x 56 on a compute stream:
+    backward-then-sync and WFBP give bit-identical parameters and buffers."""
+    d = dev()
+    wl = I.workload(5)
+    host = I.make_tensors(wl)
+    a, b = _to_dev(host, d), _to_dev(host, d)
+    cs = torch.cuda.current_stream(d)
+    pool = api.StreamPool(2)
+    it_a = api.SyncIteration(pool, a, wl.B, wl.P, wl.lr, wl.momentum)
+    it_b = api.SyncIteration(pool, b, wl.B, wl.P, wl.lr, wl.momentum)
+    bw_a = SB.SyntheticBackward(wl, [t["W"] for t in a], d, image=56)
+    bw_b = SB.SyntheticBackward(wl, [t["W"] for t in b], d, image=56)
+    events = {l.layer: torch.cuda.Event() for l in bw_b.layers}
+    ready = bw_b.ready_list(events, len(b))
+    for step in range(2):
+        log(f"wfbp vs serial, step {step}")
+        bw_a.run(cs)
+        sa = it_a(cs)
+        bw_b.run(cs, events)
+        sb = it_b(cs, ready=ready)
+        assert sa == sb
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x["W"], y["W"]), x["spec"].name
+        if "buf" in x:
+            assert torch.equal(x["buf"], y["buf"]), x["spec"].name
+    pool.close()
+
+
+def _oracle_layers(host):
+    out = []
+    for h in host:
+        L = {"fc": h["spec"].kind == I.FC, "W": h["W"].numpy()}
+        for k in ("U", "V", "shards", "buf"):
+            if k in h:
+                L[k] = h[k].numpy()
+        out.append(L)
+    return out
+
+
+def test_wfbp_update_waits_for_payload_written_by_backward():
+    """Each layer's 'backward' first keeps the compute stream busy, then
+    scales this node's own payload (its B rows of U, or shard 0) by 64 --
+    exact in fp32 -- and records the layer's event.  The updates must see the
+    scaled payload: W matches the oracle on the scaled inputs and is far from
+    the oracle on the unscaled ones."""
+    d = dev()
+    wl = I.workload(5)
+    names = ["fc7.W", "fc7.b", "conv5_4.W", "conv5_4.b", "conv5_3.W", "conv5_3.b"]
+    host = I.make_tensors(wl, only=names)
+    devt = _to_dev(host, d)
+    scaled = []
+    for h in host:
+        h2 = dict(h)
+        if "U" in h:
+            h2["U"] = h["U"].clone()
+            h2["U"][: wl.B] *= 64
+        else:
+            h2["shards"] = h["shards"].clone()
+            h2["shards"][0] *= 64
+        scaled.append(h2)
+    ref = oracle.sync_iteration(_oracle_layers(scaled), wl.B, wl.P, wl.lr, wl.momentum)
+    old = oracle.sync_iteration(_oracle_layers(host), wl.B, wl.P, wl.lr, wl.momentum)
+
+    cs = torch.cuda.current_stream(d)
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    busy_a = torch.randn(4096, 4096, device=d)
+    busy_c = torch.empty_like(busy_a)
+    events = [torch.cuda.Event() for _ in devt]
+    log("wfbp payload written by the backward pass")
+    with torch.cuda.stream(cs):
+        for i in reversed(range(len(devt))):
+            for _ in range(4):
+                torch.mm(busy_a, busy_a, out=busy_c)
+            t = devt[i]
+            if "U" in t:
+                t["U"][: wl.B].mul_(64)
+            else:
+                t["shards"][0].mul_(64)
+            events[i].record(cs)
+    it(cs, ready=events)
+    cs.synchronize()
+    for i, t in enumerate(devt):
+        name = host[i]["spec"].name
+        want = ref[i]["W"].reshape(-1)
+        assert_close(to_np(t["W"]).reshape(-1), want, W_TOL, name)
+        tol = W_TOL * float(np.max(np.abs(want)))
+        assert float(np.max(np.abs(old[i]["W"].reshape(-1) - want))) > 20 * tol, name   # distinguishable
+        if "buf" in t:
+            assert_close(to_np(t["buf"]), ref[i]["buf"], BUF_TOL, name + " buf")
+    pool.close()
+
+
+def test_wfbp_backward_reads_weights_before_their_update():
+    """The synthetic backward's dX = delta @ W (FC) and W^T @ dY (CONV) read the
+    weights the same iteration updates; with WFBP they still see the old ones.
+    (The vendor GEMMs may sum in a run-dependent order, so outputs are compared
+    to 1e-5 of their range; outputs computed from the updated weights differ
+    by far more.)"""
+    d = dev()
+    wl = I.workload(5)
+    host = I.make_tensors(wl)
+    devt = _to_dev(host, d)
+    cs = torch.cuda.current_stream(d)
+    bw = SB.SyntheticBackward(wl, [t["W"] for t in devt], d, image=28)
+
+    def outputs(record=None):
+        res = {}
+        with torch.cuda.stream(cs):
+            for l in bw.layers:
+                bw.layer(l)
+                res[l.layer] = bw.output(l).clone()
+                if record is not None:
+                    record[l.layer].record(cs)
+        return res
+
+    before = outputs()
+    cs.synchronize()
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    events = {l.layer: torch.cuda.Event() for l in bw.layers}
+    log("wfbp: backward reads pre-update weights")
+    during = outputs(events)
+    it(cs, ready=bw.ready_list(events, len(devt)))
+    cs.synchronize()
+    after = outputs()                      # from the updated weights
+    cs.synchronize()
+    for l in bw.layers:
+        if l.kind == I.CONV and not l.input_grad:
+            continue                       # dW only: does not read W
+        ref = before[l.layer]
+        tol = 1e-5 * float(ref.abs().max())
+        assert float((during[l.layer] - ref).abs().max()) <= tol, l.layer
+        assert float((after[l.layer] - ref).abs().max()) > 10 * tol, l.layer
+    pool.close()
+
+
+@pytest.mark.skipif(not hasattr(torch.cuda, "_sleep"), reason="needs torch.cuda._sleep")
+def test_wfbp_updates_overlap_later_backward_work():
+    """All updates' events are recorded before a long single-wave sleep kernel
+    (the rest of a backward pass that leaves the GPU idle): with WFBP the
+    iteration ends with the sleep, not after it."""
+    d = dev()
+    wl = I.workload(3)
+    devt = _to_dev(I.make_tensors(wl), d)
+    cs = torch.cuda.current_stream(d)
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(cs)
+        fn()
+        b.record(cs)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b)
+
+    cycles = 40_000_000                        # tens of ms at GPU clocks
+    with torch.cuda.stream(cs):
+        timed(lambda: torch.cuda._sleep(cycles))
+        t_sleep = min(timed(lambda: torch.cuda._sleep(cycles)) for _ in range(2))
+    t_sync = min(timed(lambda: it(cs)) for _ in range(3))
+    ev = torch.cuda.Event()
+
+    def wfbp():
+        ev.record(cs)
+        with torch.cuda.stream(cs):
+            torch.cuda._sleep(cycles)
+        it(cs, ready=[ev] * len(devt))
+
+    log(f"wfbp overlap: sleep {t_sleep:.2f} ms, sync {t_sync:.2f} ms")
+    t_wfbp = min(timed(wfbp) for _ in range(3))
+    log(f"wfbp overlap: wfbp {t_wfbp:.2f} ms")
+    assert t_sleep > 4 * t_sync
+    assert t_wfbp < t_sleep + 0.5 * t_sync
+    pool.close()
+
+
+def test_wfbp_launch_records_and_errors():
+    d = dev()
+    wl = I.workload(5)
+    host = I.make_tensors(wl, only=["fc7.W", "fc7.b", "conv5_4.W"])
+    devt = _to_dev(host, d)
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    cs = torch.cuda.current_stream(d)
+    ev = torch.cuda.Event()
+    ev.record(cs)
+    with pytest.raises(ValueError):
+        it(cs, ready=[ev])
+    with pytest.raises(api.PoseidonError):
+        it(cs, ready=[ev, 0, ev])
+    pool.set_timing(True)
+    log("wfbp timing records")
+    it(cs, ready=[ev] * len(devt))
+    recs = pool.launch_times()
+    want = [(api.SFB, i, 0) if h["spec"].kind == I.FC else (api.PS, i, 1)
+            for i, h in reversed(list(enumerate(host)))]
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in recs] == want
+    assert all(r["ms"] > 0 for r in recs)
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    pool.close()
