@@ -48,6 +48,7 @@ extern "C" {
 /* Synchronisation schemes (Alg. 1 returns one of these). */
 #define POSEIDON_PS   0
 #define POSEIDON_SFB  1
+#define POSEIDON_ADAM 2   /* Adam's scheme (cost model only): SFs to one server, the matrix back */
 
 /* Tensor kinds: only fully-connected weights can be synchronised by SFB;
  * convolution kernels, biases and normalisation vectors always use the
@@ -168,6 +169,35 @@ int poseidon_hybcomm_choose(int64_t M, int64_t N, int64_t B, int64_t P);
  */
 int poseidon_hybcomm_cost(int64_t M, int64_t N, int64_t B, int64_t P1, int64_t P2,
                           int64_t* ps_x_p2, int64_t* sfb_x_p2);
+
+/*
+ * Table 1's Adam row (Sec. 3.2): workers send their B factor pairs to the
+ * one server holding the layer, which sends the whole rebuilt M x N matrix
+ * back to every worker.  Per-node traffic in values, multiplied by P2 like
+ * poseidon_hybcomm_cost:
+ *   *server_x_p2 = (P1 M N + P1 B (M + N)) P2    (the holder, not a worker)
+ *   *worker_x_p2 = (B (M + N) + M N) P2          (a worker, not the holder)
+ *   *both_x_p2   = (P1 - 1)(M N + B (M + N)) P2  (the holder that is also a worker)
+ * Host-only.  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG (as
+ * poseidon_hybcomm_cost).
+ */
+int poseidon_hybcomm_cost_adam(int64_t M, int64_t N, int64_t B, int64_t P1, int64_t P2,
+                               int64_t* server_x_p2, int64_t* worker_x_p2, int64_t* both_x_p2);
+
+/*
+ * The three-way choice between PS, SFB and Adam's scheme for an M x N FC
+ * layer on P nodes that are each worker and server (Table 1; Sec. 5.3 ranks
+ * the schemes by the load of the busiest node, which for Adam is the node
+ * holding the layer): the scheme whose busiest node moves the fewest values,
+ *   PS   2 M N (2P - 2) / P,   SFB   2 B (P - 1)(M + N),
+ *   Adam (P - 1)(M N + B (M + N)),
+ * compared exactly in integers; a tie prefers SFB, then PS.  With P1 = P2
+ * Adam never moves strictly less than both others, so the result always
+ * equals poseidon_hybcomm_choose.  Host-only.  Returns POSEIDON_PS,
+ * POSEIDON_SFB, POSEIDON_ADAM or POSEIDON_ERR_INVALID_ARG (as
+ * poseidon_hybcomm_choose).
+ */
+int poseidon_hybcomm_choose3(int64_t M, int64_t N, int64_t B, int64_t P);
 
 /*
  * One parameter tensor of a network, as handed to poseidon_sync_iteration.

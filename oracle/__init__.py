@@ -17,7 +17,7 @@ Functions and the passages they follow:
 * ``ps_apply`` / ``ps_apply_points`` -- parameter-server aggregation of the P
   workers' dense gradients and its application (Sec. 2.1 "Parameter Server",
   Sec. 4.1 "KV Store", "Managing Consistency"), with heavy-ball momentum.
-* ``hybcomm_traffic`` / ``hybcomm_choose`` / ``best_scheme`` -- the hybrid
+* ``hybcomm_traffic`` / ``hybcomm_choose`` / ``hybcomm_choose3`` / ``best_scheme`` -- the hybrid
   communication decision by exhaustive message counting (Sec. 3.2, Table 1,
   Alg. 1).
 * ``sync_iteration`` -- one node's synchronisation of every layer of a network
@@ -76,6 +76,8 @@ def _load():
     lib.oracle_hybcomm_traffic.restype = ctypes.c_int
     lib.oracle_hybcomm_choose.argtypes = [_i64, _i64, _i64, _i64]
     lib.oracle_hybcomm_choose.restype = ctypes.c_int
+    lib.oracle_hybcomm_choose3.argtypes = [_i64, _i64, _i64, _i64]
+    lib.oracle_hybcomm_choose3.restype = ctypes.c_int
     lib.oracle_num_threads.argtypes = []
     lib.oracle_num_threads.restype = ctypes.c_int
     _lib = lib
@@ -216,6 +218,15 @@ def hybcomm_traffic(M: int, N: int, B: int, roles, scheme: int) -> np.ndarray:
 def hybcomm_choose(M: int, N: int, B: int, P: int) -> int:
     """SFB (1) or PS (0) for an M x N FC layer, batch B, P worker+server nodes."""
     rc = _load().oracle_hybcomm_choose(M, N, B, P)
+    if rc < 0:
+        raise ValueError("invalid arguments")
+    return rc
+
+
+def hybcomm_choose3(M: int, N: int, B: int, P: int) -> int:
+    """PS (0), SFB (1) or ADAM (2): the scheme whose busiest node moves the
+    fewest values on P worker+server nodes (ties: SFB, then PS, then Adam)."""
+    rc = _load().oracle_hybcomm_choose3(M, N, B, P)
     if rc < 0:
         raise ValueError("invalid arguments")
     return rc

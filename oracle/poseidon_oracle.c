@@ -344,6 +344,48 @@ int oracle_hybcomm_choose(int64_t M, int64_t N, int64_t B, int64_t P)
     return rc;
 }
 
+/* The three-way choice with Adam's scheme added (Table 1's Adam row; Sec.
+ * 5.3 compares the three by the load on the busiest node, Adam's row being
+ * that maximum).  On P nodes that are each worker and server, every scheme's
+ * traffic is enumerated as above and the one whose busiest node moves the
+ * fewest values wins; on a tie SFB is preferred (Alg. 1's "<="), then PS,
+ * then Adam.  Returns 0 (PS), 1 (SFB), 2 (Adam) or -1 on invalid input. */
+int oracle_hybcomm_choose3(int64_t M, int64_t N, int64_t B, int64_t P)
+{
+    if (P < 1 || P > 1 << 16 || M < 0 || N < 0 || B < 0)
+        return -1;
+    const int32_t nodes = (int32_t)P;
+    int32_t *roles = (int32_t *)malloc((size_t)nodes * sizeof(int32_t));
+    int64_t *t = (int64_t *)malloc((size_t)nodes * sizeof(int64_t));
+    int64_t busiest[3] = {0, 0, 0};
+    int rc = -1;
+    if (roles && t) {
+        for (int32_t j = 0; j < nodes; ++j)
+            roles[j] = ROLE_WORKER | ROLE_SERVER;
+        rc = 0;
+        for (int32_t scheme = 0; scheme < 3 && rc == 0; ++scheme) {
+            if (oracle_hybcomm_traffic(M, N, B, roles, nodes, scheme, t) != 0) {
+                rc = -1;
+                break;
+            }
+            for (int32_t j = 0; j < nodes; ++j)
+                if (t[j] > busiest[scheme])
+                    busiest[scheme] = t[j];
+        }
+        if (rc == 0) {
+            const int order[3] = {ORACLE_SFB, ORACLE_PS, ORACLE_ADAM};   /* tie preference */
+            int best = order[0];
+            for (int i = 1; i < 3; ++i)
+                if (busiest[order[i]] < busiest[best])
+                    best = order[i];
+            rc = best;
+        }
+    }
+    free(roles);
+    free(t);
+    return rc;
+}
+
 /* Threads the parallel loops above use (for reporting the CPU baseline). */
 int oracle_num_threads(void)
 {

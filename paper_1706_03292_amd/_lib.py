@@ -17,11 +17,13 @@ ERR_HIP = -2
 ERR_PAYLOAD = -3
 PS = 0
 SFB = 1
+ADAM = 2
 KIND_FC = 0
 KIND_OTHER = 1
 
 EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_batch", "poseidon_ps_apply", "poseidon_ps_apply_batch",
-           "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_pool_create",
+           "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_hybcomm_cost_adam",
+           "poseidon_hybcomm_choose3", "poseidon_pool_create",
            "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_sync_iteration_wfbp",
            "poseidon_pool_set_timing",
            "poseidon_pool_launch_times", "poseidon_abi_version")
@@ -69,6 +71,8 @@ def lib() -> ctypes.CDLL:
     L.poseidon_hybcomm_choose.argtypes = [i64, i64, i64, i64]
     L.poseidon_hybcomm_cost.argtypes = [i64, i64, i64, i64, i64,
                                         ctypes.POINTER(i64), ctypes.POINTER(i64)]
+    L.poseidon_hybcomm_cost_adam.argtypes = [i64, i64, i64, i64, i64] + [ctypes.POINTER(i64)] * 3
+    L.poseidon_hybcomm_choose3.argtypes = [i64, i64, i64, i64]
     L.poseidon_pool_create.argtypes = [i32, ctypes.POINTER(vp)]
     L.poseidon_pool_destroy.argtypes = [vp]
     L.poseidon_sync_iteration.argtypes = [vp, ctypes.POINTER(PoseidonTensor), i32, i64, i32,

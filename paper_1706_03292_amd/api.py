@@ -13,7 +13,7 @@ import ctypes
 import torch
 
 from . import _lib as L
-from ._lib import ERR_HIP, ERR_INVALID_ARG, ERR_PAYLOAD, KIND_FC, KIND_OTHER, PS, SFB  # noqa: F401
+from ._lib import ADAM, ERR_HIP, ERR_INVALID_ARG, ERR_PAYLOAD, KIND_FC, KIND_OTHER, PS, SFB  # noqa: F401
 
 
 class PoseidonError(RuntimeError):
@@ -162,6 +162,20 @@ def hybcomm_cost(M: int, N: int, B: int, P1: int, P2: int) -> tuple[int, int]:
     _check("poseidon_hybcomm_cost", L.lib().poseidon_hybcomm_cost(
         M, N, B, P1, P2, ctypes.byref(ps), ctypes.byref(sfb)))
     return ps.value, sfb.value
+
+
+def hybcomm_cost_adam(M: int, N: int, B: int, P1: int, P2: int) -> tuple[int, int, int]:
+    """Table 1's Adam row x P2: (holder, worker, holder that is also a worker)."""
+    v = [ctypes.c_int64() for _ in range(3)]
+    _check("poseidon_hybcomm_cost_adam", L.lib().poseidon_hybcomm_cost_adam(
+        M, N, B, P1, P2, *[ctypes.byref(x) for x in v]))
+    return tuple(x.value for x in v)
+
+
+def hybcomm_choose3(M: int, N: int, B: int, P: int) -> int:
+    """PS (0), SFB (1) or ADAM (2) by the busiest node's traffic on P
+    worker+server nodes."""
+    return _check("poseidon_hybcomm_choose3", L.lib().poseidon_hybcomm_choose3(M, N, B, P))
 
 
 # --------------------------------------------------------------------------

@@ -63,3 +63,39 @@ def test_workload_decisions():
                 assert api.hybcomm_choose(*s.shape, wl.B, wl.P) == api.SFB == oracle.hybcomm_choose(*s.shape, wl.B, wl.P)
     for P in (2, 4, 8, 16, 32):
         assert api.hybcomm_choose(4096, 4096, 32, P) == api.SFB
+
+
+def test_adam_cost_matches_enumerated_traffic():
+    """Table 1's Adam row against the enumerator: the holder alone (server
+    only, node 0), a plain worker, and a holder that is also a worker."""
+    rng = np.random.default_rng(2)
+    for _ in range(300):
+        M, N, B = (int(x) for x in rng.integers(1, 5000, 3))
+        P1, P2 = (int(x) for x in rng.integers(1, 40, 2))
+        server, worker, both = api.hybcomm_cost_adam(M, N, B, P1, P2)
+        # holder = first server; separate servers after it scale the units only
+        roles = [ROLE_SERVER] * P2 + [ROLE_WORKER] * P1
+        t = oracle.hybcomm_traffic(M, N, B, roles, oracle.ADAM)
+        assert server == t[0] and worker == t[P2], (M, N, B, P1, P2)
+        roles = [ROLE_WORKER | ROLE_SERVER] + [ROLE_SERVER] * (P2 - 1) + [ROLE_WORKER] * (P1 - 1)
+        assert both == oracle.hybcomm_traffic(M, N, B, roles, oracle.ADAM)[0], (M, N, B, P1, P2)
+
+
+def test_choose3_matches_enumerator_and_never_picks_adam():
+    """Three-way choice by the busiest node: equal to the oracle's enumeration
+    everywhere on a dense grid and on the paper's layers, and with P1 = P2 it
+    is always Alg. 1's choice (Adam never moves strictly less than both)."""
+    Bs = [0, 1, 2, 5, 13, 32, 64]
+    Ps = [1, 2, 3, 4, 5, 8, 16, 33]
+    for M, N in itertools.product(range(0, 49, 4), range(1, 49, 3)):
+        for B in Bs:
+            for P in Ps:
+                c = api.hybcomm_choose3(M, N, B, P)
+                assert c == oracle.hybcomm_choose3(M, N, B, P), (M, N, B, P)
+                assert c == api.hybcomm_choose(M, N, B, P) != api.ADAM, (M, N, B, P)
+    for M, N in [(4096, 25088), (4096, 4096), (21841, 4096), (1000, 1024)]:
+        for B in (1, 32, 128):
+            for P in (1, 2, 3, 8, 32, 128):
+                assert api.hybcomm_choose3(M, N, B, P) == oracle.hybcomm_choose3(M, N, B, P)
+    with pytest.raises(api.PoseidonError):
+        api.hybcomm_choose3(4, 4, 1, 0)

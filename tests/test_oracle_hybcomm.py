@@ -116,3 +116,22 @@ def test_invalid_arguments():
         oracle.hybcomm_choose(-1, 10, 1, 2)
     with pytest.raises(ValueError):
         oracle.hybcomm_traffic(10, 10, 1, [ROLE_WORKER, ROLE_WORKER], PS)   # no server
+
+
+
+def test_choose3_pins():
+    """The three-way choice on clusters of worker+server nodes.  Pins: P = 1
+    moves nothing (a three-way tie, SFB by the tie rule); the VGG19 4096 x 4096
+    layer of the worked example goes to SFB; a layer that fits in fewer values
+    than its factors (M = N = 8, B = 64) goes to PS; and Adam's busiest node
+    (the holder, Table 1's Server & Worker cell) moves at least as much as
+    the cheaper of PS and SFB: with x = MN, y = B(M+N) and P >= 2,
+    min(4x/P, 2y) <= min(2x, 2y) <= x + y, so (P-1)(x+y) is never below
+    min(4x(P-1)/P, 2y(P-1)) -- Adam is never chosen."""
+    assert oracle.hybcomm_choose3(4096, 4096, 32, 1) == SFB
+    assert oracle.hybcomm_choose3(4096, 4096, 32, 8) == SFB
+    assert oracle.hybcomm_choose3(8, 8, 64, 8) == PS
+    for P in (2, 3, 4, 8):
+        for M, N, B in ((8, 8, 64), (100, 3, 7), (64, 64, 32), (1, 1, 1)):
+            assert oracle.hybcomm_choose3(M, N, B, P) in (PS, SFB)
+            assert oracle.hybcomm_choose3(M, N, B, P) == oracle.hybcomm_choose(M, N, B, P)
