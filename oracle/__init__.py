@@ -10,10 +10,11 @@ numpy; inputs are fp32 like the layers they stand for, outputs are fresh arrays
 
 Functions and the passages they follow:
 
-* ``sf_delta`` / ``sf_apply`` / ``sf_apply_points`` -- sufficient-factor
+* ``sf_delta`` / ``sf_apply`` / ``sf_apply_points`` / ``sf_apply_momentum`` -- sufficient-factor
   reconstruction of a fully-connected layer's gradient, the sum over the P*B
   rank-1 factor pairs (Sec. 2.1 "Sufficient Factor Broadcasting", Eq. 2),
-  applied by one SGD step (Eq. 1).
+  applied by one SGD step (Eq. 1), or by a heavy-ball step with a momentum
+  buffer.
 * ``ps_apply`` / ``ps_apply_points`` -- parameter-server aggregation of the P
   workers' dense gradients and its application (Sec. 2.1 "Parameter Server",
   Sec. 4.1 "KV Store", "Managing Consistency"), with heavy-ball momentum.
@@ -65,6 +66,12 @@ def _load():
     lib.oracle_sf_apply_points.argtypes = [_f32p, _f32p, _f32p, _i64, _i64, _i64,
                                            _f32, _i64p, _i64p, _i64, _f32p]
     lib.oracle_sf_apply_points.restype = None
+    lib.oracle_sf_apply_momentum_rows.argtypes = [_f32p, _f32p, _f32p, _f32p, _i64, _i64, _i64,
+                                                  _f32, _f32, _i64, _i64]
+    lib.oracle_sf_apply_momentum_rows.restype = None
+    lib.oracle_sf_apply_momentum_points.argtypes = [_f32p, _f32p, _f32p, _f32p, _i64, _i64, _i64,
+                                                    _f32, _f32, _i64p, _i64p, _i64, _f32p, _f32p]
+    lib.oracle_sf_apply_momentum_points.restype = None
     lib.oracle_ps_apply_range.argtypes = [_f32p, _f32p, _i32, _i64, _f32, _f32,
                                           ctypes.c_void_p, _i64, _i64]
     lib.oracle_ps_apply_range.restype = ctypes.c_int
@@ -140,6 +147,39 @@ def sf_apply_points(W, U, V, lr: float, rows, cols) -> np.ndarray:
     _load().oracle_sf_apply_points(W.reshape(-1) if W.size else W, U, V, M, N, K,
                                    np.float32(lr), rows, cols, rows.size, out)
     return out
+
+
+def sf_apply_momentum(W, buf, U, V, lr: float, mu: float,
+                      rows: tuple[int, int] | None = None) -> tuple[np.ndarray, np.ndarray]:
+    """An SFB layer with a momentum buffer: returns (W', buf') with
+    buf' = (float)(mu * buf + U^T V) and W' = (float)(W - lr * buf'), the
+    gradient summed in fp64.  ``rows=(m0, m1)`` updates only those rows."""
+    W, buf, U, V = _f32c(W), _f32c(buf), _f32c(U), _f32c(V)
+    M, N, K = _sf_dims(U, V)
+    if W.shape != (M, N) or buf.shape != (M, N):
+        raise ValueError(f"W and buf must be {M} x {N}")
+    w_out, b_out = W.copy(), buf.copy()
+    m0, m1 = rows if rows is not None else (0, M)
+    _load().oracle_sf_apply_momentum_rows(w_out, b_out, U, V, M, N, K, np.float32(lr), np.float32(mu), m0, m1)
+    return w_out, b_out
+
+
+def sf_apply_momentum_points(W, buf, U, V, lr: float, mu: float, rows, cols):
+    """(W', buf') at the points (rows[i], cols[i])."""
+    W, buf, U, V = _f32c(W), _f32c(buf), _f32c(U), _f32c(V)
+    M, N, K = _sf_dims(U, V)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    if rows.shape != cols.shape:
+        raise ValueError("rows and cols must have the same shape")
+    if rows.size and (rows.min() < 0 or rows.max() >= M or cols.min() < 0 or cols.max() >= N):
+        raise IndexError("point outside W")
+    w_out = np.empty(rows.shape, dtype=np.float32)
+    b_out = np.empty(rows.shape, dtype=np.float32)
+    _load().oracle_sf_apply_momentum_points(W.reshape(-1) if W.size else W, buf.reshape(-1) if buf.size else buf,
+                                            U, V, M, N, K, np.float32(lr), np.float32(mu), rows, cols, rows.size,
+                                            w_out, b_out)
+    return w_out, b_out
 
 
 # --------------------------------------------------------------------------
@@ -248,8 +288,9 @@ def sync_iteration(layers, B: int, P: int, lr: float, mu: float):
     ``fc`` (bool), ``W`` (array), ``U``/``V`` (K x M / K x N, for FC layers),
     ``shards`` (P x n) and ``buf`` (n, or None).  Layers are processed from the
     last to the first (backpropagation order); each FC layer goes through
-    ``best_scheme``.  SFB layers take a plain SGD step; PS layers take the
-    momentum step.  Returns a list (forward order) of dicts with ``scheme``,
+    ``best_scheme``.  SFB layers take a plain SGD step, or the momentum step
+    when they carry a ``buf``; PS layers take the momentum step (when they
+    carry a ``buf``).  Returns a list (forward order) of dicts with ``scheme``,
     ``W`` and ``buf``."""
     out = [None] * len(layers)
     for l in range(len(layers) - 1, -1, -1):
@@ -261,8 +302,11 @@ def sync_iteration(layers, B: int, P: int, lr: float, mu: float):
         else:
             scheme = PS
         if scheme == SFB:
-            out[l] = {"scheme": SFB, "W": sf_apply(W, L["U"], L["V"], lr),
-                      "buf": None if L.get("buf") is None else np.array(L["buf"], copy=True)}
+            if L.get("buf") is None:
+                out[l] = {"scheme": SFB, "W": sf_apply(W, L["U"], L["V"], lr), "buf": None}
+            else:
+                w2, b2 = sf_apply_momentum(W, np.asarray(L["buf"]).reshape(W.shape), L["U"], L["V"], lr, mu)
+                out[l] = {"scheme": SFB, "W": w2, "buf": b2.reshape(-1)}
         else:
             w2, b2 = ps_apply(W.reshape(-1), L["shards"], lr, mu if L.get("buf") is not None else 0.0,
                               L.get("buf"))

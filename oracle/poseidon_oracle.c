@@ -113,6 +113,62 @@ void oracle_sf_apply_points(const float *W, const float *U, const float *V,
     }
 }
 
+/* An SFB layer that keeps a momentum buffer: the same heavy-ball rule as the
+ * parameter-server apply below, with the reconstructed gradient in place of
+ * the shard sum (the paper's solver settings use momentum for every layer;
+ * Eq. 1 itself is plain SGD):
+ *   b = (double)mu * buf[m][n] + dW[m][n];  buf' = (float)b;
+ *   W'  = (float)((double)W[m][n] - (double)lr * (double)buf').
+ * Rows m0 <= m < m1 only. */
+void oracle_sf_apply_momentum_rows(float *W, float *buf, const float *U, const float *V,
+                                   int64_t M, int64_t N, int64_t K, float lr, float mu,
+                                   int64_t m0, int64_t m1)
+{
+    if (m0 < 0) m0 = 0;
+    if (m1 > M) m1 = M;
+    #pragma omp parallel
+    {
+        double *acc = (double *)malloc((size_t)(N > 0 ? N : 1) * sizeof(double));
+        #pragma omp for schedule(static)
+        for (int64_t m = m0; m < m1; ++m) {
+            for (int64_t n = 0; n < N; ++n)
+                acc[n] = 0.0;
+            for (int64_t k = 0; k < K; ++k) {
+                const double u = (double)U[k * M + m];
+                const float *vk = V + k * N;
+                for (int64_t n = 0; n < N; ++n)
+                    acc[n] += u * (double)vk[n];
+            }
+            float *w = W + m * N, *b = buf + m * N;
+            for (int64_t n = 0; n < N; ++n) {
+                const float nb = (float)((double)mu * (double)b[n] + acc[n]);
+                b[n] = nb;
+                w[n] = (float)((double)w[n] - (double)lr * (double)nb);
+            }
+        }
+        free(acc);
+    }
+}
+
+/* The same at cnt chosen points of W and buf (not modified); w_out[i] and
+ * b_out[i] receive the updated values. */
+void oracle_sf_apply_momentum_points(const float *W, const float *buf, const float *U, const float *V,
+                                     int64_t M, int64_t N, int64_t K, float lr, float mu,
+                                     const int64_t *rows, const int64_t *cols, int64_t cnt,
+                                     float *w_out, float *b_out)
+{
+    #pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < cnt; ++i) {
+        const int64_t m = rows[i], n = cols[i];
+        double acc = 0.0;
+        for (int64_t k = 0; k < K; ++k)
+            acc += (double)U[k * M + m] * (double)V[k * N + n];
+        const float nb = (float)((double)mu * (double)buf[m * N + n] + acc);
+        b_out[i] = nb;
+        w_out[i] = (float)((double)W[m * N + n] - (double)lr * (double)nb);
+    }
+}
+
 /* ------------------------------------------------------------------------ */
 /* Parameter-server aggregation and apply (Sec. 2.1, "Parameter Server",     */
 /* steps (1)-(2); Sec. 4.1, "KV Store" and "Managing Consistency"): the       */

@@ -170,3 +170,93 @@ def test_sfb_degenerate_shapes():
     assert oracle.sf_delta(np.zeros((2, 0), np.float32), np.zeros((2, 5), np.float32)).shape == (0, 5)
     with pytest.raises(ValueError):
         oracle.sf_apply(W, np.zeros((2, 4), np.float32), np.zeros((2, 4), np.float32), 0.1)
+
+
+# ---------------------------------------------------------------------------
+# An SFB layer with a momentum buffer (heavy-ball step on the rebuilt gradient)
+# ---------------------------------------------------------------------------
+
+def test_sfb_momentum_matches_torch_sgd_momentum():
+    """Three steps of torch.optim.SGD(momentum) on fp64 copies, fed the fp64
+    U^T V of fresh factors each step and starting from a nonzero buffer,
+    agree with the oracle to 1 ulp in W and buf."""
+    rng = np.random.default_rng(11)
+    K, M, N = 12, 9, 7
+    lr, mu = 0.01, 0.9
+    W = (0.01 * rng.standard_normal((M, N))).astype(np.float32)
+    buf = (1e-2 * rng.standard_normal((M, N))).astype(np.float32)
+    p = torch.nn.Parameter(torch.tensor(W, dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=float(np.float32(lr)), momentum=float(np.float32(mu)))
+    opt.state[p]["momentum_buffer"] = torch.tensor(buf, dtype=torch.float64)
+    w, b = W, buf
+    for step in range(3):
+        U = rng.standard_normal((K, M)).astype(np.float32)
+        V = rng.standard_normal((K, N)).astype(np.float32)
+        p.grad = torch.tensor(U.astype(np.float64).T @ V.astype(np.float64))
+        opt.step()
+        w, b = oracle.sf_apply_momentum(w, b, U, V, lr, mu)
+        # the oracle rounds W and buf to fp32 each step, torch keeps fp64
+        ref_b = opt.state[p]["momentum_buffer"].numpy().astype(np.float32)
+        np.testing.assert_allclose(b, ref_b, rtol=0, atol=5e-7 * (step + 1) * float(np.abs(ref_b).max()))
+        np.testing.assert_allclose(w, p.detach().numpy().astype(np.float32), rtol=0, atol=1e-8 * (step + 1))
+    # first step exactly: from the same fp32 start
+    U = rng.standard_normal((K, M)).astype(np.float32)
+    V = rng.standard_normal((K, N)).astype(np.float32)
+    p2 = torch.nn.Parameter(torch.tensor(W, dtype=torch.float64))
+    opt2 = torch.optim.SGD([p2], lr=float(np.float32(lr)), momentum=float(np.float32(mu)))
+    opt2.state[p2]["momentum_buffer"] = torch.tensor(buf, dtype=torch.float64)
+    p2.grad = torch.tensor(U.astype(np.float64).T @ V.astype(np.float64))
+    opt2.step()
+    w1, b1 = oracle.sf_apply_momentum(W, buf, U, V, lr, mu)
+    np.testing.assert_array_max_ulp(b1, opt2.state[p2]["momentum_buffer"].numpy().astype(np.float32), maxulp=1)
+    # W' differs from the fp64 step only by lr times the rounding of buf'
+    # (the oracle applies the stored fp32 buffer) plus its own rounding.
+    ref_w = p2.detach().numpy()
+    assert np.all(np.abs(w1 - ref_w) <= np.spacing(np.abs(ref_w).astype(np.float32)) + lr * np.spacing(np.abs(b1)))
+
+
+def test_sfb_momentum_zero_buffer_is_rounded_gradient():
+    """mu = 0 (or buf = 0): buf' is the reconstructed gradient rounded once to
+    fp32, bit for bit; with lr = 0, W is unchanged."""
+    rng = np.random.default_rng(12)
+    K, M, N = 20, 13, 11
+    U = rng.standard_normal((K, M)).astype(np.float32)
+    V = rng.standard_normal((K, N)).astype(np.float32)
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    dW = (U.astype(np.float64).T @ V.astype(np.float64)).astype(np.float32)
+    w, b = oracle.sf_apply_momentum(W, np.zeros((M, N), np.float32), U, V, 0.0, 0.9)
+    assert np.array_equal(w, W)
+    np.testing.assert_array_max_ulp(b, dW, maxulp=1)
+    _, b0 = oracle.sf_apply_momentum(W, rng.standard_normal((M, N)).astype(np.float32), U, V, 0.1, 0.0)
+    assert np.array_equal(b0, (oracle.sf_delta(U, V)).astype(np.float32))
+
+
+def test_sfb_momentum_constant_gradient_closed_form():
+    """With the same factors every step from buf = 0, the buffer after T steps
+    is g (1 - mu^T) / (1 - mu) (geometric series)."""
+    rng = np.random.default_rng(13)
+    K, M, N = 4, 5, 6
+    mu = 0.5
+    U = rng.standard_normal((K, M)).astype(np.float32)
+    V = rng.standard_normal((K, N)).astype(np.float32)
+    g = U.astype(np.float64).T @ V.astype(np.float64)
+    w, b = np.zeros((M, N), np.float32), np.zeros((M, N), np.float32)
+    for T in range(1, 8):
+        w, b = oracle.sf_apply_momentum(w, b, U, V, 0.0, mu)
+        np.testing.assert_allclose(b, g * (1 - mu ** T) / (1 - mu), rtol=1e-6 * T, atol=1e-7)
+
+
+def test_sfb_momentum_points_and_rows_agree_with_full():
+    rng = np.random.default_rng(14)
+    K, M, N = 9, 21, 15
+    U = rng.standard_normal((K, M)).astype(np.float32)
+    V = rng.standard_normal((K, N)).astype(np.float32)
+    W = rng.standard_normal((M, N)).astype(np.float32)
+    buf = rng.standard_normal((M, N)).astype(np.float32)
+    fw, fb = oracle.sf_apply_momentum(W, buf, U, V, 0.3, 0.9)
+    rows, cols = rng.integers(0, M, 40), rng.integers(0, N, 40)
+    pw, pb = oracle.sf_apply_momentum_points(W, buf, U, V, 0.3, 0.9, rows, cols)
+    assert np.array_equal(pw, fw[rows, cols]) and np.array_equal(pb, fb[rows, cols])
+    rw, rb = oracle.sf_apply_momentum(W, buf, U, V, 0.3, 0.9, rows=(4, 10))
+    assert np.array_equal(rw[4:10], fw[4:10]) and np.array_equal(rb[4:10], fb[4:10])
+    assert np.array_equal(rw[:4], W[:4]) and np.array_equal(rb[10:], buf[10:])
