@@ -311,6 +311,18 @@ def main():
         layers.append({"tensor": spec.name, "scheme": "SFB",
                        "ms": round(it_ms, 4), "tflops": round(f / it_ms / 1e9, 2) if it_ms else None,
                        "alone_ms": round(ms, 4), "alone_tflops": round(f / ms / 1e9, 2)})
+    # The same layers with a momentum buffer (poseidon_sf_apply_momentum):
+    # W and buf each read and written once.
+    layers_mom = []
+    for (W, U, V), i in zip(fc_list, fc_idx):
+        spec = host[i]["spec"]
+        mbuf = torch.zeros_like(W)
+        ms = _time(lambda: api.sf_apply_momentum(W, mbuf, U, V, wl.lr, wl.momentum, stream=stream))
+        M, N = spec.shape
+        layers_mom.append({"tensor": spec.name, "alone_ms": round(ms, 4),
+                           "tflops": round(_sf_flops(spec, wl.K) / ms / 1e9, 2),
+                           "gbs": round(4.0 * (4 * M * N + wl.K * (M + N)) / ms / 1e6, 1)})
+        del mbuf
     for i, (h, sch) in enumerate(zip(host, schemes)):
         spec = h["spec"]
         if sch == api.SFB:
@@ -368,6 +380,7 @@ def main():
         "sfb_tflops": round(sfb_tflops, 2) if sfb_tflops else None,
         "ps_gbs": round(ps_gbs, 1) if ps_gbs else None,
         "layers_sfb": layers,
+        "layers_sfb_momentum": layers_mom,
     }
     if args.wfbp == "on" and wl.config == 5:
         print("[bench] WFBP phase (synthetic backward)", file=sys.stderr, flush=True)

@@ -78,6 +78,25 @@ int poseidon_sf_apply(float* W, const float* U, const float* V,
                       int64_t M, int64_t N, int64_t K, float lr,
                       hipStream_t stream);
 
+/*
+ * The same reconstruction for an FC layer that keeps a heavy-ball momentum
+ * buffer (the update rule of poseidon_ps_apply, with the reconstructed
+ * gradient in place of the shard sum; Eq. 2 for the gradient):
+ *
+ *     buf[m][n] <- momentum * buf[m][n] + sum_{k<K} U[k][m] * V[k][n]
+ *     W[m][n]   <- W[m][n] - lr * buf[m][n]
+ *
+ * buf: M x N row-major like W, caller-owned, updated in place; W and buf are
+ * each read and written once (16 M N bytes).  K = 0 is a step on the buffer
+ * alone (U and V may then be NULL).  Layouts and accumulation as for
+ * poseidon_sf_apply.  Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (as
+ * poseidon_sf_apply; also NULL buf with M*N > 0, or buf overlapping W, U or
+ * V) or POSEIDON_ERR_HIP.
+ */
+int poseidon_sf_apply_momentum(float* W, float* buf, const float* U, const float* V,
+                               int64_t M, int64_t N, int64_t K, float lr, float momentum,
+                               hipStream_t stream);
+
 /* One fully-connected layer of a grouped SF reconstruction. */
 typedef struct poseidon_sf_tensor {
     float*       W;   /* M x N row-major, updated in place */
@@ -205,7 +224,7 @@ int poseidon_hybcomm_choose3(int64_t M, int64_t N, int64_t B, int64_t P);
  * flattened, M*N = n).  U/V are the SF payload (K x M and K x N, K = P*B) and
  * shards the dense payload (P x M*N); a tensor carries the payload of the
  * scheme it will use and may set the other to NULL.  buf is the momentum
- * buffer (M*N values) used by the PS apply, or NULL for plain SGD.
+ * buffer (M*N values) used by either scheme's update, or NULL for plain SGD.
  */
 typedef struct poseidon_tensor {
     int32_t      kind;     /* POSEIDON_KIND_FC or POSEIDON_KIND_OTHER */
@@ -245,9 +264,10 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation order: the SFB updates (bound by the matrix cores) on the
  * pool's first stream, the PS updates (bound by memory bandwidth) on its
  * second, so that the two kinds overlap; a one-stream pool runs everything in
- * order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), PS
- * tensors take poseidon_ps_apply(W, shards, P, M*N, lr, momentum, buf)
- * (momentum is used only when buf != NULL).  Every pool stream first waits for the work already
+ * order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
+ * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
+ * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,
+ * momentum, buf) (momentum is used only when buf != NULL).  Every pool stream first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so
  * the call behaves like one asynchronous operation on `stream` (the
  * bulk-synchronous barrier of Sec. 4.1 "Managing Consistency").

@@ -21,7 +21,7 @@ ADAM = 2
 KIND_FC = 0
 KIND_OTHER = 1
 
-EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_batch", "poseidon_ps_apply", "poseidon_ps_apply_batch",
+EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply_batch", "poseidon_ps_apply", "poseidon_ps_apply_batch",
            "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_hybcomm_cost_adam",
            "poseidon_hybcomm_choose3", "poseidon_pool_create",
            "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_sync_iteration_wfbp",
@@ -68,6 +68,7 @@ def lib() -> ctypes.CDLL:
     vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float
     L.poseidon_sf_apply.argtypes = [vp, vp, vp, i64, i64, i64, f32, vp]
     L.poseidon_ps_apply.argtypes = [vp, vp, i32, i64, f32, f32, vp, vp]
+    L.poseidon_sf_apply_momentum.argtypes = [vp, vp, vp, vp, i64, i64, i64, f32, f32, vp]
     L.poseidon_hybcomm_choose.argtypes = [i64, i64, i64, i64]
     L.poseidon_hybcomm_cost.argtypes = [i64, i64, i64, i64, i64,
                                         ctypes.POINTER(i64), ctypes.POINTER(i64)]

@@ -74,6 +74,25 @@ def sf_apply(W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, lr: float, strea
             _stream_handle(stream, W.device)))
 
 
+def sf_apply_momentum(W: torch.Tensor, buf: torch.Tensor, U: torch.Tensor, V: torch.Tensor, lr: float,
+                      momentum: float, stream=None) -> None:
+    """buf = momentum * buf + U^T @ V; W -= lr * buf, in place
+    (poseidon_sf_apply_momentum)."""
+    _dev_f32("W", W), _dev_f32("buf", buf), _dev_f32("U", U), _dev_f32("V", V)
+    _same_device(W, buf, U, V)
+    if W.dim() != 2 or U.dim() != 2 or V.dim() != 2:
+        raise ValueError("W, U, V must be 2-D")
+    M, N = W.shape
+    K = U.shape[0]
+    if U.shape != (K, M) or V.shape != (K, N) or buf.numel() != M * N:
+        raise ValueError(f"shapes: W {tuple(W.shape)}, buf {tuple(buf.shape)}, U {tuple(U.shape)}, "
+                         f"V {tuple(V.shape)}")
+    with torch.cuda.device(W.device):
+        _check("poseidon_sf_apply_momentum", L.lib().poseidon_sf_apply_momentum(
+            W.data_ptr(), buf.data_ptr(), U.data_ptr(), V.data_ptr(), M, N, K, float(lr), float(momentum),
+            _stream_handle(stream, W.device)))
+
+
 def sf_apply_batch(layers: list, lr: float, stream=None) -> None:
     """poseidon_sf_apply for several FC layers with the same K in one pass
     (poseidon_sf_apply_batch).  ``layers`` is a list of (W, U, V)."""

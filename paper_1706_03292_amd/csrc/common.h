@@ -29,6 +29,8 @@ hipError_t launch_sf_apply(float* W, const float* U, const float* V,
                            int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream);
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
                            float lr, float momentum, float* buf, hipStream_t stream);
+hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M,
+                                    int64_t N, int64_t K, float lr, float mu, hipStream_t stream);
 
 // One FC layer of a grouped SF launch (same layout as poseidon_sf_tensor).
 struct SfTensor {
@@ -60,6 +62,8 @@ hipError_t launch_ps_apply_batch(const PsTensor* tensors, int32_t count, int32_t
 // Argument checks of the public entry points (no device work).
 int check_sf_args(const float* W, const float* U, const float* V,
                   int64_t M, int64_t N, int64_t K);
+int check_sf_momentum_args(const float* W, const float* buf, const float* U, const float* V,
+                           int64_t M, int64_t N, int64_t K);
 int check_ps_args(const float* W, const float* shards, int32_t P, int64_t n,
                   float momentum, const float* buf);
 

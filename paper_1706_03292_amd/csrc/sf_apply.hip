@@ -160,10 +160,15 @@ constexpr int BUF_RSRC_WORD3 = 0x00020000;
 // floats, Bs: 2 x BK*LDB; buffer b starts at b*BK*LD), so that several
 // inlined variants share one allocation.  Always inlined: as a called function it would keep both the
 // 16-byte and the scalar operand loads and pay the call convention.
-template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int EPI, bool HUGE_N>
+//
+// MOM: the layer keeps a momentum buffer (same shape as W): the epilogue
+// updates buf <- mu*buf + dW and W <- W - lr*buf, and K may be 0 (a step on
+// the buffer alone).
+template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int EPI, bool HUGE_N,
+          bool MOM = false>
 __device__ __forceinline__ void sf_tile(
     float* As, float* Bs, float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
-    int64_t M, int64_t N, int64_t K, float lr, int tm, int tn)
+    int64_t M, int64_t N, int64_t K, float lr, int tm, int tn, float* __restrict__ buf = nullptr, float mu = 0.f)
 {
     using T = SfTile<BM, BN, BK, WM, WN>;
     constexpr int SA = BK * T::LDA, SB = BK * T::LDB;   // floats per LDS buffer
@@ -212,6 +217,76 @@ __device__ __forceinline__ void sf_tile(
 
     // Epilogue: accumulator register r of lane l holds block row
     // 8*(r/4) + 4*(l/32) + r%4, block column l%32.
+    if constexpr (MOM) {
+        if (nkt > 0)
+            mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + last * SA + a_off, Bs + last * SB + b_off);
+        const int rows_left = static_cast<int>(M - m0 < BM ? M - m0 : BM);
+        const int cols_left = static_cast<int>(N - n0 < BN ? N - n0 : BN);
+        if constexpr (!HUGE_N) {
+            // Half an MFMA block (8 values per lane) at a time: W and buf
+            // loads in flight together, then both stores.  Elements outside
+            // W read the tile origin (inside W) and are not stored.
+            const int64_t first = m0 * N + n0;
+            const int64_t avail = (M * N - first) * 4;
+            const int nrec = static_cast<int>(avail < 0x7fffffff ? avail : 0x7fffffff);
+            const __amdgpu_buffer_rsrc_t wr =
+                __builtin_amdgcn_make_buffer_rsrc(W + first, static_cast<short>(0), nrec, BUF_RSRC_WORD3);
+            const __amdgpu_buffer_rsrc_t br =
+                __builtin_amdgcn_make_buffer_rsrc(buf + first, static_cast<short>(0), nrec, BUF_RSRC_WORD3);
+            const int ni = static_cast<int>(N);
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j) {
+                    const int col = wn + 32 * j + lcol;
+#pragma unroll
+                    for (int h = 0; h < 16; h += 8) {
+                        float wv[8], bv[8];
+                        int off[8];
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) {
+                            const int r = h + q;
+                            const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                            off[q] = (row < rows_left && col < cols_left) ? (row * ni + col) * 4 : 0;
+                            wv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wr, off[q], 0, 0));
+                            bv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(br, off[q], 0, 0));
+                        }
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) {
+                            const int r = h + q;
+                            const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                            if (row < rows_left && col < cols_left) {
+                                const float nb = fmaf(mu, bv[q], acc[i][j][r]);
+                                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, nb), br, off[q], 0, 0);
+                                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fmaf(-lr, nb, wv[q])), wr,
+                                                                      off[q], 0, 0);
+                            }
+                        }
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
+                }
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j) {
+                    const int col = wn + 32 * j + lcol;
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                        if (row < rows_left && col < cols_left) {
+                            const int64_t e = (m0 + row) * N + n0 + col;
+                            const float nb = fmaf(mu, buf[e], acc[i][j][r]);
+                            buf[e] = nb;
+                            W[e] = fmaf(-lr, nb, W[e]);
+                        }
+                    }
+                }
+            }
+        }
+        return;
+    }
     if constexpr (!HUGE_N) {
         // Buffer-addressed epilogue: byte offsets from the tile's first
         // element fit in 31 bits (the host picks HUGE_N otherwise).
@@ -332,6 +407,21 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
     int tm, tn;
     tile_coords<GM>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
     sf_tile<BM, BN, BK, WM, WN, VEC_A, VEC_B, PREFETCH_W, EPI, HUGE_N>(As, Bs, W, U, V, M, N, K, lr, tm, tn);
+}
+
+// The layer keeps a momentum buffer (poseidon_sf_apply_momentum).
+template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, int OCC, bool HUGE_N>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_mom_kernel(
+    float* __restrict__ W, float* __restrict__ buf, const float* __restrict__ U, const float* __restrict__ V,
+    int64_t M, int64_t N, int64_t K, float lr, float mu, int tiles_m, int tiles_n)
+{
+    using T = SfTile<BM, BN, BK, WM, WN>;
+    __shared__ float As[2 * BK * T::LDA];
+    __shared__ float Bs[2 * BK * T::LDB];
+    int tm, tn;
+    tile_coords<8>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
+    sf_tile<BM, BN, BK, WM, WN, VEC_A, VEC_B, false, 1, HUGE_N, true>(As, Bs, W, U, V, M, N, K, lr, tm, tn, buf, mu);
 }
 
 // ---------------------------------------------------------------------------
@@ -458,6 +548,54 @@ hipError_t launch_sf_apply(float* W, const float* U, const float* V,
     return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, 8>(W, U, V, M, N, K, lr, stream);
 }
 
+namespace {
+
+template <int BM, int BN, int BK, int WM, int WN, bool VA, bool VB>
+void launch_mom(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
+                float mu, int tiles, int tiles_m, int tiles_n, hipStream_t stream)
+{
+    constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
+    if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
+        sf_apply_mom_kernel<BM, BN, BK, WM, WN, VA, VB, 4, false><<<tiles, NT, 0, stream>>>(
+            W, buf, U, V, M, N, K, lr, mu, tiles_m, tiles_n);
+    else
+        sf_apply_mom_kernel<BM, BN, BK, WM, WN, VA, VB, 4, true><<<tiles, NT, 0, stream>>>(
+            W, buf, U, V, M, N, K, lr, mu, tiles_m, tiles_n);
+}
+
+template <int BM, int BN, int BK, int WM, int WN>
+hipError_t launch_mom_cfg(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
+                          float lr, float mu, hipStream_t stream)
+{
+    const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+    if (tiles_m * tiles_n > INT32_MAX)
+        return hipErrorInvalidValue;
+    const int t = static_cast<int>(tiles_m * tiles_n), tmi = static_cast<int>(tiles_m),
+              tni = static_cast<int>(tiles_n);
+    const bool va = (M % 4 == 0) && aligned16(U), vb = (N % 4 == 0) && aligned16(V);
+    if (va && vb)
+        launch_mom<BM, BN, BK, WM, WN, true, true>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
+    else if (va)
+        launch_mom<BM, BN, BK, WM, WN, true, false>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
+    else if (vb)
+        launch_mom<BM, BN, BK, WM, WN, false, true>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
+    else
+        launch_mom<BM, BN, BK, WM, WN, false, false>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+// The same tile choice as launch_sf_apply.
+hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N,
+                                    int64_t K, float lr, float mu, hipStream_t stream)
+{
+    const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
+        return launch_mom_cfg<128, 128, 16, 64, 64>(W, buf, U, V, M, N, K, lr, mu, stream);
+    return launch_mom_cfg<64, 64, 32, 32, 32>(W, buf, U, V, M, N, K, lr, mu, stream);
+}
+
 // Grouped launch: every layer whose tile offsets fit 32 bits joins one tile
 // list (128 x 128 tiles) when the group has at least two tiles per CU; the
 // others, and groups too small to fill the chip, take per-layer launches.
@@ -530,7 +668,36 @@ int check_sf_args(const float* W, const float* U, const float* V,
     return POSEIDON_OK;
 }
 
+int check_sf_momentum_args(const float* W, const float* buf, const float* U, const float* V,
+                           int64_t M, int64_t N, int64_t K)
+{
+    if (M < 0 || N < 0 || K < 0)
+        return POSEIDON_ERR_INVALID_ARG;
+    if (M == 0 || N == 0)
+        return POSEIDON_OK;
+    if (!W || !buf || (K > 0 && (!U || !V)))
+        return POSEIDON_ERR_INVALID_ARG;
+    if (M > INT64_MAX / 4 / N || K > INT64_MAX / 4 / M || K > INT64_MAX / 4 / N)
+        return POSEIDON_ERR_INVALID_ARG;
+    const int64_t wb = M * N * 4;
+    if (overlaps(W, wb, buf, wb) || overlaps(W, wb, U, K * M * 4) || overlaps(W, wb, V, K * N * 4) ||
+        overlaps(buf, wb, U, K * M * 4) || overlaps(buf, wb, V, K * N * 4))
+        return POSEIDON_ERR_INVALID_ARG;
+    return POSEIDON_OK;
+}
+
 }  // namespace poseidon
+
+extern "C" int poseidon_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M,
+                                          int64_t N, int64_t K, float lr, float momentum, hipStream_t stream)
+{
+    const int rc = poseidon::check_sf_momentum_args(W, buf, U, V, M, N, K);
+    if (rc != POSEIDON_OK || M == 0 || N == 0)
+        return rc;
+    return poseidon::launch_sf_apply_momentum(W, buf, U, V, M, N, K, lr, momentum, stream) == hipSuccess
+               ? POSEIDON_OK
+               : POSEIDON_ERR_HIP;
+}
 
 extern "C" int poseidon_sf_apply(float* W, const float* U, const float* V,
                                  int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)

@@ -159,8 +159,9 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         if (scheme == POSEIDON_SFB) {
             if (n > 0 && K > 0 && (!x.U || !x.V))
                 return POSEIDON_ERR_PAYLOAD;
-            rc = check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
-            if (n > 0 && K > 0)
+            rc = x.buf ? check_sf_momentum_args(x.W, x.buf, x.U, x.V, x.M, x.N, K)
+                       : check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
+            if (n > 0 && (K > 0 || x.buf))
                 ++active;
         } else {
             if (n > 0 && !x.shards)
@@ -231,10 +232,13 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         if (n == 0)
             continue;
         if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
-            if (K == 0)
+            if (K == 0 && !x.buf)
                 continue;
             hipStream_t s = pool->streams[0];
-            if (!timed(s, POSEIDON_SFB, t, 0, [&] { return launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s); }))
+            if (!timed(s, POSEIDON_SFB, t, 0, [&] {
+                    return x.buf ? launch_sf_apply_momentum(x.W, x.buf, x.U, x.V, x.M, x.N, K, lr, momentum, s)
+                                 : launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s);
+                }))
                 return POSEIDON_ERR_HIP;
         } else {
             const int32_t si = used == 1 ? 0 : 1;

@@ -51,6 +51,11 @@ def test_invalid_arguments_rejected_before_device_work():
     # Empty work is a successful no-op, even with NULL pointers.
     assert lib.poseidon_sf_apply(None, None, None, 0, 4, 4, 0.1, None) == L.OK
     assert lib.poseidon_sf_apply(None, None, None, 4, 4, 0, 0.1, None) == L.OK
+    # sf_apply_momentum: NULL buf, buf overlapping W, empty, K = 0 needs no factors
+    assert lib.poseidon_sf_apply_momentum(fake, None, fake, fake, 4, 4, 4, 0.1, 0.9, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_sf_apply_momentum(fake, ctypes.c_void_p(0x1008), ctypes.c_void_p(0x900000),
+                                          ctypes.c_void_p(0xA00000), 4, 4, 4, 0.1, 0.9, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_sf_apply_momentum(None, None, None, None, 0, 4, 4, 0.1, 0.9, None) == L.OK
     # ps_apply: P < 1, momentum without a buffer, overlap, negative n, empty.
     assert lib.poseidon_ps_apply(fake, ctypes.c_void_p(0x900000), 0, 8, 0.1, 0.0, None, None) == L.ERR_INVALID_ARG
     assert lib.poseidon_ps_apply(fake, ctypes.c_void_p(0x900000), 2, 8, 0.1, 0.9, None, None) == L.ERR_INVALID_ARG
