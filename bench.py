@@ -74,10 +74,11 @@ def _kernel_source_hash(name: str) -> str:
 
 
 def _stored_traffic(kernel: str, source: str):
-    """HBM bytes per step of `kernel` from the committed rocprofv3 counter
-    summaries under profiles/ (lines 'traffic: kernel=... source_sha256=...
-    bytes_per_step=...'), or None when no summary matches the current source
-    of that kernel (the counters were taken on different code)."""
+    """HBM bytes of `kernel` (per step or per launch, as the roofline it goes
+    with) from the committed rocprofv3 counter summaries under profiles/
+    (lines 'traffic: kernel=... source_sha256=... bytes_per_step=...' or
+    '... bytes_per_launch=...'), or None when no summary matches the current
+    source of that kernel (the counters were taken on different code)."""
     want = _kernel_source_hash(source)
     pdir = os.path.join(ROOT, "profiles")
     if not os.path.isdir(pdir):
@@ -91,7 +92,7 @@ def _stored_traffic(kernel: str, source: str):
                 continue
             kv = dict(x.split("=", 1) for x in line[len("traffic:"):].split() if "=" in x)
             if kv.get("kernel") == kernel and kv.get("source_sha256") == want:
-                return float(kv["bytes_per_step"])
+                return float(kv.get("bytes_per_step", kv.get("bytes_per_launch")))
     return None
 
 
@@ -273,12 +274,11 @@ def main():
 
     # The PS applies share the GPU with the SF reconstructions during the
     # iteration (by design), so their bandwidth is measured in a phase of its
-    # own: the same launches, every PS tensor of the step one after another on
-    # one stream with nothing else running, between HIP events on that stream.
-    # The batched pass (poseidon_ps_apply_batch) over the same tensors and the
-    # largest tensor's launch alone are timed too.
+    # own: the library issues the same launches, every PS tensor of the step
+    # one after another on one pool stream with nothing else running, and its
+    # timing events bracket each launch on that stream.  The batched pass
+    # (poseidon_ps_apply_batch) over the same tensors is timed too.
     ps_list = [(t["W"], t["shards"], t.get("buf")) for t in reversed(devt) if t["spec"].kind != "fc"]
-    big = max(range(len(ps_list)), key=lambda i: ps_list[i][0].numel())
 
     def _time(fn):
         out = []
@@ -292,12 +292,26 @@ def main():
                 out.append(a.elapsed_time(b))
         return sum(out) / len(out)
 
-    ps_ms = _time(lambda: [api.ps_apply(W.view(-1), G, wl.lr, wl.momentum, buf, stream=stream)
-                           for W, G, buf in ps_list])
+    ps_idx = [i for i, t in enumerate(devt) if t["spec"].kind != "fc"]
+    ps_it = api.SyncIteration(pool, [devt[i] for i in ps_idx], wl.B, wl.P, wl.lr, wl.momentum)
+    ps_seq_ms = _time(lambda: ps_it(stream))          # fork, 35 launches, join
+    pool.set_timing(True)
+    ps_launch = {}
+    for _ in range(ksteps):
+        ps_it(stream)
+        for r in pool.launch_times():
+            ps_launch[r["tensor"]] = ps_launch.get(r["tensor"], 0.0) + r["ms"] / ksteps
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    ps_ms = sum(ps_launch.values())
     ps_batch_ms = _time(lambda: api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream))
-    W_, G_, b_ = ps_list[big]
-    ps_big_ms = _time(lambda: api.ps_apply(W_.view(-1), G_, wl.lr, wl.momentum, b_, stream=stream))
-    ps_big_bytes = float(W_.numel()) * (4 * wl.P + (16 if b_ is not None else 8))
+    # The dominant PS launches: the tensors of the largest size (in VGG19 the
+    # seven 512x512x3x3 kernels, 82% of the step's PS bytes).
+    n_big = max(devt[i]["W"].numel() for i in ps_idx)
+    j_bigs = [j for j, i in enumerate(ps_idx) if devt[i]["W"].numel() == n_big]
+    big_spec = devt[ps_idx[j_bigs[0]]]["spec"]
+    ps_big_ms = sum(ps_launch[j] for j in j_bigs) / len(j_bigs)
+    ps_big_bytes = _ps_bytes(big_spec, wl.P, "buf" in devt[ps_idx[j_bigs[0]]])
 
     sfb_flops = sfb_bytes = 0.0
     ps_bytes = ps_in_iter = sfb_ms = 0.0
@@ -333,7 +347,7 @@ def main():
             ps_bytes += _ps_bytes(spec, wl.P, "buf" in h)
             ps_in_iter += launch_ms.get(i, 0.0)
     sfb_tflops = sfb_flops / sfb_ms / 1e9 if sfb_ms else None
-    ps_gbs = ps_bytes / ps_ms / 1e6 if ps_ms else None
+    ps_gbs = ps_big_bytes / ps_big_ms / 1e6 if ps_big_ms else None
     n_ps = sum(1 for s_ in schemes if s_ == api.PS)
 
     result = {
@@ -364,16 +378,18 @@ def main():
                         "achieved": round(ps_gbs, 1) if ps_gbs else None,
                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
                         "frac": round(ps_gbs / PEAK_HBM_GBS, 4) if ps_gbs else None,
-                        "traffic": _stored_traffic("ps_apply", "ps_apply.hip"),
-                        "work": f"(4P+16) bytes per element over the {n_ps} PS tensors of one step "
-                                f"({ps_bytes / 1e9:.3f} GB) / the duration of their launches one after "
-                                f"another on one stream with nothing else running ({ps_ms:.4f} ms); inside "
-                                f"the iteration they overlap the SF reconstructions (summed launch time "
-                                f"{ps_in_iter:.4f} ms)",
-                        "largest_tensor": {"tensor": host[[i for i, h in enumerate(host)
-                                                           if h["spec"].kind != "fc"][::-1][big]]["spec"].name,
-                                           "ms": round(ps_big_ms, 4),
-                                           "gbs": round(ps_big_bytes / ps_big_ms / 1e6, 1)},
+                        "traffic": _stored_traffic("ps_apply_largest", "ps_apply.hip"),
+                        "work": f"(4P+16) bytes per element, {n_big} elements per launch "
+                                f"({ps_big_bytes / 1e6:.1f} MB) / the average duration of the {len(j_bigs)} "
+                                f"launches of that size ({ps_big_ms:.4f} ms; the largest PS tensors, "
+                                f"{len(j_bigs) * ps_big_bytes / ps_bytes:.0%} of the step's PS bytes), "
+                                f"issued by the library one after another on one stream with nothing else "
+                                f"running, timed by its events on that stream",
+                        "step": {"tensors": n_ps, "bytes": ps_bytes,
+                                 "sequence_ms": round(ps_seq_ms, 4),
+                                 "sequence_gbs": round(ps_bytes / ps_seq_ms / 1e6, 1),
+                                 "summed_launch_ms": round(ps_ms, 4),
+                                 "in_iteration_summed_launch_ms": round(ps_in_iter, 4)},
                         "batched_pass": {"ms": round(ps_batch_ms, 4),
                                          "gbs": round(ps_bytes / ps_batch_ms / 1e6, 1)}},
         "event_ms_per_step": round(event_ms, 4),

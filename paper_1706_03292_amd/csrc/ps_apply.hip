@@ -6,17 +6,23 @@
 //
 // The kernel is bound by HBM bandwidth: per element it reads P shard values
 // plus W and buf and writes W and buf (4P + 16 bytes), against ~P + 3 flops.
-// Each thread owns 16-byte groups of four consecutive elements, issues all of
-// a group's shard loads before the dependent adds (bytes in flight), streams
-// the single-use shards with non-temporal loads, and walks the array with a
-// grid-stride loop sized to keep every CU busy.  A scalar variant covers sizes
-// that are not a multiple of four or arrays that are not 16-byte aligned.
+// Each thread owns one 16-byte group of four consecutive elements, issues all
+// of its shard loads before the dependent adds (bytes in flight) and streams
+// the single-use shards with non-temporal loads.  One-wave workgroups, one
+// group per thread, as many workgroups as groups: a launch-shape sweep over
+// 37K-16.8M elements (block size 64-1024, one or two groups per thread,
+// grid-stride loops capped at 4-16 workgroups per CU) found this within 3% of
+// the best everywhere and 10% faster than a capped grid-stride loop on large
+// tensors, whose last partial pass leaves the chip half idle.  A scalar
+// variant covers sizes that are not a multiple of four or arrays that are not
+// 16-byte aligned.
 #include "common.h"
 
 namespace poseidon {
 namespace {
 
-constexpr int PS_THREADS = 256;
+constexpr int PS_THREADS = 64;    // one wave per workgroup (single-tensor and batched launches)
+constexpr int PS_THREADS_1 = PS_THREADS;
 constexpr int PS_CHUNK = 8;       // shard loads in flight per step when P is a runtime value
 
 __device__ inline f4 fma4(float a, f4 b, f4 c)
@@ -88,15 +94,15 @@ __device__ inline float shard_sum1(const float* __restrict__ G, int P, int64_t n
 }
 
 template <int PT, bool MOM>
-__global__ __launch_bounds__(PS_THREADS) void ps_apply_vec4(
+__global__ __launch_bounds__(PS_THREADS_1) void ps_apply_vec4(
     float* __restrict__ W, const float* __restrict__ G, int P, int64_t n4,
     float lr, float mu, float* __restrict__ buf)
 {
     const f4* G4 = reinterpret_cast<const f4*>(G);
     f4* W4 = reinterpret_cast<f4*>(W);
     f4* B4 = reinterpret_cast<f4*>(buf);
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS + threadIdx.x; i < n4; i += stride) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS_1;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS_1 + threadIdx.x; i < n4; i += stride) {
         const f4 s = shard_sum4<PT>(G4, P, n4, i);
         f4 w = W4[i];
         if constexpr (MOM) {
@@ -111,12 +117,12 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_vec4(
 }
 
 template <int PT, bool MOM>
-__global__ __launch_bounds__(PS_THREADS) void ps_apply_scalar(
+__global__ __launch_bounds__(PS_THREADS_1) void ps_apply_scalar(
     float* __restrict__ W, const float* __restrict__ G, int P, int64_t n,
     float lr, float mu, float* __restrict__ buf)
 {
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS + threadIdx.x; i < n; i += stride) {
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS_1;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS_1 + threadIdx.x; i < n; i += stride) {
         const float s = shard_sum1<PT>(G, P, n, i);
         float w = W[i];
         if constexpr (MOM) {
@@ -135,13 +141,15 @@ hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, f
                      float* buf, bool vec, hipStream_t stream)
 {
     const int64_t items = vec ? n / 4 : n;
-    const int64_t want = (items + PS_THREADS - 1) / PS_THREADS;
-    const int64_t cap = static_cast<int64_t>(device_cu_count()) * 8;
+    // One item per thread; the kernels' grid-stride loop only matters beyond
+    // 2^30 workgroups.
+    const int64_t want = (items + PS_THREADS_1 - 1) / PS_THREADS_1;
+    const int64_t cap = int64_t{1} << 30;
     const int grid = static_cast<int>(want < cap ? want : cap);
     if (vec)
-        ps_apply_vec4<PT, MOM><<<grid, PS_THREADS, 0, stream>>>(W, G, P, items, lr, mu, buf);
+        ps_apply_vec4<PT, MOM><<<grid, PS_THREADS_1, 0, stream>>>(W, G, P, items, lr, mu, buf);
     else
-        ps_apply_scalar<PT, MOM><<<grid, PS_THREADS, 0, stream>>>(W, G, P, items, lr, mu, buf);
+        ps_apply_scalar<PT, MOM><<<grid, PS_THREADS_1, 0, stream>>>(W, G, P, items, lr, mu, buf);
     return hipGetLastError();
 }
 
@@ -167,8 +175,8 @@ hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, 
 // groups when the tensor allows it, single elements otherwise).
 // ---------------------------------------------------------------------------
 
-constexpr int PS_BLOCK_ELEMS = 4096;     // elements per work block in a batch
-constexpr int PS_BATCH_MAX_GRID = 8192;  // workgroups per batched launch (they loop over the work blocks)
+constexpr int PS_BLOCK_ELEMS = 4 * PS_THREADS;  // elements per work block: one 16-byte group per thread
+constexpr int PS_BATCH_MAX_GRID = 1 << 30;     // one workgroup per work block below this
 
 struct PsBatchItem {
     float* W;
@@ -189,11 +197,18 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_batch_kernel(const PsBatc
                                                                     float mu, int total_blocks)
 {
     // Workgroup g handles work blocks g, g + gridDim.x, ... (one pass when the
-    // grid covers every block).
-    int t = 0;
+    // grid covers every block); the block's tensor is found by binary search
+    // over the descriptors' first blocks (uniform, scalar loads).
     for (int b = blockIdx.x; b < total_blocks; b += gridDim.x) {
-        while (t + 1 < args.count && b >= args.item[t + 1].first_block)
-            ++t;
+        int lo = 0, hi = args.count - 1;
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (args.item[mid].first_block <= b)
+                lo = mid;
+            else
+                hi = mid - 1;
+        }
+        const int t = lo;
         float* __restrict__ W = args.item[t].W;
         const float* __restrict__ G = args.item[t].G;
         float* __restrict__ buf = args.item[t].buf;
