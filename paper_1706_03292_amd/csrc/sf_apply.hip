@@ -9,21 +9,33 @@
 // operand, 64 lanes, 16 accumulator registers per lane).
 //
 // Tiling: a workgroup owns a BM x BN block of W and loops over K in steps of
-// BK.  U[k0:k0+BK, m0:m0+BM] and V[k0:k0+BK, n0:n0+BN] are staged through LDS,
-// double-buffered, with the next step's global loads in flight while the
-// matrix cores work on the current one, and each wave reads the operand
-// fragments of the next MFMA step while the current one runs.  Each wave owns a
-// WM x WN sub-block (WM/32 x WN/32 MFMA blocks).
+// BK; each wave owns a WM x WN sub-block (WM/32 x WN/32 MFMA blocks).  The
+// K-slices U[k0:k0+BK, m0:m0+BM] and V[k0:k0+BK, n0:n0+BN] go straight from
+// global memory into LDS with the gfx950 LDS-direct buffer loads (each lane
+// moves 16 bytes, a wave instruction fills 1 KB of LDS), two slices in
+// flight: the next slice streams in while the matrix cores work on the
+// current one, with no register staging and no LDS store instructions.
+// Out-of-range operand reads are handled by the buffer resource's range
+// check (they read 0), so the K tail needs no branch; reads past the end of a
+// row in the last tile column fetch the next row's values, which only feed
+// outputs outside W that are never stored.  Inside a slice, 16-byte chunks of
+// odd rows are stored with their chunk index XOR 8, so the two half-waves of
+// an MFMA operand read (rows k and k+1) hit disjoint LDS banks.
 //
 // The SGD update is the epilogue: W is read once and written once, straight
 // from the accumulators, so the gradient is never materialised.  On tiles that
-// lie wholly inside W the epilogue's loads are issued before the last K step
-// (their latency hides behind its MFMAs) and carry no per-element branch.
+// lie wholly inside W the first block of W is loaded before the last K step
+// (its latency hides behind that step's MFMAs) and no access carries a
+// per-element branch.
 //
 // Tile order: the hardware hands consecutive workgroups to the 8 XCDs in turn,
 // and each XCD has its own L2.  Workgroup ids are remapped so that every XCD
 // owns one contiguous run of tiles, walked a group of tile rows at a time, so
 // the tiles an XCD runs at the same time share U and V panels in its L2.
+//
+// Operands whose byte offsets do not fit the 32-bit buffer offsets (K*M or
+// K*N of 2^29 elements and more, or rows over 4,194,303 elements) take a
+// register-staged variant of the same tile with 64-bit addressing.
 #include <vector>
 
 #include "common.h"
@@ -33,9 +45,13 @@ namespace {
 
 typedef float f16v __attribute__((ext_vector_type(16)));
 typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));   // 16 bytes, 4-byte aligned
+typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int LDS_PAD = 4;    // floats of padding per LDS row (keeps 16-byte alignment)
 constexpr int NUM_XCD = 8;    // MI355X: 8 accelerator complex dies, one L2 each
+
+// Buffer resource word 3 for raw (untyped) dword accesses on CDNA.  The raw
+// buffer builtins move 32-bit integers: values are bit-cast, never converted.
+constexpr int BUF_RSRC_WORD3 = 0x00020000;
 
 template <int BM, int BN, int BK, int WM, int WN>
 struct SfTile {
@@ -44,26 +60,374 @@ struct SfTile {
     static constexpr int THREADS = NWM * NWN * 64;
     static constexpr int TM = WM / 32;
     static constexpr int TN = WN / 32;
-    static constexpr int LDA = BM + LDS_PAD;
-    static constexpr int LDB = BN + LDS_PAD;
-    static constexpr int A_V4 = BK * BM / 4 / THREADS;   // 16-byte groups per thread per step
-    static constexpr int B_V4 = BK * BN / 4 / THREADS;
     static_assert(BM % WM == 0 && BN % WN == 0 && WM % 32 == 0 && WN % 32 == 0, "tile");
     static_assert(BK % 2 == 0, "MFMA depth is 2");
-    static_assert(A_V4 * THREADS * 4 == BK * BM && B_V4 * THREADS * 4 == BK * BN, "staging");
 };
 
-// Load one BK x (4*COLS4) slice of a K-major operand X (row length ld = its
-// number of columns) into registers: group j of this thread covers row
-// g / COLS4 and columns 4*(g % COLS4) .. +3 with g = tid + j*THREADS.
-// Out-of-range rows/columns read as 0, which adds nothing to the sum.  Every
-// group is one 16-byte load: with VEC (ld % 4 == 0, X 16-byte aligned) a group
-// is wholly in or out; otherwise rows start at any 4-byte boundary (global
-// loads of several dwords need only 4-byte alignment) and only a group that
-// runs past the end of its row is read element by element.
-template <int NV4, int COLS4, int THREADS, bool VEC>
-__device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int64_t ld,
-                                  int64_t rows, int64_t k0, int64_t c0, int tid)
+// Workgroup id -> (tile row, tile column): contiguous runs per XCD, GM tile
+// rows at a time inside a run.
+template <int GM>
+__device__ inline void tile_coords(int bid, int tiles, int tiles_m, int tiles_n, int& tm, int& tn)
+{
+    const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
+    const int x = bid % NUM_XCD, j = bid / NUM_XCD;
+    const int t = x * q + (x < r ? x : r) + j;
+    const int per_group = GM * tiles_n;
+    const int g = t / per_group;
+    const int first_m = g * GM;
+    const int rows = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
+    const int in = t - g * per_group;
+    tm = first_m + in % rows;
+    tn = in / rows;
+}
+
+template <int TM, int TN>
+__device__ __forceinline__ void zero_acc(f16v (&acc)[TM][TN])
+{
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                acc[i][j][r] = 0.f;
+}
+
+// ---------------------------------------------------------------------------
+// Epilogues.  Accumulator register r of lane l holds block row
+// 8*(r/4) + 4*(l/32) + r%4, block column l%32.  `wr` (and `br`) address W
+// (buf) from the tile's first element; the byte offsets of a tile fit in 31
+// bits (the host checks).
+// ---------------------------------------------------------------------------
+
+// Row offset (bytes / n4) of accumulator register r in block row i.
+__device__ __forceinline__ constexpr int acc_row(int i, int r) { return 32 * i + 8 * (r >> 2) + (r & 3); }
+
+// Values of W's first MFMA block that an interior tile loads ahead of the last
+// K step (as many as the register budget holds without spilling).
+constexpr int W_PRE = 10;
+
+__device__ __forceinline__ void load_w_block(float (&wv)[16], __amdgpu_buffer_rsrc_t wr, int voff, int n4, int r0,
+                                             int r1)
+{
+#pragma unroll
+    for (int r = r0; r < r1; ++r)
+        wv[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wr, voff, acc_row(0, r) * n4, 0));
+}
+
+// Interior tile: one shared lane offset (voff) and uniform row offsets, one
+// MFMA block at a time; the first W_PRE values of block 0 are already in wv.
+template <int TM, int TN>
+__device__ __forceinline__ void epi_interior(const f16v (&acc)[TM][TN], float (&wv)[16], __amdgpu_buffer_rsrc_t wr,
+                                             int voff, int n4, float lr)
+{
+#pragma unroll
+    for (int c = 0; c < TM * TN; ++c) {
+        const int i = c / TN, j = c % TN;
+#pragma unroll
+        for (int r = (c == 0 ? W_PRE : 0); r < 16; ++r)
+            wv[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                wr, voff + 128 * j, acc_row(i, r) * n4, 0));
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], wv[r])), wr,
+                                                  voff + 128 * j, acc_row(i, r) * n4, 0);
+    }
+}
+
+// Ragged edge tile: every element gets its own lane offset; an element outside
+// W loads the tile's first element instead (always inside W, value unused) and
+// is not stored.
+template <int TM, int TN>
+__device__ __forceinline__ void epi_edge(const f16v (&acc)[TM][TN], __amdgpu_buffer_rsrc_t wr, int ni, int wm, int wn,
+                                         int lrow, int lcol, int rows_left, int cols_left, float lr)
+{
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = wn + 32 * j + lcol;
+            float ev[16];
+            int off[16];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                off[r] = (row < rows_left && col < cols_left) ? (row * ni + col) * 4 : 0;
+                ev[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wr, off[r], 0, 0));
+            }
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                if (row < rows_left && col < cols_left)
+                    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], ev[r])),
+                                                          wr, off[r], 0, 0);
+            }
+            // One MFMA block at a time: keeps the scheduler from hoisting
+            // every block's loads and offsets together.
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+}
+
+// Momentum: buf <- mu*buf + dW, W <- W - lr*buf, half an MFMA block (8 values
+// per lane) at a time, W and buf loads in flight together, then both stores.
+template <int TM, int TN>
+__device__ __forceinline__ void epi_momentum(const f16v (&acc)[TM][TN], __amdgpu_buffer_rsrc_t wr,
+                                             __amdgpu_buffer_rsrc_t br, int ni, int wm, int wn, int lrow, int lcol,
+                                             int rows_left, int cols_left, float lr, float mu)
+{
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int col = wn + 32 * j + lcol;
+#pragma unroll
+            for (int h = 0; h < 16; h += 8) {
+                float wv[8], bv[8];
+                int off[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int r = h + q;
+                    const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                    off[q] = (row < rows_left && col < cols_left) ? (row * ni + col) * 4 : 0;
+                    wv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wr, off[q], 0, 0));
+                    bv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(br, off[q], 0, 0));
+                }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int r = h + q;
+                    const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
+                    if (row < rows_left && col < cols_left) {
+                        const float nb = fmaf(mu, bv[q], acc[i][j][r]);
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, nb), br, off[q], 0, 0);
+                        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fmaf(-lr, nb, wv[q])), wr,
+                                                              off[q], 0, 0);
+                    }
+                }
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+    }
+}
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(float* base, int64_t M, int64_t N, int64_t first)
+{
+    const int64_t avail = (M * N - first) * 4;
+    return __builtin_amdgcn_make_buffer_rsrc(base + first, static_cast<short>(0),
+                                             static_cast<int>(avail < 0x7fffffff ? avail : 0x7fffffff),
+                                             BUF_RSRC_WORD3);
+}
+
+// The epilogue of one tile for offsets that fit 31 bits.  PREF: the caller
+// has loaded block 0 of an interior tile into wv.
+template <int TM, int TN, bool MOM>
+__device__ __forceinline__ void epilogue(const f16v (&acc)[TM][TN], float (&wv)[16], __amdgpu_buffer_rsrc_t wr,
+                                         float* __restrict__ buf, int64_t M, int64_t N, int64_t m0, int64_t n0,
+                                         int BM, int BN, int wm, int wn, int lrow, int lcol, bool interior,
+                                         float lr, float mu)
+{
+    const int ni = static_cast<int>(N);
+    const int rows_left = static_cast<int>(M - m0 < BM ? M - m0 : BM);
+    const int cols_left = static_cast<int>(N - n0 < BN ? N - n0 : BN);
+    if constexpr (MOM) {
+        const __amdgpu_buffer_rsrc_t br = tile_rsrc(buf, M, N, m0 * N + n0);
+        epi_momentum<TM, TN>(acc, wr, br, ni, wm, wn, lrow, lcol, rows_left, cols_left, lr, mu);
+    } else if (interior) {
+        epi_interior<TM, TN>(acc, wv, wr, ((wm + 4 * lrow) * ni + wn + lcol) * 4, ni * 4, lr);
+    } else {
+        epi_edge<TM, TN>(acc, wr, ni, wm, wn, lrow, lcol, rows_left, cols_left, lr);
+    }
+}
+
+// ---------------------------------------------------------------------------
+// LDS-direct tile (the main path).
+// ---------------------------------------------------------------------------
+
+// Each pipeline stage is an LDS object of its own: the compiler can then tell
+// that the in-flight LDS-direct loads into one stage do not alias the LDS
+// reads of the other, and does not wait for them before reading.
+template <int SIZE, int S, int WHICH>
+struct LdsStage {
+    static __device__ __forceinline__ float* ptr()
+    {
+        __shared__ float a[SIZE];
+        return a;
+    }
+};
+
+// Chunk (16 bytes) c of slice row k is stored at chunk position c ^ swz(k).
+__device__ __forceinline__ constexpr int swz(int k) { return (k & 1) << 3; }
+
+// Wait for every outstanding vector-memory load of this wave (the LDS-direct
+// loads included); the workgroup barrier that follows makes every wave's
+// loads of the slice visible.
+__device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
+
+template <int BM, int BN, int BK, int WM, int WN>
+struct Direct {
+    using T = SfTile<BM, BN, BK, WM, WN>;
+    static constexpr int NT = T::THREADS;
+    template <int S> static __device__ __forceinline__ float* A() { return LdsStage<BK * BM, S, 0>::ptr(); }
+    template <int S> static __device__ __forceinline__ float* B() { return LdsStage<BK * BN, S, 1>::ptr(); }
+
+    // One BK x BX slice of a K-major operand into an LDS stage.  Wave
+    // instruction q fills LDS chunks 64q .. 64q+63 (row-major, BX/4 chunks a
+    // row); its lane l loads global chunk (row g / (BX/4), column chunk
+    // (g % (BX/4)) ^ swz(row)) with g = 64q + l.  `rs` addresses the operand
+    // from the tile's first column; voffsets are bytes from there, and the
+    // resource's size makes every read at or past row K return 0.
+    template <int BX>
+    static __device__ __forceinline__ void issue_panel(__amdgpu_buffer_rsrc_t rs, float* stage, int ld_bytes, int k0,
+                                                       int tid)
+    {
+        constexpr int CPR = BX / 4;
+        constexpr int PER = BK * CPR / NT;
+        static_assert(PER * NT == BK * CPR, "slice");
+        const int wave = tid >> 6, lane = tid & 63;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int g0 = (wave + j * (NT / 64)) * 64;
+            const int g = g0 + lane;
+            const int k = g / CPR;
+            const int c = (g % CPR) ^ swz(k);
+            const int voff = (k0 + k) * ld_bytes + c * 16;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(stage + g0 * 4), 16, voff, 0, 0, 0);
+        }
+    }
+
+    template <int S>
+    static __device__ __forceinline__ void issue(__amdgpu_buffer_rsrc_t ur, __amdgpu_buffer_rsrc_t vr, int ldu,
+                                                 int ldv, int kt, int tid)
+    {
+        issue_panel<BM>(ur, A<S>(), ldu, kt * BK, tid);
+        issue_panel<BN>(vr, B<S>(), ldv, kt * BK, tid);
+    }
+
+    // One BK-deep step of the contraction out of LDS stage S: the MFMA
+    // operands of step kk+2 are read while the matrix cores work on step kk.
+    template <int S>
+    static __device__ __forceinline__ void mma(f16v (&acc)[T::TM][T::TN], int wm, int wn, int lane)
+    {
+        const float* a_s = A<S>();
+        const float* b_s = B<S>();
+        const int lrow = lane >> 5, lcol = lane & 31;
+        auto at = [&](const float* s, int ld, int kk, int x) {
+            const int k = kk + lrow;
+            return s[k * ld + ((((x >> 2) ^ swz(k)) << 2) | (x & 3))];
+        };
+        float a[2][T::TM], b[2][T::TN];
+#pragma unroll
+        for (int i = 0; i < T::TM; ++i)
+            a[0][i] = at(a_s, BM, 0, wm + 32 * i + lcol);
+#pragma unroll
+        for (int j = 0; j < T::TN; ++j)
+            b[0][j] = at(b_s, BN, 0, wn + 32 * j + lcol);
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            const int c = (kk >> 1) & 1;
+            if (kk + 2 < BK) {
+#pragma unroll
+                for (int i = 0; i < T::TM; ++i)
+                    a[c ^ 1][i] = at(a_s, BM, kk + 2, wm + 32 * i + lcol);
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j)
+                    b[c ^ 1][j] = at(b_s, BN, kk + 2, wn + 32 * j + lcol);
+            }
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i)
+#pragma unroll
+                for (int j = 0; j < T::TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[c][i], b[c][j], acc[i][j], 0, 0, 0);
+        }
+    }
+
+    // Slice kt (not the last) in stage S: wait until it has landed, then
+    // start slice kt+1 into the other stage (free: every wave has passed the
+    // barrier after reading it) and multiply.
+    template <int S>
+    static __device__ __forceinline__ void step(f16v (&acc)[T::TM][T::TN], __amdgpu_buffer_rsrc_t ur,
+                                                __amdgpu_buffer_rsrc_t vr, int ldu, int ldv, int kt, int wm, int wn,
+                                                int lane, int tid)
+    {
+        wait_loads();
+        __syncthreads();
+        issue<S ^ 1>(ur, vr, ldu, ldv, kt + 1, tid);
+        mma<S>(acc, wm, wn, lane);
+    }
+};
+
+// One BM x BN tile of W: the whole K loop and the fused update.  Slice kt
+// lives in stage (nkt-1-kt) & 1, so the last slice is always in stage 0 and
+// the loop body and the final step are each emitted once.
+template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+__device__ __forceinline__ void sf_tile_direct(float* __restrict__ W, const float* __restrict__ U,
+                                               const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
+                                               float lr, int tm, int tn, float* __restrict__ buf, float mu)
+{
+    using D = Direct<BM, BN, BK, WM, WN>;
+    using T = SfTile<BM, BN, BK, WM, WN>;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = tid >> 6;
+    const int64_t m0 = static_cast<int64_t>(tm) * BM;
+    const int64_t n0 = static_cast<int64_t>(tn) * BN;
+    const int wm = (wave / T::NWN) * WM;
+    const int wn = (wave % T::NWN) * WN;
+    const int lrow = lane >> 5, lcol = lane & 31;
+    const bool interior = (m0 + BM <= M) && (n0 + BN <= N);
+
+    f16v acc[T::TM][T::TN];
+    zero_acc(acc);
+    const int64_t first = m0 * N + n0;
+    const __amdgpu_buffer_rsrc_t wr = tile_rsrc(W, M, N, first);
+    const int ni = static_cast<int>(N);
+    const int voff = ((wm + 4 * lrow) * ni + wn + lcol) * 4;
+    float wv[16];
+
+    const int nkt = static_cast<int>((K + BK - 1) / BK);
+    if (nkt > 0) {
+        const __amdgpu_buffer_rsrc_t ur = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(U) + m0, static_cast<short>(0), static_cast<int>((K * M - m0) * 4), BUF_RSRC_WORD3);
+        const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(V) + n0, static_cast<short>(0), static_cast<int>((K * N - n0) * 4), BUF_RSRC_WORD3);
+        const int ldu = static_cast<int>(M) * 4, ldv = static_cast<int>(N) * 4;
+        int kt = 0;
+        if ((nkt & 1) == 0) {
+            D::template issue<1>(ur, vr, ldu, ldv, 0, tid);
+            D::template step<1>(acc, ur, vr, ldu, ldv, 0, wm, wn, lane, tid);
+            kt = 1;
+        } else {
+            D::template issue<0>(ur, vr, ldu, ldv, 0, tid);
+        }
+        for (; kt < nkt - 1; kt += 2) {
+            D::template step<0>(acc, ur, vr, ldu, ldv, kt, wm, wn, lane, tid);
+            D::template step<1>(acc, ur, vr, ldu, ldv, kt + 1, wm, wn, lane, tid);
+        }
+        wait_loads();
+        __syncthreads();
+        if (!MOM && interior)
+            load_w_block(wv, wr, voff, ni * 4, 0, W_PRE);
+        D::template mma<0>(acc, wm, wn, lane);
+    }
+    epilogue<T::TM, T::TN, MOM>(acc, wv, wr, buf, M, N, m0, n0, BM, BN, wm, wn, lrow, lcol, interior, lr, mu);
+}
+
+// ---------------------------------------------------------------------------
+// Register-staged tile for operands beyond 32-bit offsets: K-slices go global
+// -> registers -> LDS (row-padded by 4 floats), double-buffered; 64-bit
+// addressing throughout, and W rows too long for 32-bit tile offsets
+// (WIDE) take guarded 64-bit accesses in the epilogue.
+// ---------------------------------------------------------------------------
+constexpr int LDS_PAD = 4;
+
+// Load one BK x (4*COLS4) slice of a K-major operand X (row length ld) into
+// registers: group j of this thread covers row g / COLS4 and columns
+// 4*(g % COLS4) .. +3 with g = tid + j*THREADS.  Out-of-range rows/columns
+// read as 0.  Global loads of several dwords need only 4-byte alignment;
+// only a group that runs past the end of its row is read element by element.
+template <int NV4, int COLS4, int THREADS>
+__device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int64_t ld, int64_t rows, int64_t k0,
+                                  int64_t c0, int tid)
 {
 #pragma unroll
     for (int j = 0; j < NV4; ++j) {
@@ -72,9 +436,7 @@ __device__ inline void load_panel(f4 (&r)[NV4], const float* __restrict__ X, int
         const int64_t c = c0 + 4 * (g % COLS4);
         const float* src = X + k * ld + c;
         const bool kin = k < rows;
-        if constexpr (VEC) {
-            r[j] = (kin && c < ld) ? *reinterpret_cast<const f4*>(src) : f4{0.f, 0.f, 0.f, 0.f};
-        } else if (kin && c + 3 < ld) {
+        if (kin && c + 3 < ld) {
             r[j] = *reinterpret_cast<const f4u*>(src);
         } else {
             r[j].x = (kin && c + 0 < ld) ? src[0] : 0.f;
@@ -95,83 +457,37 @@ __device__ inline void store_panel(float* lds, const f4 (&r)[NV4], int tid)
     }
 }
 
-// Workgroup id -> (tile row, tile column): contiguous runs per XCD, GM tile
-// rows at a time inside a run (GM = 0: plain row-major order, no remap).
-template <int GM>
-__device__ inline void tile_coords(int bid, int tiles, int tiles_m, int tiles_n, int& tm, int& tn)
-{
-    if constexpr (GM == 0) {
-        tm = bid / tiles_n;
-        tn = bid % tiles_n;
-    } else {
-        const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
-        const int x = bid % NUM_XCD, j = bid / NUM_XCD;
-        const int t = x * q + (x < r ? x : r) + j;
-        const int per_group = GM * tiles_n;
-        const int g = t / per_group;
-        const int first_m = g * GM;
-        const int rows = (tiles_m - first_m) < GM ? (tiles_m - first_m) : GM;
-        const int in = t - g * per_group;
-        tm = first_m + in % rows;
-        tn = in / rows;
-    }
-}
-
-// One BK-deep step of the contraction out of LDS: each wave reads its U and V
-// fragments for MFMA step kk+2 while the matrix cores work on step kk (the
-// compiler interleaves the reads with the MFMAs; pinning other orders with
-// scheduling barriers or priorities measured no faster).
 template <int BK, int LDA, int LDB, int TM, int TN>
-__device__ inline void mma_step(f16v (&acc)[TM][TN], const float* a_s, const float* b_s)
+__device__ inline void mma_staged(f16v (&acc)[TM][TN], const float* a_s, const float* b_s)
 {
-    float a[2][TM], b[2][TN];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-        a[0][i] = a_s[32 * i];
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
-        b[0][j] = b_s[32 * j];
 #pragma unroll
     for (int kk = 0; kk < BK; kk += 2) {
-        const int c = (kk >> 1) & 1;
-        if (kk + 2 < BK) {
+        float a[TM], b[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                a[c ^ 1][i] = a_s[(kk + 2) * LDA + 32 * i];
+        for (int i = 0; i < TM; ++i)
+            a[i] = a_s[kk * LDA + 32 * i];
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                b[c ^ 1][j] = b_s[(kk + 2) * LDB + 32 * j];
-        }
+        for (int j = 0; j < TN; ++j)
+            b[j] = b_s[kk * LDB + 32 * j];
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
             for (int j = 0; j < TN; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[c][i], b[c][j], acc[i][j], 0, 0, 0);
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[i], b[j], acc[i][j], 0, 0, 0);
     }
 }
 
-// Buffer resource word 3 for raw (untyped) dword accesses on CDNA.  The raw
-// buffer builtins move 32-bit integers: values are bit-cast, never converted.
-constexpr int BUF_RSRC_WORD3 = 0x00020000;
-
-// One BM x BN tile of W: the whole K loop and the fused update.  EPI: MFMA
-// blocks of W (16 values per lane each) read per epilogue chunk.  The
-// double-buffered K slices live in the caller's LDS arrays (As: 2 x BK*LDA
-// floats, Bs: 2 x BK*LDB; buffer b starts at b*BK*LD), so that several
-// inlined variants share one allocation.  Always inlined: as a called function it would keep both the
-// 16-byte and the scalar operand loads and pay the call convention.
-//
-// MOM: the layer keeps a momentum buffer (same shape as W): the epilogue
-// updates buf <- mu*buf + dW and W <- W - lr*buf, and K may be 0 (a step on
-// the buffer alone).
-template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int EPI, bool HUGE_N,
-          bool MOM = false>
-__device__ __forceinline__ void sf_tile(
-    float* As, float* Bs, float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
-    int64_t M, int64_t N, int64_t K, float lr, int tm, int tn, float* __restrict__ buf = nullptr, float mu = 0.f)
+template <int BM, int BN, int BK, int WM, int WN, bool WIDE, bool MOM>
+__device__ __forceinline__ void sf_tile_staged(float* As, float* Bs, float* __restrict__ W,
+                                               const float* __restrict__ U, const float* __restrict__ V, int64_t M,
+                                               int64_t N, int64_t K, float lr, int tm, int tn,
+                                               float* __restrict__ buf, float mu)
 {
     using T = SfTile<BM, BN, BK, WM, WN>;
-    constexpr int SA = BK * T::LDA, SB = BK * T::LDB;   // floats per LDS buffer
+    constexpr int LDA = BM + LDS_PAD, LDB = BN + LDS_PAD;
+    constexpr int SA = BK * LDA, SB = BK * LDB;
+    constexpr int A_V4 = BK * BM / 4 / T::THREADS, B_V4 = BK * BN / 4 / T::THREADS;
+    static_assert(A_V4 * T::THREADS * 4 == BK * BM && B_V4 * T::THREADS * 4 == BK * BN, "staging");
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -180,202 +496,43 @@ __device__ __forceinline__ void sf_tile(
     const int64_t n0 = static_cast<int64_t>(tn) * BN;
     const int wm = (wave / T::NWN) * WM;
     const int wn = (wave % T::NWN) * WN;
-    const int lrow = lane >> 5;        // which of the two k of an MFMA step this lane supplies
-    const int lcol = lane & 31;
-    const bool interior = (m0 + BM <= M) && (n0 + BN <= N);
+    const int lrow = lane >> 5, lcol = lane & 31;
 
     f16v acc[T::TM][T::TN];
-#pragma unroll
-    for (int i = 0; i < T::TM; ++i)
-#pragma unroll
-        for (int j = 0; j < T::TN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                acc[i][j][r] = 0.f;
-
-    f4 ra[T::A_V4], rb[T::B_V4];
+    zero_acc(acc);
+    f4 ra[A_V4], rb[B_V4];
     const int64_t nkt = (K + BK - 1) / BK;
-
-    load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, 0, m0, tid);
-    load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, 0, n0, tid);
-    store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As, ra, tid);
-    store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs, rb, tid);
-    __syncthreads();
-
-    const int a_off = lrow * T::LDA + wm + lcol;
-    const int b_off = lrow * T::LDB + wn + lcol;
-    for (int64_t kt = 0; kt + 1 < nkt; ++kt) {
-        const int cur = static_cast<int>(kt & 1);
-        load_panel<T::A_V4, BM / 4, T::THREADS, VEC_A>(ra, U, M, K, (kt + 1) * BK, m0, tid);
-        load_panel<T::B_V4, BN / 4, T::THREADS, VEC_B>(rb, V, N, K, (kt + 1) * BK, n0, tid);
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + cur * SA + a_off, Bs + cur * SB + b_off);
-        store_panel<T::A_V4, BM / 4, T::THREADS, T::LDA>(As + (cur ^ 1) * SA, ra, tid);
-        store_panel<T::B_V4, BN / 4, T::THREADS, T::LDB>(Bs + (cur ^ 1) * SB, rb, tid);
+    if (nkt > 0) {
+        load_panel<A_V4, BM / 4, T::THREADS>(ra, U, M, K, 0, m0, tid);
+        load_panel<B_V4, BN / 4, T::THREADS>(rb, V, N, K, 0, n0, tid);
+        store_panel<A_V4, BM / 4, T::THREADS, LDA>(As, ra, tid);
+        store_panel<B_V4, BN / 4, T::THREADS, LDB>(Bs, rb, tid);
         __syncthreads();
+        const int a_off = lrow * LDA + wm + lcol;
+        const int b_off = lrow * LDB + wn + lcol;
+        for (int64_t kt = 0; kt < nkt; ++kt) {
+            const int cur = static_cast<int>(kt & 1);
+            if (kt + 1 < nkt) {
+                load_panel<A_V4, BM / 4, T::THREADS>(ra, U, M, K, (kt + 1) * BK, m0, tid);
+                load_panel<B_V4, BN / 4, T::THREADS>(rb, V, N, K, (kt + 1) * BK, n0, tid);
+            }
+            mma_staged<BK, LDA, LDB, T::TM, T::TN>(acc, As + cur * SA + a_off, Bs + cur * SB + b_off);
+            if (kt + 1 < nkt) {
+                store_panel<A_V4, BM / 4, T::THREADS, LDA>(As + (cur ^ 1) * SA, ra, tid);
+                store_panel<B_V4, BN / 4, T::THREADS, LDB>(Bs + (cur ^ 1) * SB, rb, tid);
+            }
+            __syncthreads();
+        }
     }
-    const int last = static_cast<int>((nkt - 1) & 1);
-
-    // Epilogue: accumulator register r of lane l holds block row
-    // 8*(r/4) + 4*(l/32) + r%4, block column l%32.
-    if constexpr (MOM) {
-        if (nkt > 0)
-            mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + last * SA + a_off, Bs + last * SB + b_off);
-        const int rows_left = static_cast<int>(M - m0 < BM ? M - m0 : BM);
-        const int cols_left = static_cast<int>(N - n0 < BN ? N - n0 : BN);
-        if constexpr (!HUGE_N) {
-            // Half an MFMA block (8 values per lane) at a time: W and buf
-            // loads in flight together, then both stores.  Elements outside
-            // W read the tile origin (inside W) and are not stored.
-            const int64_t first = m0 * N + n0;
-            const int64_t avail = (M * N - first) * 4;
-            const int nrec = static_cast<int>(avail < 0x7fffffff ? avail : 0x7fffffff);
-            const __amdgpu_buffer_rsrc_t wr =
-                __builtin_amdgcn_make_buffer_rsrc(W + first, static_cast<short>(0), nrec, BUF_RSRC_WORD3);
-            const __amdgpu_buffer_rsrc_t br =
-                __builtin_amdgcn_make_buffer_rsrc(buf + first, static_cast<short>(0), nrec, BUF_RSRC_WORD3);
-            const int ni = static_cast<int>(N);
-#pragma unroll
-            for (int i = 0; i < T::TM; ++i) {
-#pragma unroll
-                for (int j = 0; j < T::TN; ++j) {
-                    const int col = wn + 32 * j + lcol;
-#pragma unroll
-                    for (int h = 0; h < 16; h += 8) {
-                        float wv[8], bv[8];
-                        int off[8];
-#pragma unroll
-                        for (int q = 0; q < 8; ++q) {
-                            const int r = h + q;
-                            const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
-                            off[q] = (row < rows_left && col < cols_left) ? (row * ni + col) * 4 : 0;
-                            wv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wr, off[q], 0, 0));
-                            bv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(br, off[q], 0, 0));
-                        }
-#pragma unroll
-                        for (int q = 0; q < 8; ++q) {
-                            const int r = h + q;
-                            const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
-                            if (row < rows_left && col < cols_left) {
-                                const float nb = fmaf(mu, bv[q], acc[i][j][r]);
-                                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, nb), br, off[q], 0, 0);
-                                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fmaf(-lr, nb, wv[q])), wr,
-                                                                      off[q], 0, 0);
-                            }
-                        }
-                        __builtin_amdgcn_sched_barrier(0);
-                    }
-                }
-            }
-        } else {
-#pragma unroll
-            for (int i = 0; i < T::TM; ++i) {
-#pragma unroll
-                for (int j = 0; j < T::TN; ++j) {
-                    const int col = wn + 32 * j + lcol;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
-                        if (row < rows_left && col < cols_left) {
-                            const int64_t e = (m0 + row) * N + n0 + col;
-                            const float nb = fmaf(mu, buf[e], acc[i][j][r]);
-                            buf[e] = nb;
-                            W[e] = fmaf(-lr, nb, W[e]);
-                        }
-                    }
-                }
-            }
-        }
-        return;
-    }
-    if constexpr (!HUGE_N) {
-        // Buffer-addressed epilogue: byte offsets from the tile's first
-        // element fit in 31 bits (the host picks HUGE_N otherwise).
-        const int64_t first = m0 * N + n0;
-        const int64_t avail = (M * N - first) * 4;
-        const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(
-            W + first, static_cast<short>(0), static_cast<int>(avail < 0x7fffffff ? avail : 0x7fffffff),
-            BUF_RSRC_WORD3);
-        const int ni = static_cast<int>(N);
-        const int voff = ((wm + 4 * lrow) * ni + wn + lcol) * 4;
-        const int n4 = ni * 4;
-        constexpr int NB = T::TM * T::TN;
-        constexpr int CH = NB < EPI ? NB : EPI;
-        static_assert(NB % CH == 0, "epilogue chunking");
-        // W is read in chunks of up to EPI MFMA blocks (16 values per block
-        // and lane, all loads of a chunk in flight together).  Interior tiles
-        // use one shared lane offset and uniform row offsets; with PREFETCH_W
-        // their first chunk is loaded before the last step's MFMAs so that the
-        // latency hides behind them.
-        float wv[CH][16];
-        if (PREFETCH_W && interior) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int i = c / T::TN, j = c % T::TN;
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    wv[c][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                        wr, voff + 128 * j, (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0));
-            }
-        }
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + last * SA + a_off, Bs + last * SB + b_off);
-        if (interior) {
-#pragma unroll
-            for (int c0 = 0; c0 < NB; c0 += CH) {
-                if (c0 > 0 || !PREFETCH_W) {
-#pragma unroll
-                    for (int c = 0; c < CH; ++c) {
-                        const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
-#pragma unroll
-                        for (int r = 0; r < 16; ++r)
-                            wv[c][r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                wr, voff + 128 * j, (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0));
-                    }
-                }
-#pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    const int i = (c0 + c) / T::TN, j = (c0 + c) % T::TN;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        __builtin_amdgcn_raw_buffer_store_b32(
-                            __builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], wv[c][r])), wr, voff + 128 * j,
-                            (32 * i + 8 * (r >> 2) + (r & 3)) * n4, 0);
-                }
-            }
-        } else {
-            // Ragged edge tile: every element gets its own lane offset; an
-            // element outside W loads the tile's first element instead (always
-            // inside W, value unused) and is not stored.
-            const int rows_left = static_cast<int>(M - m0 < BM ? M - m0 : BM);
-            const int cols_left = static_cast<int>(N - n0 < BN ? N - n0 : BN);
-#pragma unroll
-            for (int i = 0; i < T::TM; ++i) {
-#pragma unroll
-                for (int j = 0; j < T::TN; ++j) {
-                    const int col = wn + 32 * j + lcol;
-                    float ev[16];
-                    int off[16];
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
-                        off[r] = (row < rows_left && col < cols_left) ? (row * ni + col) * 4 : 0;
-                        ev[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(wr, off[r], 0, 0));
-                    }
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int row = wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
-                        if (row < rows_left && col < cols_left)
-                            __builtin_amdgcn_raw_buffer_store_b32(
-                                __builtin_bit_cast(unsigned, fmaf(-lr, acc[i][j][r], ev[r])), wr, off[r], 0, 0);
-                    }
-                    // One MFMA block at a time: keeps the scheduler from
-                    // hoisting every block's loads and offsets together.
-                    __builtin_amdgcn_sched_barrier(0);
-                }
-            }
-        }
+    if constexpr (!WIDE) {
+        const bool interior = (m0 + BM <= M) && (n0 + BN <= N);
+        const __amdgpu_buffer_rsrc_t wr = tile_rsrc(W, M, N, m0 * N + n0);
+        float wv[16];
+        if (!MOM && interior)
+            load_w_block(wv, wr, ((wm + 4 * lrow) * static_cast<int>(N) + wn + lcol) * 4, static_cast<int>(N) * 4, 0,
+                         W_PRE);
+        epilogue<T::TM, T::TN, MOM>(acc, wv, wr, buf, M, N, m0, n0, BM, BN, wm, wn, lrow, lcol, interior, lr, mu);
     } else {
-        // Rows so long that tile offsets need 64 bits: plain guarded accesses.
-        mma_step<BK, T::LDA, T::LDB, T::TM, T::TN>(acc, As + last * SA + a_off, Bs + last * SB + b_off);
 #pragma unroll
         for (int i = 0; i < T::TM; ++i) {
 #pragma unroll
@@ -385,8 +542,14 @@ __device__ __forceinline__ void sf_tile(
                 for (int r = 0; r < 16; ++r) {
                     const int64_t row = m0 + wm + 32 * i + 8 * (r >> 2) + 4 * lrow + (r & 3);
                     if (row < M && col < N) {
-                        float* w = W + row * N + col;
-                        *w = fmaf(-lr, acc[i][j][r], *w);
+                        const int64_t e = row * N + col;
+                        if constexpr (MOM) {
+                            const float nb = fmaf(mu, buf[e], acc[i][j][r]);
+                            buf[e] = nb;
+                            W[e] = fmaf(-lr, nb, W[e]);
+                        } else {
+                            W[e] = fmaf(-lr, acc[i][j][r], W[e]);
+                        }
                     }
                 }
             }
@@ -394,34 +557,31 @@ __device__ __forceinline__ void sf_tile(
     }
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, bool PREFETCH_W, int OCC, int EPI,
-          int GM, bool HUGE_N>
+// ---------------------------------------------------------------------------
+// Kernels.  OCC waves per SIMD: 4 for both tile shapes (128 VGPRs).
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int BK, int WM, int WN, bool MOM>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_kernel(
-    float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V,
-    int64_t M, int64_t N, int64_t K, float lr, int tiles_m, int tiles_n)
+__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_kernel(
+    float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
+    float lr, int tiles_m, int tiles_n, float* __restrict__ buf, float mu)
 {
-    using T = SfTile<BM, BN, BK, WM, WN>;
-    __shared__ float As[2 * BK * T::LDA];
-    __shared__ float Bs[2 * BK * T::LDB];
-    int tm, tn;
-    tile_coords<GM>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
-    sf_tile<BM, BN, BK, WM, WN, VEC_A, VEC_B, PREFETCH_W, EPI, HUGE_N>(As, Bs, W, U, V, M, N, K, lr, tm, tn);
-}
-
-// The layer keeps a momentum buffer (poseidon_sf_apply_momentum).
-template <int BM, int BN, int BK, int WM, int WN, bool VEC_A, bool VEC_B, int OCC, bool HUGE_N>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_mom_kernel(
-    float* __restrict__ W, float* __restrict__ buf, const float* __restrict__ U, const float* __restrict__ V,
-    int64_t M, int64_t N, int64_t K, float lr, float mu, int tiles_m, int tiles_n)
-{
-    using T = SfTile<BM, BN, BK, WM, WN>;
-    __shared__ float As[2 * BK * T::LDA];
-    __shared__ float Bs[2 * BK * T::LDB];
     int tm, tn;
     tile_coords<8>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
-    sf_tile<BM, BN, BK, WM, WN, VEC_A, VEC_B, false, 1, HUGE_N, true>(As, Bs, W, U, V, M, N, K, lr, tm, tn, buf, mu);
+    sf_tile_direct<BM, BN, BK, WM, WN, MOM>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool WIDE, bool MOM>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_staged_kernel(
+    float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
+    float lr, int tiles_m, int tiles_n, float* __restrict__ buf, float mu)
+{
+    __shared__ float As[2 * BK * (BM + LDS_PAD)];
+    __shared__ float Bs[2 * BK * (BN + LDS_PAD)];
+    int tm, tn;
+    tile_coords<8>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
+    sf_tile_staged<BM, BN, BK, WM, WN, WIDE, MOM>(As, Bs, W, U, V, M, N, K, lr, tm, tn, buf, mu);
 }
 
 // ---------------------------------------------------------------------------
@@ -441,7 +601,7 @@ struct SfBatchItem {
     int32_t first_tile;
     int32_t tiles_m;
     int32_t tiles_n;
-    int32_t vec;   // bit 0: U rows 16-byte loadable, bit 1: V rows
+    int32_t pad;
 };
 
 struct SfBatchArgs {
@@ -450,10 +610,9 @@ struct SfBatchArgs {
     int32_t total_tiles;
 };
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREFETCH_W, int OCC, int EPI>
+template <int BM, int BN, int BK, int WM, int WN>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K,
-                                                                           float lr)
+__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K, float lr)
 {
     const int tiles = args.total_tiles;
     const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
@@ -470,145 +629,82 @@ __attribute__((amdgpu_waves_per_eu(OCC, OCC))) void sf_apply_batch_kernel(const 
     const int first_m = g * G;
     const int rows = (tiles_m - first_m) < G ? (tiles_m - first_m) : G;
     const int in = local - g * per_group;
-    using T = SfTile<BM, BN, BK, WM, WN>;
-    __shared__ float As[2 * BK * T::LDA];
-    __shared__ float Bs[2 * BK * T::LDB];
     const SfBatchItem& it = args.item[l];
-    const int tm = first_m + in % rows, tn = in / rows;
-    // The operand-load variant is uniform per layer: four inlined copies.
-    switch (it.vec & 3) {
-    case 3:
-        sf_tile<BM, BN, BK, WM, WN, true, true, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K, lr,
-                                                                        tm, tn);
-        break;
-    case 2:
-        sf_tile<BM, BN, BK, WM, WN, false, true, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K, lr,
-                                                                         tm, tn);
-        break;
-    case 1:
-        sf_tile<BM, BN, BK, WM, WN, true, false, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K, lr,
-                                                                         tm, tn);
-        break;
-    default:
-        sf_tile<BM, BN, BK, WM, WN, false, false, PREFETCH_W, EPI, false>(As, Bs, it.W, it.U, it.V, it.M, it.N, K,
-                                                                          lr, tm, tn);
-        break;
-    }
+    sf_tile_direct<BM, BN, BK, WM, WN, false>(it.W, it.U, it.V, it.M, it.N, K, lr, first_m + in % rows, in / rows,
+                                              nullptr, 0.f);
 }
 
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI, int GM, bool VA, bool VB>
-void launch_kernel(int tiles, int tiles_m, int tiles_n, float* W, const float* U, const float* V,
-                   int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
+// True when the LDS-direct tile's 32-bit buffer offsets cover the layer: the
+// operand reads (K + BK rows, so the last slice's rows past K still have
+// representable offsets) and the W offsets inside one BM-row tile.
+bool direct_fits(int64_t M, int64_t N, int64_t K, int BM, int BN, int BK)
 {
-    // The buffer-addressed epilogue needs every byte offset inside a tile,
-    // ((BM-1)*N + BN) * 4, to fit in a signed 32-bit offset.
+    constexpr int64_t LIM = 0x7fffffffLL;
+    return (K + BK) * M * 4 < LIM && (K + BK) * N * 4 < LIM && (static_cast<int64_t>(BM) * N + BN) * 4 < LIM;
+}
+
+template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
+                        float lr, float mu, hipStream_t stream)
+{
     constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
-    if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
-        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, GM, false><<<tiles, NT, 0, stream>>>(
-            W, U, V, M, N, K, lr, tiles_m, tiles_n);
-    else
-        sf_apply_kernel<BM, BN, BK, WM, WN, VA, VB, PREF, OCC, EPI, GM, true><<<tiles, NT, 0, stream>>>(
-            W, U, V, M, N, K, lr, tiles_m, tiles_n);
-}
-
-template <int BM, int BN, int BK, int WM, int WN, bool PREF, int OCC, int EPI = 4, int GM = 8>
-hipError_t launch_cfg(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
-                      float lr, hipStream_t stream)
-{
     const int64_t tiles_m = (M + BM - 1) / BM;
     const int64_t tiles_n = (N + BN - 1) / BN;
-    const int64_t tiles = tiles_m * tiles_n;
-    if (tiles > INT32_MAX)
-        return hipErrorInvalidValue;
-    const bool va = (M % 4 == 0) && aligned16(U);
-    const bool vb = (N % 4 == 0) && aligned16(V);
-    const int t = static_cast<int>(tiles), tmi = static_cast<int>(tiles_m), tni = static_cast<int>(tiles_n);
-    if (va && vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, true, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
-    else if (va)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, true, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
-    else if (vb)
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, false, true>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
-    else
-        launch_kernel<BM, BN, BK, WM, WN, PREF, OCC, EPI, GM, false, false>(t, tmi, tni, W, U, V, M, N, K, lr, stream);
-    return hipGetLastError();
-}
-
-}  // namespace
-
-// Tile choice: 128 x 128 workgroup tiles (64 x 64 per wave, W prefetched,
-// 4 waves per SIMD) when the layer has at least two such tiles per CU;
-// otherwise 64 x 64 tiles so that small layers still fill the chip.
-hipError_t launch_sf_apply(float* W, const float* U, const float* V,
-                           int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
-{
-    const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
-    if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_cfg<128, 128, 16, 64, 64, true, 4, 1, 8>(W, U, V, M, N, K, lr, stream);
-    return launch_cfg<64, 64, 32, 32, 32, true, 4, 1, 8>(W, U, V, M, N, K, lr, stream);
-}
-
-namespace {
-
-template <int BM, int BN, int BK, int WM, int WN, bool VA, bool VB>
-void launch_mom(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
-                float mu, int tiles, int tiles_m, int tiles_n, hipStream_t stream)
-{
-    constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
-    if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
-        sf_apply_mom_kernel<BM, BN, BK, WM, WN, VA, VB, 4, false><<<tiles, NT, 0, stream>>>(
-            W, buf, U, V, M, N, K, lr, mu, tiles_m, tiles_n);
-    else
-        sf_apply_mom_kernel<BM, BN, BK, WM, WN, VA, VB, 4, true><<<tiles, NT, 0, stream>>>(
-            W, buf, U, V, M, N, K, lr, mu, tiles_m, tiles_n);
-}
-
-template <int BM, int BN, int BK, int WM, int WN>
-hipError_t launch_mom_cfg(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
-                          float lr, float mu, hipStream_t stream)
-{
-    const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
     if (tiles_m * tiles_n > INT32_MAX)
         return hipErrorInvalidValue;
     const int t = static_cast<int>(tiles_m * tiles_n), tmi = static_cast<int>(tiles_m),
               tni = static_cast<int>(tiles_n);
-    const bool va = (M % 4 == 0) && aligned16(U), vb = (N % 4 == 0) && aligned16(V);
-    if (va && vb)
-        launch_mom<BM, BN, BK, WM, WN, true, true>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
-    else if (va)
-        launch_mom<BM, BN, BK, WM, WN, true, false>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
-    else if (vb)
-        launch_mom<BM, BN, BK, WM, WN, false, true>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
+    if (direct_fits(M, N, K, BM, BN, BK))
+        sf_apply_kernel<BM, BN, BK, WM, WN, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni, buf, mu);
+    else if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
+        sf_apply_staged_kernel<BM, BN, BK, WM, WN, false, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
+                                                                                     buf, mu);
     else
-        launch_mom<BM, BN, BK, WM, WN, false, false>(W, buf, U, V, M, N, K, lr, mu, t, tmi, tni, stream);
+        sf_apply_staged_kernel<BM, BN, BK, WM, WN, true, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
+                                                                                    buf, mu);
     return hipGetLastError();
+}
+
+// Tile choice: 128 x 128 workgroup tiles (64 x 64 per wave, K-slices of 16)
+// when the layer has at least two such tiles per CU; otherwise 64 x 64 tiles
+// (32 x 32 per wave, K-slices of 32) so that small layers still fill the chip.
+template <bool MOM>
+hipError_t launch_sf(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
+                     float mu, hipStream_t stream)
+{
+    const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
+    if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
+        return launch_tiles<128, 128, 16, 64, 64, MOM>(W, buf, U, V, M, N, K, lr, mu, stream);
+    return launch_tiles<64, 64, 32, 32, 32, MOM>(W, buf, U, V, M, N, K, lr, mu, stream);
 }
 
 }  // namespace
 
-// The same tile choice as launch_sf_apply.
+hipError_t launch_sf_apply(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
+                           hipStream_t stream)
+{
+    return launch_sf<false>(W, nullptr, U, V, M, N, K, lr, 0.f, stream);
+}
+
 hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N,
                                     int64_t K, float lr, float mu, hipStream_t stream)
 {
-    const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
-    if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_mom_cfg<128, 128, 16, 64, 64>(W, buf, U, V, M, N, K, lr, mu, stream);
-    return launch_mom_cfg<64, 64, 32, 32, 32>(W, buf, U, V, M, N, K, lr, mu, stream);
+    return launch_sf<true>(W, buf, U, V, M, N, K, lr, mu, stream);
 }
 
-// Grouped launch: every layer whose tile offsets fit 32 bits joins one tile
-// list (128 x 128 tiles) when the group has at least two tiles per CU; the
-// others, and groups too small to fill the chip, take per-layer launches.
+// Grouped launch: every layer the LDS-direct 128 x 128 tile covers joins one
+// tile list when the group has at least two tiles per CU; the others, and
+// groups too small to fill the chip, take per-layer launches.
 hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, float lr, hipStream_t stream)
 {
-    constexpr int BM = 128, BN = 128;
+    constexpr int BM = 128, BN = 128, BK = 16;
     std::vector<int32_t> grouped;
     int64_t tiles = 0;
     for (int32_t i = 0; i < count; ++i) {
         if (t[i].M == 0 || t[i].N == 0 || K == 0)
             continue;
         const int64_t tl = ((t[i].M + BM - 1) / BM) * ((t[i].N + BN - 1) / BN);
-        if ((static_cast<int64_t>(BM) * t[i].N + BN) * 4 < 0x7fffffffLL && tiles + tl <= INT32_MAX) {
+        if (direct_fits(t[i].M, t[i].N, K, BM, BN, BK) && tiles + tl <= INT32_MAX) {
             grouped.push_back(i);
             tiles += tl;
         } else {
@@ -639,11 +735,10 @@ hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, fl
             it.tiles_m = static_cast<int32_t>((x.M + BM - 1) / BM);
             it.tiles_n = static_cast<int32_t>((x.N + BN - 1) / BN);
             it.first_tile = first;
-            it.vec = ((x.M % 4 == 0) && aligned16(x.U) ? 1 : 0) | ((x.N % 4 == 0) && aligned16(x.V) ? 2 : 0);
             first += it.tiles_m * it.tiles_n;
         }
         a.total_tiles = first;
-        sf_apply_batch_kernel<BM, BN, 16, 64, 64, true, 4, 1><<<first, 256, 0, stream>>>(a, K, lr);
+        sf_apply_batch_kernel<BM, BN, BK, 64, 64><<<first, 256, 0, stream>>>(a, K, lr);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;

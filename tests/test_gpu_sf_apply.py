@@ -168,6 +168,34 @@ def test_sf_apply_rows_too_long_for_32bit_offsets():
     assert_close(got, ref, W_TOL, "huge rows")
 
 
+@pytest.mark.parametrize("M,N,K", [((1 << 22) + 45, 7, 128), (65400, 5, 8210)])
+def test_sf_operands_beyond_32bit_offsets(M, N, K):
+    """K*M*4 >= 2^31: U's byte offsets overflow 32 bits, so both tile shapes
+    (128 x 128 for the first case, 64 x 64 for the second) take the
+    register-staged, 64-bit-addressed variant, plain and with momentum.  U is a
+    random 4096-column block repeated along M (the kernel cannot tell); points
+    are checked against the oracle."""
+    d = dev()
+    U = I.randn(4300, (K, 4096), 1.0).repeat(1, M // 4096 + 1)[:, :M].contiguous()
+    V = I.randn(4301, (K, N), 1.0)
+    W = I.randn(4302, (M, N), 0.01)
+    buf = I.randn(4303, (M, N), 0.01)
+    rows, cols = sample_points(M, N, 3000, seed=11)
+    Ud, Vd = U.to(d), V.to(d)
+    Wd, Wm, bd = W.to(d), W.to(d), buf.to(d)
+    log(f"sf_apply / sf_apply_momentum operands beyond 32-bit offsets M={M} N={N} K={K}")
+    api.sf_apply(Wd, Ud, Vd, 0.01)
+    api.sf_apply_momentum(Wm, bd, Ud, Vd, 0.01, 0.9)
+    torch.cuda.synchronize()
+    del Ud
+    Un, Vn, Wn, bn = U.numpy(), V.numpy(), W.numpy(), buf.numpy()
+    ref = oracle.sf_apply_points(Wn, Un, Vn, 0.01, rows, cols)
+    assert_close(to_np(Wd)[rows, cols], ref, W_TOL, "W")
+    w_ref, b_ref = oracle.sf_apply_momentum_points(Wn, bn, Un, Vn, 0.01, 0.9, rows, cols)
+    assert_close(to_np(bd)[rows, cols], b_ref, DELTA_TOL, "momentum buf")
+    assert_close(to_np(Wm)[rows, cols], w_ref, W_TOL, "momentum W")
+
+
 def test_sf_apply_batch_matches_oracle_and_single_calls():
     """Grouped launch over layers of different shapes (ragged, M % 4 != 0,
     unaligned V): every layer as the oracle computes it, and bit-identical to
