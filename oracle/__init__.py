@@ -23,6 +23,10 @@ Functions and the passages they follow:
   Alg. 1).
 * ``sync_iteration`` -- one node's synchronisation of every layer of a network
   for one iteration, layer by layer in backpropagation order (Sec. 3, Alg. 2).
+* ``kv_layout`` / ``KVStore`` -- the parameter server's KV store: parameters cut
+  into fixed-size KV pairs hashed equally over the servers, and one server's
+  per-pair arrival counts, applying a pair once every worker's update of it
+  has arrived (Sec. 4.1 "Coordinator", "KV Store", "Managing Consistency").
 """
 from __future__ import annotations
 
@@ -312,6 +316,91 @@ def sync_iteration(layers, B: int, P: int, lr: float, mu: float):
                               L.get("buf"))
             out[l] = {"scheme": PS, "W": w2.reshape(W.shape), "buf": b2}
     return out
+
+
+# --------------------------------------------------------------------------
+# KV store (Sec. 4.1 "Coordinator", "KV Store", "Managing Consistency")
+# --------------------------------------------------------------------------
+
+def kv_layout(sizes, pair_elems: int, P: int):
+    """The coordinator's partition of the parameter-server tensors.
+
+    Each tensor, in the order given, is cut into consecutive KV pairs of
+    ``pair_elems`` values (its last pair may be shorter; a pair never spans two
+    tensors, since every layer has a syncer of its own), and the j-th pair
+    overall is hashed to server ``j mod P``, so every server holds the same
+    number of pairs, give or take one.  Returns a list of
+    ``(tensor, offset, length, server)`` tuples in pair order."""
+    if pair_elems < 1 or P < 1:
+        raise ValueError("pair_elems and P must be positive")
+    pairs = []
+    for t, n in enumerate(sizes):
+        if n < 0:
+            raise ValueError("negative tensor size")
+        off = 0
+        while off < n:
+            length = min(pair_elems, n - off)
+            pairs.append((t, off, length, len(pairs) % P))
+            off += length
+    return pairs
+
+
+class KVStore:
+    """One server's KV store over one iteration at a time (plain Python).
+
+    ``tensors`` is a list of ``(W, buf)`` pairs of flat fp32 arrays (``buf`` may
+    be None: plain SGD, as ``ps_apply`` without a buffer); the store keeps its
+    own copies.  ``begin()`` zeroes every pair's count.  ``receive(worker,
+    tensor, grad)`` is worker ``worker``'s update of a whole tensor arriving: the
+    count of every pair of that tensor this server holds goes up by one, and
+    once it equals P the pairs are applied -- the P updates summed and applied
+    by ``ps_apply`` (canonical order, so the order in which workers arrive
+    cannot matter) -- and become ready to be sent.  Returns the number of pairs
+    completed by the call."""
+
+    def __init__(self, tensors, pair_elems: int, P: int, rank: int, lr: float, mu: float):
+        if not 0 <= rank < P:
+            raise ValueError("rank outside 0..P-1")
+        self.W = [np.array(_f32c(w).reshape(-1)) for w, _ in tensors]
+        self.buf = [None if b is None else np.array(_f32c(b).reshape(-1)) for _, b in tensors]
+        self.P, self.rank, self.lr, self.mu = P, rank, lr, mu
+        self.pairs = kv_layout([w.size for w in self.W], pair_elems, P)
+        self.owned = [[j for j, pr in enumerate(self.pairs) if pr[0] == t and pr[3] == rank]
+                      for t in range(len(self.W))]
+        self.begin()
+
+    def begin(self):
+        self.count = [0] * len(self.pairs)
+        self.updates = [dict() for _ in self.W]
+
+    def ready(self, pair: int) -> bool:
+        """The pair may be sent: every worker's update of it has been applied."""
+        return self.count[pair] == self.P
+
+    def receive(self, worker: int, tensor: int, grad) -> int:
+        if not 0 <= worker < self.P or not 0 <= tensor < len(self.W):
+            raise ValueError("worker or tensor out of range")
+        if worker in self.updates[tensor]:
+            raise ValueError("this worker's update of the tensor has already arrived")
+        grad = _f32c(grad).reshape(-1)
+        if grad.size != self.W[tensor].size:
+            raise ValueError("update has the wrong size")
+        self.updates[tensor][worker] = grad
+        done = 0
+        for j in self.owned[tensor]:
+            self.count[j] += 1
+            if self.count[j] == self.P:
+                _, off, length, _ = self.pairs[j]
+                sl = slice(off, off + length)
+                shards = np.stack([self.updates[tensor][p][sl] for p in range(self.P)])
+                buf = self.buf[tensor]
+                w2, b2 = ps_apply(self.W[tensor][sl], shards, self.lr, self.mu if buf is not None else 0.0,
+                                  None if buf is None else buf[sl])
+                self.W[tensor][sl] = w2
+                if buf is not None:
+                    buf[sl] = b2
+                done += 1
+        return done
 
 
 def num_threads() -> int:
