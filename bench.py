@@ -398,6 +398,56 @@ def main():
         "layers_sfb": layers,
         "layers_sfb_momentum": layers_mom,
     }
+    # One node's server role through the KV store: the PS tensors cut into
+    # 2 MB pairs hashed over the P servers; server 0 receives all P workers'
+    # updates of every tensor (worker p's update = shard p) and applies its
+    # pairs as they complete.
+    pair_elems = (2 << 20) // 4
+    kv_t = [devt[i] for i in ps_idx]
+    store = api.KVStore([(t["W"].view(-1), t.get("buf")) for t in kv_t], pair_elems, wl.P, 0, wl.lr, wl.momentum)
+    owned = [(t, l) for (t, _, l, s_) in store.pairs if s_ == 0]
+    kv_elems = sum(l for _, l in owned)
+    kv_bytes = float(kv_elems) * (4 * wl.P + 16)
+    kv_rows = [t["shards"].view(wl.P, -1) for t in kv_t]
+
+    def kv_iter():
+        store.begin()
+        for p in range(wl.P):
+            for t in range(len(kv_t)):
+                store.receive(p, t, kv_rows[t][p], stream=stream)
+
+    kv_ms = _time(kv_iter)
+    # The apply launches alone: the last worker's receives (which enqueue every
+    # apply) are issued while the stream is held by a ~1 ms device-side wait,
+    # so the events around them time the launches back to back, not the host.
+    kv_apply = []
+    for _ in range(ksteps):
+        store.begin()
+        for p in range(wl.P - 1):
+            for t in range(len(kv_t)):
+                store.receive(p, t, kv_rows[t][p], stream=stream)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(2_000_000)
+        a.record(stream)
+        for t in range(len(kv_t)):
+            store.receive(wl.P - 1, t, kv_rows[t][wl.P - 1], stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        kv_apply.append(a.elapsed_time(b))
+    kv_apply_ms = sum(kv_apply) / len(kv_apply)
+    store.close()
+    result["kv_server_share"] = {
+        "what": f"server 0 of {wl.P}: its {len(owned)} of {len(store.pairs)} KV pairs (2 MB) of the {len(kv_t)} PS "
+                f"tensors, {kv_elems} elements, {(4 * wl.P + 16)} bytes each",
+        "bytes": kv_bytes,
+        "iteration_ms": round(kv_ms, 4),
+        "apply_ms": round(kv_apply_ms, 4),
+        "apply_gbs": round(kv_bytes / kv_apply_ms / 1e6, 1),
+        "note": "iteration_ms: begin plus all P x tensors receives on one stream, paced by the host's calls; "
+                "apply_ms: HIP events around the last worker's receives, which enqueue every apply, queued "
+                "behind a device-side wait so that the applies run back to back"}
+    print(f"[bench] KV server share: {result['kv_server_share']}", file=sys.stderr, flush=True)
     if args.wfbp == "on" and wl.config == 5:
         print("[bench] WFBP phase (synthetic backward)", file=sys.stderr, flush=True)
         result["wfbp"] = _wfbp_phase(wl, devt, it, pool, d, args.wfbp_steps)

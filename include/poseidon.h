@@ -164,6 +164,108 @@ int poseidon_ps_apply_batch(const poseidon_ps_tensor* tensors, int32_t count, in
                             float lr, float momentum, hipStream_t stream);
 
 /*
+ * KV store (Sec. 4.1 "Coordinator", "KV Store", "Managing Consistency").
+ *
+ * The parameter-server tensors are cut into KV pairs of a fixed small size
+ * (2 MB in the paper) that the coordinator hashes equally over the P server
+ * nodes, so that every server carries the same share of the traffic instead
+ * of one server per tensor (Sec. 5.2).  Each server's KV store counts, per
+ * pair and per iteration, the workers' updates that have arrived, and applies
+ * a pair -- the sum of the P updates, then the momentum SGD step of
+ * poseidon_ps_apply -- once its count equals the number of workers, after
+ * which the pair is ready to be sent back.  On one GPU a store is one node's
+ * server role: it updates only the pairs hashed to its rank, in place in the
+ * caller's full parameter tensors.
+ */
+
+/* One KV pair. */
+typedef struct poseidon_kv_pair {
+    int32_t tensor;   /* index into the tensor list */
+    int32_t server;   /* rank of the KV store that holds the pair */
+    int64_t offset;   /* first element of the pair in its tensor */
+    int64_t length;   /* elements: pair_elems, or fewer for a tensor's last pair */
+} poseidon_kv_pair;
+
+/*
+ * The coordinator's partition of `count` tensors of sizes[t] elements: each
+ * tensor, in order, is cut into consecutive pairs of pair_elems elements (the
+ * last pair of a tensor may be shorter; a pair never spans two tensors, as
+ * every layer has a syncer of its own), and the j-th pair overall goes to
+ * server j mod P (pair counts per server differ by at most one; the pieces of
+ * a big tensor land on consecutive servers).  Writes the pairs in order to
+ * pairs[0 .. *npairs) when capacity suffices (pairs may be NULL with capacity
+ * 0 to query *npairs).  Host-only.  Returns POSEIDON_OK or
+ * POSEIDON_ERR_INVALID_ARG (count < 0, a negative size, pair_elems < 1,
+ * P < 1, NULL sizes or npairs, more than 2^31 - 1 pairs, capacity too small
+ * -- *npairs is still set).
+ */
+int poseidon_kv_layout(const int64_t* sizes, int32_t count, int64_t pair_elems, int32_t P,
+                       poseidon_kv_pair* pairs, int32_t capacity, int32_t* npairs);
+
+/* One parameter-server tensor of a KV store: W (n values) and its momentum
+ * buffer (n values, or NULL for plain SGD), caller-owned device memory that
+ * must stay valid for the store's lifetime. */
+typedef struct poseidon_kv_tensor {
+    float*  W;
+    float*  buf;
+    int64_t n;
+} poseidon_kv_tensor;
+
+typedef struct poseidon_kv_store poseidon_kv_store;
+
+/*
+ * Create the KV store of server `rank` (0 .. P-1) over the given tensors,
+ * laid out as by poseidon_kv_layout(sizes, count, pair_elems, P), with the
+ * step's lr and momentum (used only for tensors that have a buf).  The store
+ * keeps the tensor list, the layout, one count per pair and one update
+ * pointer per (tensor, worker); it allocates no device memory.  All counts
+ * start at 0 (as after poseidon_kv_begin).  P <= 64.  Returns POSEIDON_OK,
+ * POSEIDON_ERR_INVALID_ARG (bad sizes, NULL W or buf/W overlap with n > 0,
+ * rank outside 0..P-1, P outside 1..64, count < 0, NULL out) or
+ * POSEIDON_ERR_HIP.
+ */
+int poseidon_kv_create(const poseidon_kv_tensor* tensors, int32_t count, int64_t pair_elems, int32_t P,
+                       int32_t rank, float lr, float momentum, poseidon_kv_store** out);
+
+/* Destroy a store (no device work is pending on its behalf once the streams
+ * its receives used have drained).  NULL is a no-op. */
+int poseidon_kv_destroy(poseidon_kv_store* store);
+
+/* Start of an iteration: every pair's count back to 0, every recorded update
+ * forgotten.  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG. */
+int poseidon_kv_begin(poseidon_kv_store* store);
+
+/*
+ * Worker `worker`'s update of tensor `tensor` has arrived: grad holds the
+ * tensor's n gradient values (device memory, caller-owned, not modified; only
+ * the slices of this store's pairs are read).  The count of every pair of the
+ * tensor that this store holds goes up by one.  When those counts reach P,
+ * the pairs are applied on `stream`: for every element i of them
+ *
+ *     s_i = sum_{p<P} grad_p[i]  (p in increasing worker order, whatever the
+ *                                 order of arrival; fp32)
+ *     buf_i <- momentum * buf_i + s_i ;  W_i <- W_i - lr * buf_i
+ *
+ * (without buf: W_i <- W_i - lr * s_i), the arithmetic of poseidon_ps_apply.
+ * The P update pointers of the tensor must stay valid, and their data
+ * complete in the order of `stream`, until that work has run.  Returns the
+ * number of pairs this call completed (their counts reached P), or
+ * POSEIDON_ERR_INVALID_ARG (NULL store; worker or tensor out of range; NULL
+ * grad with n > 0; grad overlapping W or buf; this worker's update of the
+ * tensor already received in this iteration -- nothing changes then) or
+ * POSEIDON_ERR_HIP.
+ */
+int poseidon_kv_receive(poseidon_kv_store* store, int32_t worker, int32_t tensor, const float* grad,
+                        hipStream_t stream);
+
+/* The store's count of pair `pair` (an index into its layout) in the current
+ * iteration: the number of workers whose update of it has arrived, or 0 for
+ * a pair held by another server.  A pair whose count equals P has been
+ * applied (enqueued) and may be sent.  Returns POSEIDON_OK or
+ * POSEIDON_ERR_INVALID_ARG. */
+int poseidon_kv_pair_count(const poseidon_kv_store* store, int32_t pair, int32_t* count);
+
+/*
  * Coordinator.BestScheme for a fully-connected M x N layer (Alg. 1; Table 1)
  * on a cluster of P nodes that are each both worker and server (P1 = P2 = P),
  * per-worker batch B:

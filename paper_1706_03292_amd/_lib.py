@@ -26,7 +26,9 @@ EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply
            "poseidon_hybcomm_choose3", "poseidon_pool_create",
            "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_sync_iteration_wfbp",
            "poseidon_pool_set_timing",
-           "poseidon_pool_launch_times", "poseidon_abi_version")
+           "poseidon_pool_launch_times", "poseidon_abi_version",
+           "poseidon_kv_layout", "poseidon_kv_create", "poseidon_kv_destroy", "poseidon_kv_begin",
+           "poseidon_kv_receive", "poseidon_kv_pair_count")
 
 
 class PoseidonTensor(ctypes.Structure):
@@ -53,6 +55,17 @@ class PoseidonLaunchRecord(ctypes.Structure):
     """Mirror of ``poseidon_launch_record`` in include/poseidon.h."""
     _fields_ = [("scheme", ctypes.c_int32), ("tensor", ctypes.c_int32), ("stream", ctypes.c_int32),
                 ("ms", ctypes.c_float)]
+
+
+class PoseidonKvPair(ctypes.Structure):
+    """Mirror of ``poseidon_kv_pair`` in include/poseidon.h."""
+    _fields_ = [("tensor", ctypes.c_int32), ("server", ctypes.c_int32), ("offset", ctypes.c_int64),
+                ("length", ctypes.c_int64)]
+
+
+class PoseidonKvTensor(ctypes.Structure):
+    """Mirror of ``poseidon_kv_tensor`` in include/poseidon.h."""
+    _fields_ = [("W", ctypes.c_void_p), ("buf", ctypes.c_void_p), ("n", ctypes.c_int64)]
 
 
 _lib = None
@@ -86,6 +99,14 @@ def lib() -> ctypes.CDLL:
     L.poseidon_pool_launch_times.argtypes = [vp, ctypes.POINTER(PoseidonLaunchRecord), i32,
                                              ctypes.POINTER(i32)]
     L.poseidon_abi_version.argtypes = []
+    L.poseidon_kv_layout.argtypes = [ctypes.POINTER(i64), i32, i64, i32, ctypes.POINTER(PoseidonKvPair), i32,
+                                     ctypes.POINTER(i32)]
+    L.poseidon_kv_create.argtypes = [ctypes.POINTER(PoseidonKvTensor), i32, i64, i32, i32, f32, f32,
+                                     ctypes.POINTER(vp)]
+    L.poseidon_kv_destroy.argtypes = [vp]
+    L.poseidon_kv_begin.argtypes = [vp]
+    L.poseidon_kv_receive.argtypes = [vp, i32, i32, vp, vp]
+    L.poseidon_kv_pair_count.argtypes = [vp, i32, ctypes.POINTER(i32)]
     for name in EXPORTS:
         getattr(L, name).restype = ctypes.c_int
     if L.poseidon_abi_version() != ABI_VERSION:

@@ -315,3 +315,92 @@ class SyncIteration:
                     self.pool.handle, self._arr, self.count, self.B, self.P, self.lr, self.momentum,
                     evs, h, self._schemes))
         return list(self._schemes[:self.count])
+
+
+# --------------------------------------------------------------------------
+# KV store (one server's share of the parameter server)
+# --------------------------------------------------------------------------
+
+def kv_layout(sizes, pair_elems: int, P: int) -> list[tuple[int, int, int, int]]:
+    """The coordinator's partition (poseidon_kv_layout): a list of
+    ``(tensor, offset, length, server)`` tuples in pair order.  Host-only."""
+    sizes = [int(x) for x in sizes]
+    arr = (ctypes.c_int64 * max(1, len(sizes)))(*sizes)
+    n = ctypes.c_int32()
+    _check("poseidon_kv_layout", L.lib().poseidon_kv_layout(arr, len(sizes), int(pair_elems), int(P), None, 0,
+                                                            ctypes.byref(n)))
+    out = (L.PoseidonKvPair * max(1, n.value))()
+    _check("poseidon_kv_layout", L.lib().poseidon_kv_layout(arr, len(sizes), int(pair_elems), int(P), out,
+                                                            n.value, ctypes.byref(n)))
+    return [(q.tensor, q.offset, q.length, q.server) for q in out[:n.value]]
+
+
+class KVStore:
+    """Server ``rank``'s KV store over flat parameter tensors.
+
+    ``tensors`` is a list of ``(W, buf)`` device tensors (``buf`` may be None
+    for plain SGD); the store updates the pairs hashed to ``rank`` in place.
+    ``begin()`` starts an iteration; ``receive(worker, tensor, grad)`` records
+    worker ``worker``'s update of a tensor (a device tensor of the same size,
+    which must stay alive until the work it triggers has run) and returns the
+    number of this store's pairs it completed -- their apply is then enqueued
+    on ``stream``."""
+
+    def __init__(self, tensors: list, pair_elems: int, P: int, rank: int, lr: float, momentum: float = 0.0):
+        self._keep = []
+        arr = (L.PoseidonKvTensor * max(1, len(tensors)))()
+        dev = None
+        for i, (W, buf) in enumerate(tensors):
+            _dev_f32("W", W)
+            if buf is not None:
+                _dev_f32("buf", buf)
+                if buf.numel() != W.numel():
+                    raise ValueError("buf must have as many values as W")
+            _same_device(W, buf)
+            if dev is not None and W.device != dev:
+                raise ValueError("all tensors must be on one device")
+            dev = W.device
+            arr[i] = L.PoseidonKvTensor(W.data_ptr(), _ptr(buf), W.numel())
+            self._keep.append((W, buf))
+        self.device = dev if dev is not None else torch.device("cuda", torch.cuda.current_device())
+        self.sizes = [W.numel() for W, _ in tensors]
+        self.P, self.rank = int(P), int(rank)
+        self._h = ctypes.c_void_p()
+        self._grads = {}
+        with torch.cuda.device(self.device):
+            _check("poseidon_kv_create", L.lib().poseidon_kv_create(arr, len(tensors), int(pair_elems), self.P,
+                                                                    self.rank, float(lr), float(momentum),
+                                                                    ctypes.byref(self._h)))
+        self.pairs = kv_layout(self.sizes, pair_elems, P)
+
+    def begin(self) -> None:
+        _check("poseidon_kv_begin", L.lib().poseidon_kv_begin(self._h))
+        self._grads = {}
+
+    def receive(self, worker: int, tensor: int, grad: torch.Tensor, stream=None) -> int:
+        _dev_f32("grad", grad)
+        if not 0 <= tensor < len(self.sizes) or grad.numel() != self.sizes[tensor]:
+            raise ValueError("grad must have the tensor's size")
+        if grad.device != self.device:
+            raise ValueError("grad must be on the store's device")
+        with torch.cuda.device(self.device):
+            done = _check("poseidon_kv_receive", L.lib().poseidon_kv_receive(
+                self._h, int(worker), int(tensor), grad.data_ptr(), _stream_handle(stream, self.device)))
+        self._grads[(worker, tensor)] = grad
+        return done
+
+    def count(self, pair: int) -> int:
+        c = ctypes.c_int32()
+        _check("poseidon_kv_pair_count", L.lib().poseidon_kv_pair_count(self._h, int(pair), ctypes.byref(c)))
+        return c.value
+
+    def close(self):
+        if self._h:
+            L.lib().poseidon_kv_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

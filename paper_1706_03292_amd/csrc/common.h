@@ -59,6 +59,14 @@ constexpr int PS_BATCH_MAX = 48;   // descriptors per batched launch (kernel-arg
 hipError_t launch_ps_apply_batch(const PsTensor* tensors, int32_t count, int32_t P, float lr,
                                  float momentum, hipStream_t stream);
 
+// KV-store apply of one tensor's pairs held by one server (arguments
+// validated; P <= KV_MAX_P; every range inside the tensor; grads[p] is worker
+// p's whole-tensor update).  Ranges beyond KV_MAX_RANGES take further launches.
+constexpr int KV_MAX_P = 64;
+constexpr int KV_MAX_RANGES = 32;
+hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int32_t P, const int64_t* offsets,
+                           const int64_t* lengths, int32_t nranges, float lr, float momentum, hipStream_t stream);
+
 // Argument checks of the public entry points (no device work).
 int check_sf_args(const float* W, const float* U, const float* V,
                   int64_t M, int64_t N, int64_t K);

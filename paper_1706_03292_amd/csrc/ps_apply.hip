@@ -277,6 +277,124 @@ void launch_batch_mom(const PsBatchArgs& a, int blocks, int grid, int32_t P, flo
     }
 }
 
+// ---------------------------------------------------------------------------
+// KV-store apply: the pairs of one tensor that one server holds, with the P
+// workers' updates at separate addresses (one pointer per worker, passed in
+// worker order).  Range r covers tensor elements [offset, offset + length)
+// and owns the workgroups [first_block[r], first_block[r+1]); each workgroup
+// updates PS_BLOCK_ELEMS consecutive elements of its range, one group of four
+// per thread (16-byte accesses when the whole launch allows them).
+// ---------------------------------------------------------------------------
+
+struct KvRange {
+    int64_t offset;
+    int64_t length;
+    int32_t first_block;
+    int32_t pad;
+};
+
+struct KvArgs {
+    const float* g[KV_MAX_P];
+    KvRange r[KV_MAX_RANGES];
+    int32_t nranges;
+};
+
+// Sum of the P updates of the four elements at e, in increasing worker order.
+template <int PT>
+__device__ inline f4 kv_sum4(const KvArgs& a, int P, int64_t e)
+{
+    if constexpr (PT > 0) {
+        f4 g[PT];
+#pragma unroll
+        for (int p = 0; p < PT; ++p)
+            g[p] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[p] + e));
+        f4 s = g[0];
+#pragma unroll
+        for (int p = 1; p < PT; ++p)
+            s += g[p];
+        return s;
+    } else {
+        f4 s = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[0] + e));
+        int p = 1;
+        for (; p + PS_CHUNK <= P; p += PS_CHUNK) {
+            f4 g[PS_CHUNK];
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                g[c] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[p + c] + e));
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                s += g[c];
+        }
+        for (; p < P; ++p)
+            s += __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[p] + e));
+        return s;
+    }
+}
+
+template <int PT>
+__device__ inline float kv_sum1(const KvArgs& a, int P, int64_t e)
+{
+    float s = a.g[0][e];
+    for (int p = 1; p < (PT > 0 ? PT : P); ++p)
+        s += a.g[p][e];
+    return s;
+}
+
+template <int PT, bool MOM>
+__global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, int P, float* __restrict__ W,
+                                                               float* __restrict__ buf, float lr, float mu, int vec)
+{
+    const int b = blockIdx.x;
+    int r = 0;
+    while (r + 1 < a.nranges && a.r[r + 1].first_block <= b)
+        ++r;
+    const int64_t len = a.r[r].length;
+    const int64_t j = static_cast<int64_t>(b - a.r[r].first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
+    if (j >= len)
+        return;
+    const int64_t e = a.r[r].offset + j;
+    if (vec && j + 3 < len) {
+        const f4 s = kv_sum4<PT>(a, P, e);
+        f4* W4 = reinterpret_cast<f4*>(W + e);
+        f4 w = *W4;
+        if constexpr (MOM) {
+            f4* B4 = reinterpret_cast<f4*>(buf + e);
+            const f4 bv = fma4(mu, *B4, s);
+            *B4 = bv;
+            w = fma4(-lr, bv, w);
+        } else {
+            w = fma4(-lr, s, w);
+        }
+        *W4 = w;
+    } else {
+        for (int q = 0; q < 4 && j + q < len; ++q) {
+            const float s = kv_sum1<PT>(a, P, e + q);
+            float w = W[e + q];
+            if constexpr (MOM) {
+                const float bv = fmaf(mu, buf[e + q], s);
+                buf[e + q] = bv;
+                w = fmaf(-lr, bv, w);
+            } else {
+                w = fmaf(-lr, s, w);
+            }
+            W[e + q] = w;
+        }
+    }
+}
+
+template <bool MOM>
+void launch_kv_mom(const KvArgs& a, int grid, int32_t P, float* W, float* buf, float lr, float mu, int vec,
+                   hipStream_t stream)
+{
+    switch (P) {
+    case 4:  kv_apply_kernel<4, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
+    case 8:  kv_apply_kernel<8, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
+    case 16: kv_apply_kernel<16, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
+    case 32: kv_apply_kernel<32, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
+    default: kv_apply_kernel<0, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
+    }
+}
+
 }  // namespace
 
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
@@ -331,6 +449,41 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
             blocks += nb;
         }
         const hipError_t e = flush();
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int32_t P, const int64_t* offsets,
+                           const int64_t* lengths, int32_t nranges, float lr, float momentum, hipStream_t stream)
+{
+    bool vec = aligned16(W) && (!buf || aligned16(buf));
+    for (int32_t p = 0; p < P; ++p)
+        vec = vec && aligned16(grads[p]);
+    for (int32_t i = 0; i < nranges; ++i)
+        vec = vec && offsets[i] % 4 == 0;
+    for (int32_t i0 = 0; i0 < nranges; i0 += KV_MAX_RANGES) {
+        KvArgs a{};
+        for (int32_t p = 0; p < P; ++p)
+            a.g[p] = grads[p];
+        int64_t blocks = 0;
+        for (int32_t i = i0; i < nranges && i < i0 + KV_MAX_RANGES; ++i) {
+            KvRange& r = a.r[a.nranges++];
+            r.offset = offsets[i];
+            r.length = lengths[i];
+            r.first_block = static_cast<int32_t>(blocks);
+            blocks += (lengths[i] + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
+            if (blocks > INT32_MAX)
+                return hipErrorInvalidValue;
+        }
+        if (blocks == 0)
+            continue;
+        if (buf)
+            launch_kv_mom<true>(a, static_cast<int>(blocks), P, W, buf, lr, momentum, vec ? 1 : 0, stream);
+        else
+            launch_kv_mom<false>(a, static_cast<int>(blocks), P, W, nullptr, lr, 0.0f, vec ? 1 : 0, stream);
+        const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
     }

@@ -39,6 +39,9 @@ def test_struct_layout_matches_header():
     assert ctypes.sizeof(L.PoseidonPsTensor) == 32 and L.PoseidonPsTensor.n.offset == 24
     assert ctypes.sizeof(L.PoseidonSfTensor) == 40 and L.PoseidonSfTensor.N.offset == 32
     assert ctypes.sizeof(L.PoseidonLaunchRecord) == 16 and L.PoseidonLaunchRecord.ms.offset == 12
+    # int32 tensor, int32 server, int64 offset, int64 length; W, buf, int64 n
+    assert ctypes.sizeof(L.PoseidonKvPair) == 24 and L.PoseidonKvPair.offset.offset == 8
+    assert ctypes.sizeof(L.PoseidonKvTensor) == 24 and L.PoseidonKvTensor.n.offset == 16
 
 
 def test_invalid_arguments_rejected_before_device_work():
