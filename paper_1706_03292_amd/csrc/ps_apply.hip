@@ -6,9 +6,11 @@
 //
 // The kernel is bound by HBM bandwidth: per element it reads P shard values
 // plus W and buf and writes W and buf (4P + 16 bytes), against ~P + 3 flops.
-// Each thread owns one 16-byte group of four consecutive elements, issues all
-// of its shard loads before the dependent adds (bytes in flight) and streams
-// the single-use shards with non-temporal loads.  One-wave workgroups, one
+// Each thread owns one 16-byte group of four consecutive elements and issues
+// all of its shard loads before the dependent adds (bytes in flight).  Every
+// array is touched once per launch (shards read; W and buf read, then
+// written), so all accesses are non-temporal (1-2% faster than cached W/buf
+// accesses on 2.4M-16.8M elements).  One-wave workgroups, one
 // group per thread, as many workgroups as groups: a launch-shape sweep over
 // 37K-16.8M elements (block size 64-1024, one or two groups per thread,
 // grid-stride loops capped at 4-16 workgroups per CU) found this within 3% of
@@ -104,15 +106,15 @@ __global__ __launch_bounds__(PS_THREADS_1) void ps_apply_vec4(
     const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS_1;
     for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS_1 + threadIdx.x; i < n4; i += stride) {
         const f4 s = shard_sum4<PT>(G4, P, n4, i);
-        f4 w = W4[i];
+        f4 w = __builtin_nontemporal_load(W4 + i);
         if constexpr (MOM) {
-            const f4 b = fma4(mu, B4[i], s);
-            B4[i] = b;
+            const f4 b = fma4(mu, __builtin_nontemporal_load(B4 + i), s);
+            __builtin_nontemporal_store(b, B4 + i);
             w = fma4(-lr, b, w);
         } else {
             w = fma4(-lr, s, w);
         }
-        W4[i] = w;
+        __builtin_nontemporal_store(w, W4 + i);
     }
 }
 
@@ -224,15 +226,15 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_batch_kernel(const PsBatc
                 const int64_t i = (base >> 2) + u * PS_THREADS + threadIdx.x;
                 if (i < n4) {
                     const f4 s = shard_sum4<PT>(G4, P, n4, i);
-                    f4 w = W4[i];
+                    f4 w = __builtin_nontemporal_load(W4 + i);
                     if constexpr (MOM) {
-                        const f4 bv = fma4(mu, B4[i], s);
-                        B4[i] = bv;
+                        const f4 bv = fma4(mu, __builtin_nontemporal_load(B4 + i), s);
+                        __builtin_nontemporal_store(bv, B4 + i);
                         w = fma4(-lr, bv, w);
                     } else {
                         w = fma4(-lr, s, w);
                     }
-                    W4[i] = w;
+                    __builtin_nontemporal_store(w, W4 + i);
                 }
             }
         } else {
@@ -356,16 +358,16 @@ __global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, in
     if (vec && j + 3 < len) {
         const f4 s = kv_sum4<PT>(a, P, e);
         f4* W4 = reinterpret_cast<f4*>(W + e);
-        f4 w = *W4;
+        f4 w = __builtin_nontemporal_load(W4);
         if constexpr (MOM) {
             f4* B4 = reinterpret_cast<f4*>(buf + e);
-            const f4 bv = fma4(mu, *B4, s);
-            *B4 = bv;
+            const f4 bv = fma4(mu, __builtin_nontemporal_load(B4), s);
+            __builtin_nontemporal_store(bv, B4);
             w = fma4(-lr, bv, w);
         } else {
             w = fma4(-lr, s, w);
         }
-        *W4 = w;
+        __builtin_nontemporal_store(w, W4);
     } else {
         for (int q = 0; q < 4 && j + q < len; ++q) {
             const float s = kv_sum1<PT>(a, P, e + q);
