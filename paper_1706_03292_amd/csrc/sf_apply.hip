@@ -169,8 +169,9 @@ __device__ __forceinline__ void epi_edge(const f16v (&acc)[TM][TN], __amdgpu_buf
     }
 }
 
-// Momentum: buf <- mu*buf + dW, W <- W - lr*buf, half an MFMA block (8 values
-// per lane) at a time, W and buf loads in flight together, then both stores.
+// Momentum on an edge tile: buf <- mu*buf + dW, W <- W - lr*buf, half an MFMA
+// block (8 values per lane) at a time, W and buf loads in flight together,
+// then both stores; elements outside W as in epi_edge.
 template <int TM, int TN>
 __device__ __forceinline__ void epi_momentum(const f16v (&acc)[TM][TN], __amdgpu_buffer_rsrc_t wr,
                                              __amdgpu_buffer_rsrc_t br, int ni, int wm, int wn, int lrow, int lcol,
@@ -210,6 +211,37 @@ __device__ __forceinline__ void epi_momentum(const f16v (&acc)[TM][TN], __amdgpu
     }
 }
 
+// Momentum on an interior tile: one shared lane offset and uniform row offsets
+// for both W and buf, half an MFMA block at a time.
+template <int TM, int TN>
+__device__ __forceinline__ void epi_momentum_interior(const f16v (&acc)[TM][TN], __amdgpu_buffer_rsrc_t wr,
+                                                      __amdgpu_buffer_rsrc_t br, int voff, int n4, float lr, float mu)
+{
+#pragma unroll
+    for (int c = 0; c < TM * TN; ++c) {
+        const int i = c / TN, j = c % TN;
+#pragma unroll
+        for (int h = 0; h < 16; h += 8) {
+            float wv[8], bv[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                wv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    wr, voff + 128 * j, acc_row(i, h + q) * n4, 0));
+                bv[q] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                    br, voff + 128 * j, acc_row(i, h + q) * n4, 0));
+            }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const float nb = fmaf(mu, bv[q], acc[i][j][h + q]);
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, nb), br, voff + 128 * j,
+                                                      acc_row(i, h + q) * n4, 0);
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, fmaf(-lr, nb, wv[q])), wr,
+                                                      voff + 128 * j, acc_row(i, h + q) * n4, 0);
+            }
+        }
+    }
+}
+
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(float* base, int64_t M, int64_t N, int64_t first)
 {
     const int64_t avail = (M * N - first) * 4;
@@ -231,7 +263,10 @@ __device__ __forceinline__ void epilogue(const f16v (&acc)[TM][TN], float (&wv)[
     const int cols_left = static_cast<int>(N - n0 < BN ? N - n0 : BN);
     if constexpr (MOM) {
         const __amdgpu_buffer_rsrc_t br = tile_rsrc(buf, M, N, m0 * N + n0);
-        epi_momentum<TM, TN>(acc, wr, br, ni, wm, wn, lrow, lcol, rows_left, cols_left, lr, mu);
+        if (interior)
+            epi_momentum_interior<TM, TN>(acc, wr, br, ((wm + 4 * lrow) * ni + wn + lcol) * 4, ni * 4, lr, mu);
+        else
+            epi_momentum<TM, TN>(acc, wr, br, ni, wm, wn, lrow, lcol, rows_left, cols_left, lr, mu);
     } else if (interior) {
         epi_interior<TM, TN>(acc, wv, wr, ((wm + 4 * lrow) * ni + wn + lcol) * 4, ni * 4, lr);
     } else {
