@@ -202,6 +202,159 @@ def _cpu_baseline(wl, host, fraction):
     }
 
 
+def _sf_phase(wl, host, devt, schemes, launch_ms, time_fn, stream):
+    """The SF-reconstruction kernel: per-layer durations inside the iteration
+    (launch records) and alone, with and without a momentum buffer; None when
+    no layer takes SFB."""
+    from paper_1706_03292_amd import api
+    import torch
+    idx = [i for i, s_ in enumerate(schemes) if s_ == api.SFB][::-1]      # backprop order
+    if not idx:
+        return None
+    layers, layers_mom = [], []
+    flops = in_ms = 0.0
+    for i in idx:
+        spec, t = host[i]["spec"], devt[i]
+        W, U, V = t["W"], t["U"], t["V"]
+        f = _sf_flops(spec, wl.K)
+        ms = time_fn(lambda: api.sf_apply(W, U, V, wl.lr, stream=stream))
+        it_ms = launch_ms.get(i, 0.0)
+        flops += f
+        in_ms += it_ms
+        layers.append({"tensor": spec.name, "scheme": "SFB",
+                       "ms": round(it_ms, 4), "tflops": round(f / it_ms / 1e9, 2) if it_ms else None,
+                       "alone_ms": round(ms, 4), "alone_tflops": round(f / ms / 1e9, 2)})
+        # the same layer with a momentum buffer: W and buf each read and written once
+        mbuf = torch.zeros_like(W)
+        ms = time_fn(lambda: api.sf_apply_momentum(W, mbuf, U, V, wl.lr, wl.momentum, stream=stream))
+        M, N = spec.shape
+        layers_mom.append({"tensor": spec.name, "alone_ms": round(ms, 4), "tflops": round(f / ms / 1e9, 2),
+                           "gbs": round(4.0 * (4 * M * N + wl.K * (M + N)) / ms / 1e6, 1)})
+        del mbuf
+    tflops = flops / in_ms / 1e9 if in_ms else None
+    return {
+        "in_iteration_ms": in_ms,
+        "layers": layers,
+        "layers_momentum": layers_mom,
+        "roofline": {"bound": "mfma", "kernel": "sf_apply (fp32 MFMA; one launch per FC layer)",
+                     "achieved": round(tflops, 2) if tflops else None,
+                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tflops / PEAK_FP32_MFMA_TFLOPS, 4) if tflops else None,
+                     "traffic": _stored_traffic("sf_apply", "sf_apply.hip") if wl.config == 5 else None,
+                     "work": f"2*M*N*K flops of the {len(idx)} SFB layers of one step ({flops / 1e9:.1f} GFLOP) / "
+                             f"the summed average durations of their launches inside the iteration "
+                             f"({in_ms:.4f} ms)"},
+    }
+
+
+def _ps_phase(wl, devt, schemes, launch_ms, time_fn, stream, pool, ksteps):
+    """The PS kernel, measured in a phase of its own (inside the iteration the
+    PS applies share the GPU with the SF reconstructions by design): the
+    library issues the step's PS launches one after another on one pool
+    stream with nothing else running, and its timing events bracket each
+    launch on that stream; the batched pass is timed too.  None when no tensor
+    takes PS."""
+    from paper_1706_03292_amd import api
+    import torch
+    ps_idx = [i for i, s_ in enumerate(schemes) if s_ == api.PS]
+    if not ps_idx:
+        return None
+    ps_list = [(devt[i]["W"], devt[i]["shards"], devt[i].get("buf")) for i in reversed(ps_idx)]
+    ps_it = api.SyncIteration(pool, [devt[i] for i in ps_idx], wl.B, wl.P, wl.lr, wl.momentum)
+    seq_ms = time_fn(lambda: ps_it(stream))
+    pool.set_timing(True)
+    per = {}
+    for _ in range(ksteps):
+        ps_it(stream)
+        for r in pool.launch_times():
+            per[r["tensor"]] = per.get(r["tensor"], 0.0) + r["ms"] / ksteps
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    batch_ms = time_fn(lambda: api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream))
+    step_bytes = sum(_ps_bytes(devt[i]["spec"], wl.P, "buf" in devt[i]) for i in ps_idx)
+    in_iter = sum(launch_ms.get(i, 0.0) for i in ps_idx) + launch_ms.get(-1, 0.0)   # -1: small tensors, batched
+    # The dominant PS launches: the tensors of the largest size (in VGG19 the
+    # seven 512x512x3x3 kernels, 82% of the step's PS bytes).
+    n_big = max(devt[i]["W"].numel() for i in ps_idx)
+    j_bigs = [j for j, i in enumerate(ps_idx) if devt[i]["W"].numel() == n_big]
+    big_bytes = _ps_bytes(devt[ps_idx[j_bigs[0]]]["spec"], wl.P, "buf" in devt[ps_idx[j_bigs[0]]])
+    # (tensors below the iteration's batching threshold have no launch of their own)
+    big_ms = sum(per[j] for j in j_bigs) / len(j_bigs) if all(j in per for j in j_bigs) else None
+    gbs = big_bytes / big_ms / 1e6 if big_ms else None
+    return {
+        "roofline": {"bound": "hbm", "kernel": "ps_apply",
+                     "achieved": round(gbs, 1) if gbs else None,
+                     "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_HBM_GBS, 4) if gbs else None,
+                     "traffic": _stored_traffic("ps_apply_largest", "ps_apply.hip") if wl.config == 5 else None,
+                     "work": f"(4P+16) bytes per element, {n_big} elements per launch ({big_bytes / 1e6:.1f} MB) / "
+                             f"the average duration of the {len(j_bigs)} launches of that size ({big_ms or 0:.4f} ms; "
+                             f"the largest PS tensors, {len(j_bigs) * big_bytes / step_bytes:.0%} of the step's PS "
+                             f"bytes), issued by the library one after another on one stream with nothing else "
+                             f"running, timed by its events on that stream"},
+        "step": {"tensors": len(ps_idx), "bytes": step_bytes,
+                 "sequence_ms": round(seq_ms, 4), "sequence_gbs": round(step_bytes / seq_ms / 1e6, 1),
+                 "summed_launch_ms": round(sum(per.values()), 4),
+                 "in_iteration_summed_launch_ms": round(in_iter, 4)},
+        "batched_pass": {"ms": round(batch_ms, 4), "gbs": round(step_bytes / batch_ms / 1e6, 1)},
+    }
+
+
+def _kv_phase(wl, devt, time_fn, stream, ksteps):
+    """One node's server role through the KV store: the PS tensors cut into
+    2 MB pairs hashed over the P servers; server 0 receives all P workers'
+    updates of every tensor (worker p's update = shard p) and applies its
+    pairs as they complete."""
+    from paper_1706_03292_amd import api
+    import torch
+    pair_elems = (2 << 20) // 4
+    kv_t = [t for t in devt if t["spec"].kind != "fc"]
+    store = api.KVStore([(t["W"].view(-1), t.get("buf")) for t in kv_t], pair_elems, wl.P, 0, wl.lr, wl.momentum)
+    owned = [(t, l) for (t, _, l, s_) in store.pairs if s_ == 0]
+    kv_elems = sum(l for _, l in owned)
+    kv_bytes = float(kv_elems) * (4 * wl.P + 16)
+    rows = [t["shards"].view(wl.P, -1) for t in kv_t]
+
+    def one_iteration():
+        store.begin()
+        for p in range(wl.P):
+            for t in range(len(kv_t)):
+                store.receive(p, t, rows[t][p], stream=stream)
+
+    it_ms = time_fn(one_iteration)
+    # The apply launches alone: the last worker's receives (which enqueue every
+    # apply) are issued while the stream is held by a ~1 ms device-side wait,
+    # so the events around them time the launches back to back, not the host.
+    apply = []
+    for _ in range(ksteps):
+        store.begin()
+        for p in range(wl.P - 1):
+            for t in range(len(kv_t)):
+                store.receive(p, t, rows[t][p], stream=stream)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(2_000_000)
+        a.record(stream)
+        for t in range(len(kv_t)):
+            store.receive(wl.P - 1, t, rows[t][wl.P - 1], stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        apply.append(a.elapsed_time(b))
+    apply_ms = sum(apply) / len(apply)
+    npairs = len(store.pairs)
+    store.close()
+    return {
+        "what": f"server 0 of {wl.P}: its {len(owned)} of {npairs} KV pairs (2 MB) of the {len(kv_t)} PS tensors, "
+                f"{kv_elems} elements, {(4 * wl.P + 16)} bytes each",
+        "bytes": kv_bytes,
+        "iteration_ms": round(it_ms, 4),
+        "apply_ms": round(apply_ms, 4),
+        "apply_gbs": round(kv_bytes / apply_ms / 1e6, 1) if apply_ms else None,
+        "note": "iteration_ms: begin plus all P x tensors receives on one stream, paced by the host's calls; "
+                "apply_ms: HIP events around the last worker's receives, which enqueue every apply, queued "
+                "behind a device-side wait so that the applies run back to back"}
+
+
 def main():
     args = _parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -270,16 +423,6 @@ def main():
     pool.set_timing(False)
     torch.cuda.synchronize()
 
-    fc_list = [(t["W"], t["U"], t["V"]) for t in reversed(devt) if t["spec"].kind == "fc"]
-
-    # The PS applies share the GPU with the SF reconstructions during the
-    # iteration (by design), so their bandwidth is measured in a phase of its
-    # own: the library issues the same launches, every PS tensor of the step
-    # one after another on one pool stream with nothing else running, and its
-    # timing events bracket each launch on that stream.  The batched pass
-    # (poseidon_ps_apply_batch) over the same tensors is timed too.
-    ps_list = [(t["W"], t["shards"], t.get("buf")) for t in reversed(devt) if t["spec"].kind != "fc"]
-
     def _time(fn):
         out = []
         for rep in range(ksteps + 1):
@@ -292,64 +435,14 @@ def main():
                 out.append(a.elapsed_time(b))
         return sum(out) / len(out)
 
-    ps_idx = [i for i, t in enumerate(devt) if t["spec"].kind != "fc"]
-    ps_it = api.SyncIteration(pool, [devt[i] for i in ps_idx], wl.B, wl.P, wl.lr, wl.momentum)
-    ps_seq_ms = _time(lambda: ps_it(stream))          # fork, 35 launches, join
-    pool.set_timing(True)
-    ps_launch = {}
-    for _ in range(ksteps):
-        ps_it(stream)
-        for r in pool.launch_times():
-            ps_launch[r["tensor"]] = ps_launch.get(r["tensor"], 0.0) + r["ms"] / ksteps
-    pool.set_timing(False)
-    torch.cuda.synchronize()
-    ps_ms = sum(ps_launch.values())
-    ps_batch_ms = _time(lambda: api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream))
-    # The dominant PS launches: the tensors of the largest size (in VGG19 the
-    # seven 512x512x3x3 kernels, 82% of the step's PS bytes).
-    n_big = max(devt[i]["W"].numel() for i in ps_idx)
-    j_bigs = [j for j, i in enumerate(ps_idx) if devt[i]["W"].numel() == n_big]
-    big_spec = devt[ps_idx[j_bigs[0]]]["spec"]
-    ps_big_ms = sum(ps_launch[j] for j in j_bigs) / len(j_bigs)
-    ps_big_bytes = _ps_bytes(big_spec, wl.P, "buf" in devt[ps_idx[j_bigs[0]]])
-
-    sfb_flops = sfb_bytes = 0.0
-    ps_bytes = ps_in_iter = sfb_ms = 0.0
-    layers = []
-    fc_idx = [i for i, h in enumerate(host) if h["spec"].kind == "fc"][::-1]
-    for (W, U, V), i in zip(fc_list, fc_idx):
-        spec = host[i]["spec"]
-        ms = _time(lambda: api.sf_apply(W, U, V, wl.lr, stream=stream))
-        f = _sf_flops(spec, wl.K)
-        it_ms = launch_ms.get(i, 0.0)
-        layers.append({"tensor": spec.name, "scheme": "SFB",
-                       "ms": round(it_ms, 4), "tflops": round(f / it_ms / 1e9, 2) if it_ms else None,
-                       "alone_ms": round(ms, 4), "alone_tflops": round(f / ms / 1e9, 2)})
-    # The same layers with a momentum buffer (poseidon_sf_apply_momentum):
-    # W and buf each read and written once.
-    layers_mom = []
-    for (W, U, V), i in zip(fc_list, fc_idx):
-        spec = host[i]["spec"]
-        mbuf = torch.zeros_like(W)
-        ms = _time(lambda: api.sf_apply_momentum(W, mbuf, U, V, wl.lr, wl.momentum, stream=stream))
-        M, N = spec.shape
-        layers_mom.append({"tensor": spec.name, "alone_ms": round(ms, 4),
-                           "tflops": round(_sf_flops(spec, wl.K) / ms / 1e9, 2),
-                           "gbs": round(4.0 * (4 * M * N + wl.K * (M + N)) / ms / 1e6, 1)})
-        del mbuf
-    for i, (h, sch) in enumerate(zip(host, schemes)):
-        spec = h["spec"]
-        if sch == api.SFB:
-            sfb_flops += _sf_flops(spec, wl.K)
-            sfb_bytes += _sf_bytes(spec, wl.K)
-            sfb_ms += launch_ms.get(i, 0.0)
-        else:
-            ps_bytes += _ps_bytes(spec, wl.P, "buf" in h)
-            ps_in_iter += launch_ms.get(i, 0.0)
-    sfb_tflops = sfb_flops / sfb_ms / 1e9 if sfb_ms else None
-    ps_gbs = ps_big_bytes / ps_big_ms / 1e6 if ps_big_ms else None
-    n_ps = sum(1 for s_ in schemes if s_ == api.PS)
-
+    sf = _sf_phase(wl, host, devt, schemes, launch_ms, _time, stream)
+    ps = _ps_phase(wl, devt, schemes, launch_ms, _time, stream, pool, ksteps)
+    # the dominant kernel: the scheme with more launch time inside the iteration
+    dominant = None
+    if sf and (not ps or sf["in_iteration_ms"] >= ps["step"]["in_iteration_summed_launch_ms"]):
+        dominant = sf["roofline"]
+    elif ps:
+        dominant = ps["roofline"]
     result = {
         "metric": METRIC,
         "value": round(wall_ms, 4),
@@ -366,88 +459,19 @@ def main():
         "config": {"workload": f"{wl.name}: {sum(s.numel for s in wl.specs)} params, "
                                f"{len(wl.specs)} tensors, K={wl.K}, lr={wl.lr}, momentum={wl.momentum}",
                    "P": wl.P, "B": wl.B, "streams": args.streams},
-        "roofline": {"bound": "mfma", "kernel": "sf_apply (fp32 MFMA; one launch per FC layer)",
-                     "achieved": round(sfb_tflops, 2) if sfb_tflops else None,
-                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(sfb_tflops / PEAK_FP32_MFMA_TFLOPS, 4) if sfb_tflops else None,
-                     "traffic": _stored_traffic("sf_apply", "sf_apply.hip"),
-                     "work": f"2*M*N*K flops of the {sum(1 for s in schemes if s == api.SFB)} SFB "
-                             f"layers of one step ({sfb_flops / 1e9:.1f} GFLOP) / the summed average "
-                             f"durations of their launches inside the iteration ({sfb_ms:.4f} ms)"},
-        "roofline_ps": {"bound": "hbm", "kernel": "ps_apply",
-                        "achieved": round(ps_gbs, 1) if ps_gbs else None,
-                        "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                        "frac": round(ps_gbs / PEAK_HBM_GBS, 4) if ps_gbs else None,
-                        "traffic": _stored_traffic("ps_apply_largest", "ps_apply.hip"),
-                        "work": f"(4P+16) bytes per element, {n_big} elements per launch "
-                                f"({ps_big_bytes / 1e6:.1f} MB) / the average duration of the {len(j_bigs)} "
-                                f"launches of that size ({ps_big_ms:.4f} ms; the largest PS tensors, "
-                                f"{len(j_bigs) * ps_big_bytes / ps_bytes:.0%} of the step's PS bytes), "
-                                f"issued by the library one after another on one stream with nothing else "
-                                f"running, timed by its events on that stream",
-                        "step": {"tensors": n_ps, "bytes": ps_bytes,
-                                 "sequence_ms": round(ps_seq_ms, 4),
-                                 "sequence_gbs": round(ps_bytes / ps_seq_ms / 1e6, 1),
-                                 "summed_launch_ms": round(ps_ms, 4),
-                                 "in_iteration_summed_launch_ms": round(ps_in_iter, 4)},
-                        "batched_pass": {"ms": round(ps_batch_ms, 4),
-                                         "gbs": round(ps_bytes / ps_batch_ms / 1e6, 1)}},
+        "roofline": dominant,
         "event_ms_per_step": round(event_ms, 4),
-        "sfb_tflops": round(sfb_tflops, 2) if sfb_tflops else None,
-        "ps_gbs": round(ps_gbs, 1) if ps_gbs else None,
-        "layers_sfb": layers,
-        "layers_sfb_momentum": layers_mom,
     }
-    # One node's server role through the KV store: the PS tensors cut into
-    # 2 MB pairs hashed over the P servers; server 0 receives all P workers'
-    # updates of every tensor (worker p's update = shard p) and applies its
-    # pairs as they complete.
-    pair_elems = (2 << 20) // 4
-    kv_t = [devt[i] for i in ps_idx]
-    store = api.KVStore([(t["W"].view(-1), t.get("buf")) for t in kv_t], pair_elems, wl.P, 0, wl.lr, wl.momentum)
-    owned = [(t, l) for (t, _, l, s_) in store.pairs if s_ == 0]
-    kv_elems = sum(l for _, l in owned)
-    kv_bytes = float(kv_elems) * (4 * wl.P + 16)
-    kv_rows = [t["shards"].view(wl.P, -1) for t in kv_t]
-
-    def kv_iter():
-        store.begin()
-        for p in range(wl.P):
-            for t in range(len(kv_t)):
-                store.receive(p, t, kv_rows[t][p], stream=stream)
-
-    kv_ms = _time(kv_iter)
-    # The apply launches alone: the last worker's receives (which enqueue every
-    # apply) are issued while the stream is held by a ~1 ms device-side wait,
-    # so the events around them time the launches back to back, not the host.
-    kv_apply = []
-    for _ in range(ksteps):
-        store.begin()
-        for p in range(wl.P - 1):
-            for t in range(len(kv_t)):
-                store.receive(p, t, kv_rows[t][p], stream=stream)
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        with torch.cuda.stream(stream):
-            torch.cuda._sleep(2_000_000)
-        a.record(stream)
-        for t in range(len(kv_t)):
-            store.receive(wl.P - 1, t, kv_rows[t][wl.P - 1], stream=stream)
-        b.record(stream)
-        torch.cuda.synchronize()
-        kv_apply.append(a.elapsed_time(b))
-    kv_apply_ms = sum(kv_apply) / len(kv_apply)
-    store.close()
-    result["kv_server_share"] = {
-        "what": f"server 0 of {wl.P}: its {len(owned)} of {len(store.pairs)} KV pairs (2 MB) of the {len(kv_t)} PS "
-                f"tensors, {kv_elems} elements, {(4 * wl.P + 16)} bytes each",
-        "bytes": kv_bytes,
-        "iteration_ms": round(kv_ms, 4),
-        "apply_ms": round(kv_apply_ms, 4),
-        "apply_gbs": round(kv_bytes / kv_apply_ms / 1e6, 1),
-        "note": "iteration_ms: begin plus all P x tensors receives on one stream, paced by the host's calls; "
-                "apply_ms: HIP events around the last worker's receives, which enqueue every apply, queued "
-                "behind a device-side wait so that the applies run back to back"}
-    print(f"[bench] KV server share: {result['kv_server_share']}", file=sys.stderr, flush=True)
+    if sf:
+        result["roofline_sf"] = sf["roofline"]
+        result["sfb_tflops"] = sf["roofline"]["achieved"]
+        result["layers_sfb"] = sf["layers"]
+        result["layers_sfb_momentum"] = sf["layers_momentum"]
+    if ps:
+        result["roofline_ps"] = dict(ps["roofline"], step=ps["step"], batched_pass=ps["batched_pass"])
+        result["ps_gbs"] = ps["roofline"]["achieved"]
+        result["kv_server_share"] = _kv_phase(wl, devt, _time, stream, ksteps)
+        print(f"[bench] KV server share: {result['kv_server_share']}", file=sys.stderr, flush=True)
     if args.wfbp == "on" and wl.config == 5:
         print("[bench] WFBP phase (synthetic backward)", file=sys.stderr, flush=True)
         result["wfbp"] = _wfbp_phase(wl, devt, it, pool, d, args.wfbp_steps)

@@ -366,7 +366,11 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation order: the SFB updates (bound by the matrix cores) on the
  * pool's first stream, the PS updates (bound by memory bandwidth) on its
  * second, so that the two kinds overlap; a one-stream pool runs everything in
- * order.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
+ * order.  PS tensors of fewer than 2^17 values, which a launch of their own
+ * would leave latency-bound, are instead applied together, in
+ * backpropagation order, by one batched pass (poseidon_ps_apply_batch's
+ * kernels; the same arithmetic, so the same results) issued after the other
+ * PS launches.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
  * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
  * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,
  * momentum, buf) (momentum is used only when buf != NULL).  Every pool stream first waits for the work already
@@ -417,7 +421,7 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 /* One launch of the last iteration run with timing enabled. */
 typedef struct poseidon_launch_record {
     int32_t scheme;   /* POSEIDON_SFB or POSEIDON_PS */
-    int32_t tensor;   /* index into that call's tensors[] */
+    int32_t tensor;   /* index into that call's tensors[], or -1 for the batched pass of small PS tensors */
     int32_t stream;   /* pool stream index */
     float   ms;       /* time between the events around the launch */
 } poseidon_launch_record;

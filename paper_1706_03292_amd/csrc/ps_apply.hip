@@ -1,192 +1,201 @@
 // Parameter-server aggregation + momentum SGD apply (Sec. 2.1 "Parameter
 // Server"; Sec. 4.1 "KV Store", "Managing Consistency").
 //
-//   s_i = sum_{p<P} G[p*n + i]   (p increasing, fp32)
+//   s_i = sum_{p<P} G_p[i]   (p increasing, fp32)
 //   buf_i = fma(mu, buf_i, s_i);  W_i = fma(-lr, buf_i, W_i)
 //
-// The kernel is bound by HBM bandwidth: per element it reads P shard values
-// plus W and buf and writes W and buf (4P + 16 bytes), against ~P + 3 flops.
-// Each thread owns one 16-byte group of four consecutive elements and issues
-// all of its shard loads before the dependent adds (bytes in flight).  Every
+// The kernels are bound by HBM bandwidth: per element they read P shard
+// values plus W and buf and write W and buf (4P + 16 bytes), against ~P + 3
+// flops.  Each thread owns one group of four consecutive elements and issues
+// all of its shard loads before the dependent adds (bytes in flight); the
+// thread whose group runs past the end of the tensor finishes the last one to
+// three elements one by one.  Every access is 16 bytes wide: aligned when all
+// arrays are 16-byte aligned and the size is a multiple of four (so every
+// shard row starts at a 16-byte boundary), otherwise at 4-byte alignment,
+// which global loads and stores accept (a tensor of 2,786,166 values over 32
+// shards: 5.0 TB/s this way against 3.9 TB/s with 4-byte accesses).  Every
 // array is touched once per launch (shards read; W and buf read, then
 // written), so all accesses are non-temporal (1-2% faster than cached W/buf
-// accesses on 2.4M-16.8M elements).  One-wave workgroups, one
-// group per thread, as many workgroups as groups: a launch-shape sweep over
-// 37K-16.8M elements (block size 64-1024, one or two groups per thread,
-// grid-stride loops capped at 4-16 workgroups per CU) found this within 3% of
-// the best everywhere and 10% faster than a capped grid-stride loop on large
-// tensors, whose last partial pass leaves the chip half idle.  A scalar
-// variant covers sizes that are not a multiple of four or arrays that are not
-// 16-byte aligned.
+// accesses on 2.4M-16.8M elements).  One-wave workgroups, one group per
+// thread, as many workgroups as groups: a launch-shape sweep over 37K-16.8M
+// elements (block size 64-1024, one or two groups per thread, grid-stride
+// loops capped at 4-16 workgroups per CU) found this within 3% of the best
+// everywhere and 10% faster than a capped grid-stride loop on large tensors,
+// whose last partial pass leaves the chip half idle.
+//
+// Three launch forms share the per-group update: one tensor with P
+// contiguous shards, many such tensors in one launch, and the KV store's
+// pairs of one tensor with the P workers' updates at separate addresses.
 #include "common.h"
 
 namespace poseidon {
 namespace {
 
-constexpr int PS_THREADS = 64;    // one wave per workgroup (single-tensor and batched launches)
-constexpr int PS_THREADS_1 = PS_THREADS;
-constexpr int PS_CHUNK = 8;       // shard loads in flight per step when P is a runtime value
+constexpr int PS_THREADS = 64;                  // one wave per workgroup
+constexpr int PS_CHUNK = 8;                     // shard loads in flight per step when P is a runtime value
+constexpr int PS_BLOCK_ELEMS = 4 * PS_THREADS;  // elements per workgroup: one group of four per thread
+constexpr int64_t PS_MAX_GRID = int64_t{1} << 30;
+
+typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));   // 16 bytes at a 4-byte boundary
 
 __device__ inline f4 fma4(float a, f4 b, f4 c)
 {
     return f4{fmaf(a, b.x, c.x), fmaf(a, b.y, c.y), fmaf(a, b.z, c.z), fmaf(a, b.w, c.w)};
 }
 
-// Sum of the P shard values at vector index i, in increasing p.
-template <int PT>
-__device__ inline f4 shard_sum4(const f4* __restrict__ G4, int P, int64_t n4, int64_t i)
+template <bool AL>
+__device__ inline f4 ld4(const float* p)
+{
+    if constexpr (AL)
+        return __builtin_nontemporal_load(reinterpret_cast<const f4*>(p));
+    else
+        return __builtin_nontemporal_load(reinterpret_cast<const f4u*>(p));
+}
+
+template <bool AL>
+__device__ inline void st4(float* p, f4 v)
+{
+    if constexpr (AL)
+        __builtin_nontemporal_store(v, reinterpret_cast<f4*>(p));
+    else
+        __builtin_nontemporal_store(v, reinterpret_cast<f4u*>(p));
+}
+
+// Where worker p's values of a tensor start: P contiguous shards ...
+struct Contiguous {
+    const float* G;
+    int64_t n;
+    __device__ const float* operator()(int p) const { return G + static_cast<int64_t>(p) * n; }
+};
+
+// ... or one pointer per worker (the KV store).
+struct PerWorker {
+    const float* const* g;
+    __device__ const float* operator()(int p) const { return g[p]; }
+};
+
+// Sum of the P values of elements e .. e+3, in increasing p.
+template <int PT, bool AL, class Src>
+__device__ inline f4 sum4(const Src& src, int P, int64_t e)
 {
     if constexpr (PT > 0) {
         f4 g[PT];
 #pragma unroll
         for (int p = 0; p < PT; ++p)
-            g[p] = __builtin_nontemporal_load(G4 + static_cast<int64_t>(p) * n4 + i);
+            g[p] = ld4<AL>(src(p) + e);
         f4 s = g[0];
 #pragma unroll
         for (int p = 1; p < PT; ++p)
             s += g[p];
         return s;
     } else {
-        f4 s = __builtin_nontemporal_load(G4 + i);
+        f4 s = ld4<AL>(src(0) + e);
         int p = 1;
         for (; p + PS_CHUNK <= P; p += PS_CHUNK) {
             f4 g[PS_CHUNK];
 #pragma unroll
             for (int c = 0; c < PS_CHUNK; ++c)
-                g[c] = __builtin_nontemporal_load(G4 + static_cast<int64_t>(p + c) * n4 + i);
+                g[c] = ld4<AL>(src(p + c) + e);
 #pragma unroll
             for (int c = 0; c < PS_CHUNK; ++c)
                 s += g[c];
         }
         for (; p < P; ++p)
-            s += __builtin_nontemporal_load(G4 + static_cast<int64_t>(p) * n4 + i);
+            s += ld4<AL>(src(p) + e);
         return s;
     }
 }
 
-template <int PT>
-__device__ inline float shard_sum1(const float* __restrict__ G, int P, int64_t n, int64_t i)
+// The update of elements e .. min(e + 4, end) - 1 of one tensor.
+template <int PT, bool MOM, bool AL, class Src>
+__device__ inline void apply_group(float* __restrict__ W, float* __restrict__ buf, const Src& src, int P, int64_t e,
+                                   int64_t end, float lr, float mu)
 {
-    if constexpr (PT > 0) {
-        float g[PT];
-#pragma unroll
-        for (int p = 0; p < PT; ++p)
-            g[p] = __builtin_nontemporal_load(G + static_cast<int64_t>(p) * n + i);
-        float s = g[0];
-#pragma unroll
-        for (int p = 1; p < PT; ++p)
-            s += g[p];
-        return s;
-    } else {
-        float s = __builtin_nontemporal_load(G + i);
-        int p = 1;
-        for (; p + PS_CHUNK <= P; p += PS_CHUNK) {
-            float g[PS_CHUNK];
-#pragma unroll
-            for (int c = 0; c < PS_CHUNK; ++c)
-                g[c] = __builtin_nontemporal_load(G + static_cast<int64_t>(p + c) * n + i);
-#pragma unroll
-            for (int c = 0; c < PS_CHUNK; ++c)
-                s += g[c];
-        }
-        for (; p < P; ++p)
-            s += __builtin_nontemporal_load(G + static_cast<int64_t>(p) * n + i);
-        return s;
-    }
-}
-
-template <int PT, bool MOM>
-__global__ __launch_bounds__(PS_THREADS_1) void ps_apply_vec4(
-    float* __restrict__ W, const float* __restrict__ G, int P, int64_t n4,
-    float lr, float mu, float* __restrict__ buf)
-{
-    const f4* G4 = reinterpret_cast<const f4*>(G);
-    f4* W4 = reinterpret_cast<f4*>(W);
-    f4* B4 = reinterpret_cast<f4*>(buf);
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS_1;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS_1 + threadIdx.x; i < n4; i += stride) {
-        const f4 s = shard_sum4<PT>(G4, P, n4, i);
-        f4 w = __builtin_nontemporal_load(W4 + i);
+    if (e + 3 < end) {
+        const f4 s = sum4<PT, AL>(src, P, e);
+        f4 w = ld4<AL>(W + e);
         if constexpr (MOM) {
-            const f4 b = fma4(mu, __builtin_nontemporal_load(B4 + i), s);
-            __builtin_nontemporal_store(b, B4 + i);
+            const f4 b = fma4(mu, ld4<AL>(buf + e), s);
+            st4<AL>(buf + e, b);
             w = fma4(-lr, b, w);
         } else {
             w = fma4(-lr, s, w);
         }
-        __builtin_nontemporal_store(w, W4 + i);
-    }
-}
-
-template <int PT, bool MOM>
-__global__ __launch_bounds__(PS_THREADS_1) void ps_apply_scalar(
-    float* __restrict__ W, const float* __restrict__ G, int P, int64_t n,
-    float lr, float mu, float* __restrict__ buf)
-{
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS_1;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS_1 + threadIdx.x; i < n; i += stride) {
-        const float s = shard_sum1<PT>(G, P, n, i);
-        float w = W[i];
-        if constexpr (MOM) {
-            const float b = fmaf(mu, buf[i], s);
-            buf[i] = b;
-            w = fmaf(-lr, b, w);
-        } else {
-            w = fmaf(-lr, s, w);
+        st4<AL>(W + e, w);
+    } else {
+        for (int64_t k = e; k < end; ++k) {
+            float s = src(0)[k];
+            for (int p = 1; p < (PT > 0 ? PT : P); ++p)
+                s += src(p)[k];
+            float w = W[k];
+            if constexpr (MOM) {
+                const float b = fmaf(mu, buf[k], s);
+                buf[k] = b;
+                w = fmaf(-lr, b, w);
+            } else {
+                w = fmaf(-lr, s, w);
+            }
+            W[k] = w;
         }
-        W[i] = w;
     }
 }
 
-template <int PT, bool MOM>
-hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, float mu,
-                     float* buf, bool vec, hipStream_t stream)
+// ---------------------------------------------------------------------------
+// One tensor, P contiguous shards.
+// ---------------------------------------------------------------------------
+template <int PT, bool MOM, bool AL>
+__global__ __launch_bounds__(PS_THREADS) void ps_apply_kernel(float* __restrict__ W, const float* __restrict__ G,
+                                                              int P, int64_t n, float lr, float mu,
+                                                              float* __restrict__ buf)
 {
-    const int64_t items = vec ? n / 4 : n;
-    // One item per thread; the kernels' grid-stride loop only matters beyond
-    // 2^30 workgroups.
-    const int64_t want = (items + PS_THREADS_1 - 1) / PS_THREADS_1;
-    const int64_t cap = int64_t{1} << 30;
-    const int grid = static_cast<int>(want < cap ? want : cap);
-    if (vec)
-        ps_apply_vec4<PT, MOM><<<grid, PS_THREADS_1, 0, stream>>>(W, G, P, items, lr, mu, buf);
+    const Contiguous src{G, n};
+    const int64_t groups = (n + 3) / 4;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS + threadIdx.x; i < groups; i += stride)
+        apply_group<PT, MOM, AL>(W, buf, src, P, 4 * i, n, lr, mu);
+}
+
+template <int PT, bool MOM>
+hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, float mu, float* buf, bool al,
+                     hipStream_t stream)
+{
+    // One group per thread; the grid-stride loop only matters beyond 2^30 workgroups.
+    const int64_t want = ((n + 3) / 4 + PS_THREADS - 1) / PS_THREADS;
+    const int grid = static_cast<int>(want < PS_MAX_GRID ? want : PS_MAX_GRID);
+    if (al)
+        ps_apply_kernel<PT, MOM, true><<<grid, PS_THREADS, 0, stream>>>(W, G, P, n, lr, mu, buf);
     else
-        ps_apply_scalar<PT, MOM><<<grid, PS_THREADS_1, 0, stream>>>(W, G, P, items, lr, mu, buf);
+        ps_apply_kernel<PT, MOM, false><<<grid, PS_THREADS, 0, stream>>>(W, G, P, n, lr, mu, buf);
     return hipGetLastError();
 }
 
 template <bool MOM>
-hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, float mu,
-                      float* buf, bool vec, hipStream_t stream)
+hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, float mu, float* buf, bool al,
+                      hipStream_t stream)
 {
     switch (P) {
-    case 1:  return launch_pt<1, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
-    case 2:  return launch_pt<2, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
-    case 4:  return launch_pt<4, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
-    case 8:  return launch_pt<8, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
-    case 16: return launch_pt<16, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
-    case 32: return launch_pt<32, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
-    default: return launch_pt<0, MOM>(W, G, P, n, lr, mu, buf, vec, stream);
+    case 1:  return launch_pt<1, MOM>(W, G, P, n, lr, mu, buf, al, stream);
+    case 2:  return launch_pt<2, MOM>(W, G, P, n, lr, mu, buf, al, stream);
+    case 4:  return launch_pt<4, MOM>(W, G, P, n, lr, mu, buf, al, stream);
+    case 8:  return launch_pt<8, MOM>(W, G, P, n, lr, mu, buf, al, stream);
+    case 16: return launch_pt<16, MOM>(W, G, P, n, lr, mu, buf, al, stream);
+    case 32: return launch_pt<32, MOM>(W, G, P, n, lr, mu, buf, al, stream);
+    default: return launch_pt<0, MOM>(W, G, P, n, lr, mu, buf, al, stream);
     }
 }
 
 // ---------------------------------------------------------------------------
 // Many tensors in one launch.  The descriptors travel by value in the kernel
 // arguments; tensor t owns the workgroups [first_block[t], first_block[t+1]),
-// each of which updates PS_BLOCK_ELEMS consecutive elements of it (16-byte
-// groups when the tensor allows it, single elements otherwise).
+// each of which updates PS_BLOCK_ELEMS consecutive elements of it.
 // ---------------------------------------------------------------------------
-
-constexpr int PS_BLOCK_ELEMS = 4 * PS_THREADS;  // elements per work block: one 16-byte group per thread
-constexpr int PS_BATCH_MAX_GRID = 1 << 30;     // one workgroup per work block below this
-
 struct PsBatchItem {
     float* W;
     const float* G;
     float* buf;
     int64_t n;
     int32_t first_block;
-    int32_t vec;
+    int32_t aligned;
 };
 
 struct PsBatchArgs {
@@ -199,61 +208,23 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_batch_kernel(const PsBatc
                                                                     float mu, int total_blocks)
 {
     // Workgroup g handles work blocks g, g + gridDim.x, ... (one pass when the
-    // grid covers every block); the block's tensor is found by binary search
-    // over the descriptors' first blocks (uniform, scalar loads).
+    // grid covers every block).  The block's tensor is the number of later
+    // descriptors whose first block it has reached: a fully unrolled count
+    // whose scalar loads are independent, so a workgroup waits for one load
+    // latency (a binary search waits for one per step).
     for (int b = blockIdx.x; b < total_blocks; b += gridDim.x) {
-        int lo = 0, hi = args.count - 1;
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (args.item[mid].first_block <= b)
-                lo = mid;
-            else
-                hi = mid - 1;
-        }
-        const int t = lo;
-        float* __restrict__ W = args.item[t].W;
-        const float* __restrict__ G = args.item[t].G;
-        float* __restrict__ buf = args.item[t].buf;
-        const int64_t n = args.item[t].n;
-        const int64_t base = static_cast<int64_t>(b - args.item[t].first_block) * PS_BLOCK_ELEMS;
-        if (args.item[t].vec) {
-            const int64_t n4 = n >> 2;
-            const f4* G4 = reinterpret_cast<const f4*>(G);
-            f4* W4 = reinterpret_cast<f4*>(W);
-            f4* B4 = reinterpret_cast<f4*>(buf);
+        int t = 0;
 #pragma unroll
-            for (int u = 0; u < PS_BLOCK_ELEMS / 4 / PS_THREADS; ++u) {
-                const int64_t i = (base >> 2) + u * PS_THREADS + threadIdx.x;
-                if (i < n4) {
-                    const f4 s = shard_sum4<PT>(G4, P, n4, i);
-                    f4 w = __builtin_nontemporal_load(W4 + i);
-                    if constexpr (MOM) {
-                        const f4 bv = fma4(mu, __builtin_nontemporal_load(B4 + i), s);
-                        __builtin_nontemporal_store(bv, B4 + i);
-                        w = fma4(-lr, bv, w);
-                    } else {
-                        w = fma4(-lr, s, w);
-                    }
-                    __builtin_nontemporal_store(w, W4 + i);
-                }
-            }
-        } else {
-#pragma unroll 4
-            for (int u = 0; u < PS_BLOCK_ELEMS / PS_THREADS; ++u) {
-                const int64_t i = base + u * PS_THREADS + threadIdx.x;
-                if (i < n) {
-                    const float s = shard_sum1<PT>(G, P, n, i);
-                    float w = W[i];
-                    if constexpr (MOM) {
-                        const float bv = fmaf(mu, buf[i], s);
-                        buf[i] = bv;
-                        w = fmaf(-lr, bv, w);
-                    } else {
-                        w = fmaf(-lr, s, w);
-                    }
-                    W[i] = w;
-                }
-            }
+        for (int k = 1; k < PS_BATCH_MAX; ++k)
+            t += (k < args.count && args.item[k].first_block <= b) ? 1 : 0;
+        const PsBatchItem& it = args.item[t];
+        const int64_t e = static_cast<int64_t>(b - it.first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
+        if (e < it.n) {
+            const Contiguous src{it.G, it.n};
+            if (it.aligned)
+                apply_group<PT, MOM, true>(it.W, it.buf, src, P, e, it.n, lr, mu);
+            else
+                apply_group<PT, MOM, false>(it.W, it.buf, src, P, e, it.n, lr, mu);
         }
     }
 }
@@ -284,10 +255,8 @@ void launch_batch_mom(const PsBatchArgs& a, int blocks, int grid, int32_t P, flo
 // workers' updates at separate addresses (one pointer per worker, passed in
 // worker order).  Range r covers tensor elements [offset, offset + length)
 // and owns the workgroups [first_block[r], first_block[r+1]); each workgroup
-// updates PS_BLOCK_ELEMS consecutive elements of its range, one group of four
-// per thread (16-byte accesses when the whole launch allows them).
+// updates PS_BLOCK_ELEMS consecutive elements of its range.
 // ---------------------------------------------------------------------------
-
 struct KvRange {
     int64_t offset;
     int64_t length;
@@ -301,99 +270,31 @@ struct KvArgs {
     int32_t nranges;
 };
 
-// Sum of the P updates of the four elements at e, in increasing worker order.
-template <int PT>
-__device__ inline f4 kv_sum4(const KvArgs& a, int P, int64_t e)
-{
-    if constexpr (PT > 0) {
-        f4 g[PT];
-#pragma unroll
-        for (int p = 0; p < PT; ++p)
-            g[p] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[p] + e));
-        f4 s = g[0];
-#pragma unroll
-        for (int p = 1; p < PT; ++p)
-            s += g[p];
-        return s;
-    } else {
-        f4 s = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[0] + e));
-        int p = 1;
-        for (; p + PS_CHUNK <= P; p += PS_CHUNK) {
-            f4 g[PS_CHUNK];
-#pragma unroll
-            for (int c = 0; c < PS_CHUNK; ++c)
-                g[c] = __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[p + c] + e));
-#pragma unroll
-            for (int c = 0; c < PS_CHUNK; ++c)
-                s += g[c];
-        }
-        for (; p < P; ++p)
-            s += __builtin_nontemporal_load(reinterpret_cast<const f4*>(a.g[p] + e));
-        return s;
-    }
-}
-
-template <int PT>
-__device__ inline float kv_sum1(const KvArgs& a, int P, int64_t e)
-{
-    float s = a.g[0][e];
-    for (int p = 1; p < (PT > 0 ? PT : P); ++p)
-        s += a.g[p][e];
-    return s;
-}
-
-template <int PT, bool MOM>
+template <int PT, bool MOM, bool AL>
 __global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, int P, float* __restrict__ W,
-                                                               float* __restrict__ buf, float lr, float mu, int vec)
+                                                               float* __restrict__ buf, float lr, float mu)
 {
     const int b = blockIdx.x;
-    int r = 0;
-    while (r + 1 < a.nranges && a.r[r + 1].first_block <= b)
-        ++r;
-    const int64_t len = a.r[r].length;
+    int r = 0;                                  // as in the batched kernel: independent loads
+#pragma unroll
+    for (int k = 1; k < KV_MAX_RANGES; ++k)
+        r += (k < a.nranges && a.r[k].first_block <= b) ? 1 : 0;
     const int64_t j = static_cast<int64_t>(b - a.r[r].first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
-    if (j >= len)
+    if (j >= a.r[r].length)
         return;
-    const int64_t e = a.r[r].offset + j;
-    if (vec && j + 3 < len) {
-        const f4 s = kv_sum4<PT>(a, P, e);
-        f4* W4 = reinterpret_cast<f4*>(W + e);
-        f4 w = __builtin_nontemporal_load(W4);
-        if constexpr (MOM) {
-            f4* B4 = reinterpret_cast<f4*>(buf + e);
-            const f4 bv = fma4(mu, __builtin_nontemporal_load(B4), s);
-            __builtin_nontemporal_store(bv, B4);
-            w = fma4(-lr, bv, w);
-        } else {
-            w = fma4(-lr, s, w);
-        }
-        __builtin_nontemporal_store(w, W4);
-    } else {
-        for (int q = 0; q < 4 && j + q < len; ++q) {
-            const float s = kv_sum1<PT>(a, P, e + q);
-            float w = W[e + q];
-            if constexpr (MOM) {
-                const float bv = fmaf(mu, buf[e + q], s);
-                buf[e + q] = bv;
-                w = fmaf(-lr, bv, w);
-            } else {
-                w = fmaf(-lr, s, w);
-            }
-            W[e + q] = w;
-        }
-    }
+    const PerWorker src{a.g};
+    apply_group<PT, MOM, AL>(W, buf, src, P, a.r[r].offset + j, a.r[r].offset + a.r[r].length, lr, mu);
 }
 
-template <bool MOM>
-void launch_kv_mom(const KvArgs& a, int grid, int32_t P, float* W, float* buf, float lr, float mu, int vec,
-                   hipStream_t stream)
+template <bool MOM, bool AL>
+void launch_kv_al(const KvArgs& a, int grid, int32_t P, float* W, float* buf, float lr, float mu, hipStream_t stream)
 {
     switch (P) {
-    case 4:  kv_apply_kernel<4, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
-    case 8:  kv_apply_kernel<8, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
-    case 16: kv_apply_kernel<16, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
-    case 32: kv_apply_kernel<32, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
-    default: kv_apply_kernel<0, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu, vec); break;
+    case 4:  kv_apply_kernel<4, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
+    case 8:  kv_apply_kernel<8, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
+    case 16: kv_apply_kernel<16, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
+    case 32: kv_apply_kernel<32, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
+    default: kv_apply_kernel<0, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
     }
 }
 
@@ -402,10 +303,10 @@ void launch_kv_mom(const KvArgs& a, int grid, int32_t P, float* W, float* buf, f
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
                            float lr, float momentum, float* buf, hipStream_t stream)
 {
-    const bool vec = (n % 4 == 0) && aligned16(W) && aligned16(shards) && (!buf || aligned16(buf));
+    const bool al = (n % 4 == 0) && aligned16(W) && aligned16(shards) && (!buf || aligned16(buf));
     if (buf)
-        return launch_mom<true>(W, shards, P, n, lr, momentum, buf, vec, stream);
-    return launch_mom<false>(W, shards, P, n, lr, 0.0f, nullptr, vec, stream);
+        return launch_mom<true>(W, shards, P, n, lr, momentum, buf, al, stream);
+    return launch_mom<false>(W, shards, P, n, lr, 0.0f, nullptr, al, stream);
 }
 
 hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, float lr, float momentum,
@@ -422,7 +323,7 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
             if (a.count == 0)
                 return hipSuccess;
             const int nb = static_cast<int>(blocks);
-            const int grid = nb < PS_BATCH_MAX_GRID ? nb : PS_BATCH_MAX_GRID;
+            const int grid = nb < PS_MAX_GRID ? nb : static_cast<int>(PS_MAX_GRID);
             if (mom)
                 launch_batch_mom<true>(a, nb, grid, P, lr, momentum, stream);
             else
@@ -446,8 +347,8 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
             it.buf = t[i].buf;
             it.n = t[i].n;
             it.first_block = static_cast<int32_t>(blocks);
-            it.vec = (t[i].n % 4 == 0) && aligned16(t[i].W) && aligned16(t[i].shards) &&
-                     (!t[i].buf || aligned16(t[i].buf));
+            it.aligned = (t[i].n % 4 == 0) && aligned16(t[i].W) && aligned16(t[i].shards) &&
+                         (!t[i].buf || aligned16(t[i].buf));
             blocks += nb;
         }
         const hipError_t e = flush();
@@ -460,11 +361,11 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
 hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int32_t P, const int64_t* offsets,
                            const int64_t* lengths, int32_t nranges, float lr, float momentum, hipStream_t stream)
 {
-    bool vec = aligned16(W) && (!buf || aligned16(buf));
+    bool al = aligned16(W) && (!buf || aligned16(buf));
     for (int32_t p = 0; p < P; ++p)
-        vec = vec && aligned16(grads[p]);
+        al = al && aligned16(grads[p]);
     for (int32_t i = 0; i < nranges; ++i)
-        vec = vec && offsets[i] % 4 == 0;
+        al = al && offsets[i] % 4 == 0;
     for (int32_t i0 = 0; i0 < nranges; i0 += KV_MAX_RANGES) {
         KvArgs a{};
         for (int32_t p = 0; p < P; ++p)
@@ -481,10 +382,18 @@ hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int3
         }
         if (blocks == 0)
             continue;
-        if (buf)
-            launch_kv_mom<true>(a, static_cast<int>(blocks), P, W, buf, lr, momentum, vec ? 1 : 0, stream);
-        else
-            launch_kv_mom<false>(a, static_cast<int>(blocks), P, W, nullptr, lr, 0.0f, vec ? 1 : 0, stream);
+        const int grid = static_cast<int>(blocks);
+        if (buf) {
+            if (al)
+                launch_kv_al<true, true>(a, grid, P, W, buf, lr, momentum, stream);
+            else
+                launch_kv_al<true, false>(a, grid, P, W, buf, lr, momentum, stream);
+        } else {
+            if (al)
+                launch_kv_al<false, true>(a, grid, P, W, nullptr, lr, 0.0f, stream);
+            else
+                launch_kv_al<false, false>(a, grid, P, W, nullptr, lr, 0.0f, stream);
+        }
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;

@@ -124,6 +124,11 @@ extern "C" int poseidon_pool_destroy(poseidon_stream_pool* pool)
 
 namespace {
 
+// PS tensors below this many elements are launch-bound on their own (a launch
+// costs a few microseconds; 2^17 elements at P = 32 move 19 MB, about 4 us of
+// HBM time): the iteration gathers them into batched launches.
+constexpr int64_t SMALL_PS_ELEMS = int64_t{1} << 17;
+
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
 // for the work enqueued on `stream` before the call) and of
 // poseidon_sync_iteration_wfbp (tensor t's update waits for ready[t] only).
@@ -143,6 +148,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // Validate everything and fix every scheme before enqueueing anything.
     std::vector<int32_t> plan(static_cast<size_t>(count));
     int32_t active = 0;
+    int32_t small_ps = 0;
     for (int32_t t = 0; t < count; ++t) {
         const poseidon_tensor& x = tensors[t];
         if ((x.kind != POSEIDON_KIND_FC && x.kind != POSEIDON_KIND_OTHER) || x.reserved != 0 ||
@@ -167,7 +173,9 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
             if (n > 0 && !x.shards)
                 return POSEIDON_ERR_PAYLOAD;
             rc = check_ps_args(x.W, x.shards, P, n, x.buf ? momentum : 0.0f, x.buf);
-            if (n > 0)
+            if (n > 0 && n < SMALL_PS_ELEMS)
+                ++small_ps;
+            else if (n > 0)
                 ++active;
         }
         if (rc != POSEIDON_OK)
@@ -179,9 +187,11 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
             schemes[t] = plan[static_cast<size_t>(t)];
-    // One launch per tensor with work.  (A grouped launch of all SF layers
-    // measured slower than per-layer launches, alone and beside the PS work.)
-    const int32_t launches = active;
+    // One launch per tensor with work, except small PS tensors, which share
+    // one batched pass after the other PS launches.  (A grouped launch of the
+    // SF layers gains nothing inside the iteration, where the PS work already
+    // fills their tails, and per-layer launches keep per-layer records.)
+    const int32_t launches = active + (small_ps > 0 ? 1 : 0);
     if (pool->timing) {
         if (!reserve_timing(pool, launches))
             return POSEIDON_ERR_HIP;
@@ -226,11 +236,18 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         }
         return true;
     };
+    std::vector<PsTensor> small;     // in backpropagation order
+    std::vector<int32_t> small_idx;
     for (int32_t t = count - 1; t >= 0; --t) {
         const poseidon_tensor& x = tensors[t];
         const int64_t n = x.M * x.N;
         if (n == 0)
             continue;
+        if (plan[static_cast<size_t>(t)] == POSEIDON_PS && n < SMALL_PS_ELEMS) {
+            small.push_back(PsTensor{x.W, x.shards, x.buf, n});
+            small_idx.push_back(t);
+            continue;
+        }
         if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
             if (K == 0 && !x.buf)
                 continue;
@@ -247,6 +264,30 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
                     return launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
                 }))
                 return POSEIDON_ERR_HIP;
+        }
+    }
+
+    if (!small.empty()) {
+        // The batched pass waits for every ready event of its tensors.
+        const int32_t si = used == 1 ? 0 : 1;
+        hipStream_t s = pool->streams[si];
+        if (ready)
+            for (int32_t t : small_idx)
+                if (ready[t] != waited[si]) {
+                    if (hipStreamWaitEvent(s, ready[t], 0) != hipSuccess)
+                        return POSEIDON_ERR_HIP;
+                    waited[si] = ready[t];
+                }
+        const size_t r = pool->t_rec.size();
+        if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
+            return POSEIDON_ERR_HIP;
+        if (launch_ps_apply_batch(small.data(), static_cast<int32_t>(small.size()), P, lr, momentum, s) !=
+            hipSuccess)
+            return POSEIDON_ERR_HIP;
+        if (pool->timing) {
+            if (hipEventRecord(pool->t_stop[r], s) != hipSuccess)
+                return POSEIDON_ERR_HIP;
+            pool->t_rec.push_back(poseidon_launch_record{POSEIDON_PS, -1, si, 0.0f});
         }
     }
 

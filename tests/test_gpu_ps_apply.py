@@ -71,6 +71,22 @@ def test_ps_apply_with_buffer_and_zero_momentum():
     assert_close(to_np(bd), b_ref, BUF_TOL, "buf")
 
 
+@pytest.mark.parametrize("P,n", [(32, 9 * 1024 + 4), (16, 262144), (5, 4100)])
+def test_ps_apply_unaligned_path_bit_identical_to_aligned(P, n):
+    """The same tensor through the 16-byte-aligned accesses and, as misaligned
+    copies, through the 4-byte-aligned ones: the same sums in the same order,
+    so bit-identical results."""
+    d = dev()
+    W, G, buf = _draw(P, n, seed=21 + P, buf_std=1e-3)
+    Wa, Ga, ba = W.to(d), G.to(d), buf.to(d)
+    Wm, Gm, bm = misaligned(W.to(d)), misaligned(G.to(d)), misaligned(buf.to(d))
+    log(f"ps_apply aligned vs unaligned P={P} n={n}")
+    api.ps_apply(Wa, Ga, 0.01, 0.9, ba)
+    api.ps_apply(Wm, Gm, 0.01, 0.9, bm)
+    torch.cuda.synchronize()
+    assert torch.equal(Wa, Wm) and torch.equal(ba, bm)
+
+
 @pytest.mark.parametrize("P,n", [(16, 4096), (4, 1001)])
 def test_ps_apply_misaligned(P, n):
     d = dev()

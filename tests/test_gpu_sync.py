@@ -135,7 +135,7 @@ def test_sync_iteration_missing_payload_is_an_error():
 
 def test_sync_iteration_launch_records():
     """Timing mode: one record per launch in backprop order, SF layers on
-    stream 0 and PS tensors on stream 1."""
+    stream 0 and PS tensors on stream 1 (small ones in one batched pass)."""
     d = dev()
     wl = I.workload(5)
     host = I.make_tensors(wl, only=["fc7.W", "fc7.b", "conv5_4.W"])
@@ -146,8 +146,14 @@ def test_sync_iteration_launch_records():
     log("sync_iteration timing records")
     it()
     recs = pool.launch_times()
+    # SF layers on stream 0; PS tensors on stream 1, those under 2^17 values
+    # gathered into one batched pass (tensor -1) after the others.
     want = [(api.SFB, i, 0) if h["spec"].kind == I.FC else (api.PS, i, 1)
-            for i, h in reversed(list(enumerate(host)))]
+            for i, h in reversed(list(enumerate(host)))
+            if h["spec"].kind == I.FC or h["spec"].numel >= 1 << 17]
+    if any(h["spec"].kind != I.FC and h["spec"].numel < 1 << 17 for h in host):
+        want.append((api.PS, -1, 1))
+    assert want[-1] == (api.PS, -1, 1)                 # fc7.b (4096 values) is batched
     assert [(r["scheme"], r["tensor"], r["stream"]) for r in recs] == want
     assert all(r["ms"] > 0 for r in recs)
     pool.set_timing(False)

@@ -224,8 +224,14 @@ def test_wfbp_launch_records_and_errors():
     log("wfbp timing records")
     it(cs, ready=[ev] * len(devt))
     recs = pool.launch_times()
+    # SF layers on stream 0; PS tensors on stream 1, those under 2^17 values
+    # gathered into one batched pass (tensor -1) after the others.
     want = [(api.SFB, i, 0) if h["spec"].kind == I.FC else (api.PS, i, 1)
-            for i, h in reversed(list(enumerate(host)))]
+            for i, h in reversed(list(enumerate(host)))
+            if h["spec"].kind == I.FC or h["spec"].numel >= 1 << 17]
+    if any(h["spec"].kind != I.FC and h["spec"].numel < 1 << 17 for h in host):
+        want.append((api.PS, -1, 1))
+    assert want[-1] == (api.PS, -1, 1)                 # fc7.b (4096 values) is batched
     assert [(r["scheme"], r["tensor"], r["stream"]) for r in recs] == want
     assert all(r["ms"] > 0 for r in recs)
     pool.set_timing(False)
