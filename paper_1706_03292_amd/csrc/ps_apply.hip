@@ -199,6 +199,7 @@ struct PsBatchItem {
 };
 
 struct PsBatchArgs {
+    int32_t first_block[PS_BATCH_MAX];   // item[t].first_block, contiguous: a few wide scalar loads
     PsBatchItem item[PS_BATCH_MAX];
     int32_t count;
 };
@@ -210,13 +211,14 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_batch_kernel(const PsBatc
     // Workgroup g handles work blocks g, g + gridDim.x, ... (one pass when the
     // grid covers every block).  The block's tensor is the number of later
     // descriptors whose first block it has reached: a fully unrolled count
-    // whose scalar loads are independent, so a workgroup waits for one load
-    // latency (a binary search waits for one per step).
+    // over the contiguous first-block array, read with a few wide scalar
+    // loads, so a wave waits for one load latency before it knows its tensor
+    // (a binary search waits for one per step).
     for (int b = blockIdx.x; b < total_blocks; b += gridDim.x) {
         int t = 0;
 #pragma unroll
         for (int k = 1; k < PS_BATCH_MAX; ++k)
-            t += (k < args.count && args.item[k].first_block <= b) ? 1 : 0;
+            t += (k < args.count && args.first_block[k] <= b) ? 1 : 0;
         const PsBatchItem& it = args.item[t];
         const int64_t e = static_cast<int64_t>(b - it.first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
         if (e < it.n) {
@@ -266,6 +268,7 @@ struct KvRange {
 
 struct KvArgs {
     const float* g[KV_MAX_P];
+    int32_t first_block[KV_MAX_RANGES];   // r[k].first_block, contiguous (as in the batched kernel)
     KvRange r[KV_MAX_RANGES];
     int32_t nranges;
 };
@@ -278,7 +281,7 @@ __global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, in
     int r = 0;                                  // as in the batched kernel: independent loads
 #pragma unroll
     for (int k = 1; k < KV_MAX_RANGES; ++k)
-        r += (k < a.nranges && a.r[k].first_block <= b) ? 1 : 0;
+        r += (k < a.nranges && a.first_block[k] <= b) ? 1 : 0;
     const int64_t j = static_cast<int64_t>(b - a.r[r].first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
     if (j >= a.r[r].length)
         return;
@@ -347,6 +350,7 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
             it.buf = t[i].buf;
             it.n = t[i].n;
             it.first_block = static_cast<int32_t>(blocks);
+            a.first_block[a.count - 1] = it.first_block;
             it.aligned = (t[i].n % 4 == 0) && aligned16(t[i].W) && aligned16(t[i].shards) &&
                          (!t[i].buf || aligned16(t[i].buf));
             blocks += nb;
@@ -376,6 +380,7 @@ hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int3
             r.offset = offsets[i];
             r.length = lengths[i];
             r.first_block = static_cast<int32_t>(blocks);
+            a.first_block[a.nranges - 1] = r.first_block;
             blocks += (lengths[i] + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
             if (blocks > INT32_MAX)
                 return hipErrorInvalidValue;
