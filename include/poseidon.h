@@ -14,7 +14,10 @@
  *
  * General conventions
  *  - All array arguments are device pointers to fp32 data owned by the caller.
- *    The library keeps no pointer past a call and allocates no device memory.
+ *    The library allocates no device memory and keeps no pointer past a call,
+ *    except a KV store, which keeps its tensors' pointers for its lifetime and
+ *    each received update's pointer until the work it triggers has been
+ *    enqueued (and the caller keeps that memory valid until the work has run).
  *  - Work is enqueued asynchronously on `stream` (0 = the null stream).
  *    Argument errors are detected and reported synchronously, before anything
  *    is enqueued; a fault inside a kernel surfaces at the next synchronisation
@@ -25,8 +28,8 @@
  *  - Outputs must not overlap inputs (checked: overlapping ranges are an
  *    argument error).
  *  - The functions are thread-safe and keep no mutable global state, except the
- *    stream pool object, which belongs to its creator and must not be used by
- *    two threads at once.
+ *    stream pool and KV store objects, which belong to their creator and must
+ *    not be used by two threads at once.
  *  - Results are deterministic: the same inputs give bit-identical outputs.
  */
 #ifndef POSEIDON_H
