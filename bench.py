@@ -212,26 +212,29 @@ def _cpu_baseline(wl, host, fraction, min_seconds):
 
 
 def _sf_phase(wl, host, devt, schemes, launch_ms, time_fn, stream):
-    """The SF-reconstruction kernel: per-layer durations inside the iteration
-    (launch records) and alone, with and without a momentum buffer; None when
-    no layer takes SFB."""
+    """The SF-reconstruction kernel: its launch time inside the iteration (the
+    grouped launch of the FC layers, or per-layer launches; launch records)
+    and each layer alone, with and without a momentum buffer; None when no
+    layer takes SFB."""
     from paper_1706_03292_amd import api
     import torch
     idx = [i for i, s_ in enumerate(schemes) if s_ == api.SFB][::-1]      # backprop order
     if not idx:
         return None
     layers, layers_mom = [], []
-    flops = in_ms = 0.0
+    flops = 0.0
+    grouped_ms = launch_ms.get((api.SFB, -1))
+    in_ms = (grouped_ms or 0.0) + sum(launch_ms.get((api.SFB, i), 0.0) for i in idx)
     for i in idx:
         spec, t = host[i]["spec"], devt[i]
         W, U, V = t["W"], t["U"], t["V"]
         f = _sf_flops(spec, wl.K)
         ms = time_fn(lambda: api.sf_apply(W, U, V, wl.lr, stream=stream))
-        it_ms = launch_ms.get(i, 0.0)
+        it_ms = launch_ms.get((api.SFB, i))
         flops += f
-        in_ms += it_ms
         layers.append({"tensor": spec.name, "scheme": "SFB",
-                       "ms": round(it_ms, 4), "tflops": round(f / it_ms / 1e9, 2) if it_ms else None,
+                       "ms": round(it_ms, 4) if it_ms else None,
+                       "tflops": round(f / it_ms / 1e9, 2) if it_ms else None,
                        "alone_ms": round(ms, 4), "alone_tflops": round(f / ms / 1e9, 2)})
         # the same layer with a momentum buffer: W and buf each read and written once
         mbuf = torch.zeros_like(W)
@@ -241,18 +244,21 @@ def _sf_phase(wl, host, devt, schemes, launch_ms, time_fn, stream):
                            "gbs": round(4.0 * (4 * M * N + wl.K * (M + N)) / ms / 1e6, 1)})
         del mbuf
     tflops = flops / in_ms / 1e9 if in_ms else None
+    how = (f"the grouped launch of the {len(idx)} SFB layers inside the iteration ({grouped_ms:.4f} ms)"
+           if grouped_ms else f"the summed average durations of their launches inside the iteration ({in_ms:.4f} ms)")
     return {
         "in_iteration_ms": in_ms,
         "layers": layers,
         "layers_momentum": layers_mom,
-        "roofline": {"bound": "mfma", "kernel": "sf_apply (fp32 MFMA; one launch per FC layer)",
+        "roofline": {"bound": "mfma",
+                     "kernel": "sf_apply (fp32 MFMA; " + ("one grouped launch for the FC layers)" if grouped_ms
+                                                          else "one launch per FC layer)"),
                      "achieved": round(tflops, 2) if tflops else None,
                      "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tflops / PEAK_FP32_MFMA_TFLOPS, 4) if tflops else None,
                      "traffic": _stored_traffic("sf_apply", "sf_apply.hip") if wl.config == 5 else None,
                      "work": f"2*M*N*K flops of the {len(idx)} SFB layers of one step ({flops / 1e9:.1f} GFLOP) / "
-                             f"the summed average durations of their launches inside the iteration "
-                             f"({in_ms:.4f} ms)"},
+                             + how},
     }
 
 
@@ -281,7 +287,7 @@ def _ps_phase(wl, devt, schemes, launch_ms, time_fn, stream, pool, ksteps):
     torch.cuda.synchronize()
     batch_ms = time_fn(lambda: api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream))
     step_bytes = sum(_ps_bytes(devt[i]["spec"], wl.P, "buf" in devt[i]) for i in ps_idx)
-    in_iter = sum(launch_ms.get(i, 0.0) for i in ps_idx) + launch_ms.get(-1, 0.0)   # -1: small tensors, batched
+    in_iter = sum(launch_ms.get((api.PS, i), 0.0) for i in ps_idx) + launch_ms.get((api.PS, -1), 0.0)
     # The dominant PS launches: the tensors of the largest size (in VGG19 the
     # seven 512x512x3x3 kernels, 82% of the step's PS bytes).
     n_big = max(devt[i]["W"].numel() for i in ps_idx)
@@ -442,7 +448,8 @@ def main():
     for _ in range(ksteps):
         it(stream)
         for r in pool.launch_times():
-            launch_ms[r["tensor"]] = launch_ms.get(r["tensor"], 0.0) + r["ms"] / ksteps
+            key = (r["scheme"], r["tensor"])        # tensor -1: a shared launch of that scheme
+            launch_ms[key] = launch_ms.get(key, 0.0) + r["ms"] / ksteps
     pool.set_timing(False)
     torch.cuda.synchronize()
 

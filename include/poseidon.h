@@ -369,11 +369,14 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * backpropagation order: the SFB updates (bound by the matrix cores) on the
  * pool's first stream, the PS updates (bound by memory bandwidth) on its
  * second, so that the two kinds overlap; a one-stream pool runs everything in
- * order.  PS tensors of fewer than 2^17 values, which a launch of their own
- * would leave latency-bound, are instead applied together, in
- * backpropagation order, by one batched pass (poseidon_ps_apply_batch's
- * kernels; the same arithmetic, so the same results) issued after the other
- * PS launches.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
+ * order.  Two kinds of tensors share launches instead (with the kernels and
+ * arithmetic of the single-tensor calls, so the same results): PS tensors of
+ * fewer than 2^17 values, which a launch of their own would leave
+ * latency-bound, are applied together, in backpropagation order, by one
+ * batched pass (poseidon_ps_apply_batch) after the other PS launches; and the
+ * SFB tensors without a momentum buffer, when there are several, are rebuilt
+ * by one grouped launch (poseidon_sf_apply_batch) at the place of the first
+ * of them, so that the layers' tiles share one work list.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
  * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
  * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,
  * momentum, buf) (momentum is used only when buf != NULL).  Every pool stream first waits for the work already
@@ -402,7 +405,9 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
  * reads W_t or writes t's payload (U/V rows or shards) in this iteration;
  * tensors of one layer may share an event.  Issue order, streams, schemes,
  * payload rules and results are those of poseidon_sync_iteration (bitwise:
- * the same launches); `stream` waits for every update at the end.
+ * the same kernels), except that every SFB tensor keeps a launch of its own
+ * (no grouped launch), so that each starts after its own event; `stream`
+ * waits for every update at the end.
  * ready: count non-NULL events, caller-owned, not retained after the call.
  * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (also for NULL ready or a NULL
  * entry), POSEIDON_ERR_PAYLOAD or POSEIDON_ERR_HIP.
@@ -424,7 +429,9 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 /* One launch of the last iteration run with timing enabled. */
 typedef struct poseidon_launch_record {
     int32_t scheme;   /* POSEIDON_SFB or POSEIDON_PS */
-    int32_t tensor;   /* index into that call's tensors[], or -1 for the batched pass of small PS tensors */
+    int32_t tensor;   /* index into that call's tensors[], or -1 for a shared launch (scheme
+                         POSEIDON_PS: the batched pass of the small PS tensors; POSEIDON_SFB:
+                         the grouped launch of the SFB tensors without a buffer) */
     int32_t stream;   /* pool stream index */
     float   ms;       /* time between the events around the launch */
 } poseidon_launch_record;

@@ -149,6 +149,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     std::vector<int32_t> plan(static_cast<size_t>(count));
     int32_t active = 0;
     int32_t small_ps = 0;
+    int32_t plain_sf = 0;     // SFB layers without a momentum buffer
     for (int32_t t = 0; t < count; ++t) {
         const poseidon_tensor& x = tensors[t];
         if ((x.kind != POSEIDON_KIND_FC && x.kind != POSEIDON_KIND_OTHER) || x.reserved != 0 ||
@@ -169,6 +170,8 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
                        : check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
             if (n > 0 && (K > 0 || x.buf))
                 ++active;
+            if (n > 0 && K > 0 && !x.buf)
+                ++plain_sf;
         } else {
             if (n > 0 && !x.shards)
                 return POSEIDON_ERR_PAYLOAD;
@@ -187,11 +190,17 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
             schemes[t] = plan[static_cast<size_t>(t)];
-    // One launch per tensor with work, except small PS tensors, which share
-    // one batched pass after the other PS launches.  (A grouped launch of the
-    // SF layers gains nothing inside the iteration, where the PS work already
-    // fills their tails, and per-layer launches keep per-layer records.)
-    const int32_t launches = active + (small_ps > 0 ? 1 : 0);
+    // One launch per tensor with work, except: small PS tensors share one
+    // batched pass after the other PS launches; and without ready events the
+    // SFB layers without a momentum buffer share one grouped launch, at the
+    // place of the first of them in backpropagation order, whose single tile
+    // list lets one layer's last tiles (and a layer that is exactly one round
+    // of tiles, whose W epilogues would otherwise all run at once) overlap the
+    // next layer's (VGG19-22K iteration: 1.75 vs 1.78 ms, A/B in alternating
+    // processes).  With ready events every SFB layer keeps its own launch, so
+    // that each starts as soon as its own backward pass has run.
+    const bool group_sf = !ready && plain_sf > 1;
+    const int32_t launches = active - (group_sf ? plain_sf - 1 : 0) + (small_ps > 0 ? 1 : 0);
     if (pool->timing) {
         if (!reserve_timing(pool, launches))
             return POSEIDON_ERR_HIP;
@@ -236,6 +245,14 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         }
         return true;
     };
+    std::vector<SfTensor> grouped;   // in backpropagation order
+    if (group_sf)
+        for (int32_t t = count - 1; t >= 0; --t) {
+            const poseidon_tensor& x = tensors[t];
+            if (plan[static_cast<size_t>(t)] == POSEIDON_SFB && x.M * x.N > 0 && K > 0 && !x.buf)
+                grouped.push_back(SfTensor{x.W, x.U, x.V, x.M, x.N});
+        }
+    bool grouped_issued = false;
     std::vector<PsTensor> small;     // in backpropagation order
     std::vector<int32_t> small_idx;
     for (int32_t t = count - 1; t >= 0; --t) {
@@ -252,6 +269,17 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
             if (K == 0 && !x.buf)
                 continue;
             hipStream_t s = pool->streams[0];
+            if (group_sf && !x.buf) {
+                if (!grouped_issued) {
+                    grouped_issued = true;
+                    if (!timed(s, POSEIDON_SFB, -1, 0, [&] {
+                            return launch_sf_apply_batch(grouped.data(), static_cast<int32_t>(grouped.size()), K,
+                                                         lr, s);
+                        }))
+                        return POSEIDON_ERR_HIP;
+                }
+                continue;
+            }
             if (!timed(s, POSEIDON_SFB, t, 0, [&] {
                     return x.buf ? launch_sf_apply_momentum(x.W, x.buf, x.U, x.V, x.M, x.N, K, lr, momentum, s)
                                  : launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s);

@@ -159,3 +159,31 @@ def test_sync_iteration_launch_records():
     pool.set_timing(False)
     torch.cuda.synchronize()
     pool.close()
+
+
+def test_sync_iteration_groups_the_fc_layers_and_wfbp_does_not():
+    """Several SFB layers without a buffer share one grouped launch (record
+    tensor -1) in the plain iteration; with ready events each keeps its own
+    launch, in backprop order; the results are bit-identical."""
+    d = dev()
+    wl = I.workload(3)
+    host = I.make_tensors(wl)
+    a, b = _to_dev(host, d), _to_dev(host, d)
+    pool = api.StreamPool(2)
+    it_a = api.SyncIteration(pool, a, wl.B, wl.P, wl.lr, wl.momentum)
+    it_b = api.SyncIteration(pool, b, wl.B, wl.P, wl.lr, wl.momentum)
+    cs = torch.cuda.current_stream(d)
+    ev = torch.cuda.Event()
+    ev.record(cs)
+    pool.set_timing(True)
+    log("sync_iteration grouped FC launch")
+    it_a(cs)
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == [(api.SFB, -1, 0)]
+    it_b(cs, ready=[ev] * len(b))
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == \
+        [(api.SFB, i, 0) for i in reversed(range(len(b)))]
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    for x, y in zip(a, b):
+        assert torch.equal(x["W"], y["W"]), x["spec"].name
+    pool.close()
