@@ -23,10 +23,12 @@ Functions and the passages they follow:
   Alg. 1).
 * ``sync_iteration`` -- one node's synchronisation of every layer of a network
   for one iteration, layer by layer in backpropagation order (Sec. 3, Alg. 2).
-* ``kv_layout`` / ``KVStore`` -- the parameter server's KV store: parameters cut
-  into fixed-size KV pairs hashed equally over the servers, and one server's
-  per-pair arrival counts, applying a pair once every worker's update of it
-  has arrived (Sec. 4.1 "Coordinator", "KV Store", "Managing Consistency").
+* ``kv_layout`` / ``kv_pack`` / ``KVStore`` -- the parameter server's KV store:
+  parameters cut into fixed-size KV pairs hashed equally over the servers, a
+  worker's message to one server (its slices of that server's pairs), and one
+  server's per-pair arrival counts, applying a pair once every worker's update
+  of it has arrived (Sec. 4.1 "Coordinator", "KV Store", "Managing
+  Consistency").
 """
 from __future__ import annotations
 
@@ -345,6 +347,17 @@ def kv_layout(sizes, pair_elems: int, P: int):
     return pairs
 
 
+def kv_pack(grads, pair_elems: int, P: int, server: int) -> np.ndarray:
+    """The worker side of a push: one worker's updates of every tensor
+    (``grads[t]``, flat) cut as ``kv_layout`` cuts them, and the slices of the
+    pairs held by ``server`` concatenated in pair order -- the message that
+    worker sends to that server."""
+    grads = [_f32c(g).reshape(-1) for g in grads]
+    parts = [grads[t][off:off + length] for t, off, length, s in kv_layout([g.size for g in grads], pair_elems, P)
+             if s == server]
+    return np.concatenate(parts) if parts else np.zeros(0, np.float32)
+
+
 class KVStore:
     """One server's KV store over one iteration at a time (plain Python).
 
@@ -376,6 +389,22 @@ class KVStore:
     def ready(self, pair: int) -> bool:
         """The pair may be sent: every worker's update of it has been applied."""
         return self.count[pair] == self.P
+
+    def receive_message(self, worker: int, message) -> int:
+        """Worker ``worker``'s message (``kv_pack`` for this server) has
+        arrived: the same as receiving that worker's update of every tensor,
+        of which only this server's pairs are carried."""
+        message = _f32c(message).reshape(-1)
+        mine = [j for j, pr in enumerate(self.pairs) if pr[3] == self.rank]
+        if message.size != sum(self.pairs[j][2] for j in mine):
+            raise ValueError("message has the wrong size")
+        full = [np.zeros(w.size, np.float32) for w in self.W]
+        pos = 0
+        for j in mine:
+            t, off, length, _ = self.pairs[j]
+            full[t][off:off + length] = message[pos:pos + length]
+            pos += length
+        return sum(self.receive(worker, t, full[t]) for t in range(len(self.W)))
 
     def receive(self, worker: int, tensor: int, grad) -> int:
         if not 0 <= worker < self.P or not 0 <= tensor < len(self.W):

@@ -195,3 +195,33 @@ def test_kv_store_rejects_bad_deliveries():
         st.receive(1, 0, g[:7])             # wrong size
     with pytest.raises(ValueError):
         oracle.KVStore(t0, 4, 2, rank=2, lr=0.01, mu=0.9)
+
+
+def test_kv_messages_carry_every_parameter_once_and_feed_the_store():
+    """The P messages a worker sends (one per server) together hold each of its
+    update values exactly once; a server fed whole messages ends where per-tensor
+    receives end, bitwise."""
+    rng = np.random.default_rng(7)
+    sizes, pair, P = [37, 0, 100, 9], 16, 3
+    g = [rng.standard_normal(n).astype(np.float32) for n in sizes]
+    msgs = [oracle.kv_pack(g, pair, P, q) for q in range(P)]
+    flat = np.concatenate(g)
+    assert sum(m.size for m in msgs) == flat.size
+    assert np.array_equal(np.sort(np.concatenate(msgs)), np.sort(flat))
+    for q, m in enumerate(msgs):   # pair order: the q-th server's slices, concatenated
+        held = [g[t][o:o + l] for t, o, l, s in oracle.kv_layout(sizes, pair, P) if s == q]
+        assert np.array_equal(m, np.concatenate(held))
+    t0 = _tensors(rng, sizes)
+    grads = _grads(rng, sizes, P)
+    a = oracle.KVStore(t0, pair, P, rank=1, lr=0.01, mu=0.9)
+    b = oracle.KVStore(t0, pair, P, rank=1, lr=0.01, mu=0.9)
+    done = 0
+    for p in range(P):
+        done += a.receive_message(p, oracle.kv_pack(grads[p], pair, P, 1))
+        for t in range(len(sizes)):
+            b.receive(p, t, grads[p][t])
+    assert done == sum(1 for *_, s in a.pairs if s == 1)
+    assert all(np.array_equal(x, y) for x, y in zip(a.W, b.W))
+    assert all(np.array_equal(x, y) for x, y in zip(a.buf, b.buf))
+    with pytest.raises(ValueError):
+        a.receive_message(0, np.zeros(3, np.float32))
