@@ -261,6 +261,43 @@ int poseidon_kv_begin(poseidon_kv_store* store);
 int poseidon_kv_receive(poseidon_kv_store* store, int32_t worker, int32_t tensor, const float* grad,
                         hipStream_t stream);
 
+/*
+ * Worker `worker`'s message to this store has arrived: its slices of every
+ * pair this store holds, in pair order, concatenated (as poseidon_kv_pack
+ * makes it; poseidon_kv_message_size elements of device memory, caller-owned,
+ * not modified).  It stands for that worker's update of every tensor, as if
+ * poseidon_kv_receive had been called for each: every count of this store's
+ * pairs goes up by one, and each tensor whose pairs reach P is applied on
+ * `stream`, reading every worker's values where they arrived (a message or a
+ * whole-tensor update), summed in worker order.  The message must stay valid,
+ * and its data complete in the order of `stream`, until that work has run.
+ * Returns the number of pairs completed, or POSEIDON_ERR_INVALID_ARG (NULL
+ * store; worker out of range; NULL message when this store holds pairs; a
+ * message overlapping a W or buf; any update of this worker already received
+ * in this iteration -- nothing changes then) or POSEIDON_ERR_HIP.
+ */
+int poseidon_kv_receive_message(poseidon_kv_store* store, int32_t worker, const float* message,
+                                hipStream_t stream);
+
+/* The number of values in a message to this store (the total length of the
+ * pairs it holds).  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG. */
+int poseidon_kv_message_size(const poseidon_kv_store* store, int64_t* elems);
+
+/*
+ * The worker side of a push (Sec. 4.1 "KV Store"): one worker's updates of
+ * the `count` tensors (grads[t], sizes[t] values each, device memory), cut as
+ * poseidon_kv_layout(sizes, count, pair_elems, P) cuts them, and the slices of
+ * the pairs held by `server` copied one after another, in pair order, into
+ * `message` (device memory, capacity values) on `stream` -- the message that
+ * worker sends to that server.  *length receives the message's length;
+ * message == NULL with capacity 0 only queries it.  Returns POSEIDON_OK or
+ * POSEIDON_ERR_INVALID_ARG (bad layout arguments, server outside 0..P-1, NULL
+ * grads[t] with sizes[t] > 0, capacity too small, message overlapping an
+ * update) or POSEIDON_ERR_HIP.
+ */
+int poseidon_kv_pack(const int64_t* sizes, const float* const* grads, int32_t count, int64_t pair_elems, int32_t P,
+                     int32_t server, float* message, int64_t capacity, int64_t* length, hipStream_t stream);
+
 /* The store's count of pair `pair` (an index into its layout) in the current
  * iteration: the number of workers whose update of it has arrived, or 0 for
  * a pair held by another server.  A pair whose count equals P has been

@@ -28,7 +28,8 @@ EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply
            "poseidon_pool_set_timing",
            "poseidon_pool_launch_times", "poseidon_abi_version",
            "poseidon_kv_layout", "poseidon_kv_create", "poseidon_kv_destroy", "poseidon_kv_begin",
-           "poseidon_kv_receive", "poseidon_kv_pair_count")
+           "poseidon_kv_receive", "poseidon_kv_pair_count", "poseidon_kv_receive_message",
+           "poseidon_kv_message_size", "poseidon_kv_pack")
 
 
 class PoseidonTensor(ctypes.Structure):
@@ -107,6 +108,10 @@ def lib() -> ctypes.CDLL:
     L.poseidon_kv_begin.argtypes = [vp]
     L.poseidon_kv_receive.argtypes = [vp, i32, i32, vp, vp]
     L.poseidon_kv_pair_count.argtypes = [vp, i32, ctypes.POINTER(i32)]
+    L.poseidon_kv_receive_message.argtypes = [vp, i32, vp, vp]
+    L.poseidon_kv_message_size.argtypes = [vp, ctypes.POINTER(i64)]
+    L.poseidon_kv_pack.argtypes = [ctypes.POINTER(i64), ctypes.POINTER(vp), i32, i64, i32, i32, vp, i64,
+                                   ctypes.POINTER(i64), vp]
     for name in EXPORTS:
         getattr(L, name).restype = ctypes.c_int
     if L.poseidon_abi_version() != ABI_VERSION:

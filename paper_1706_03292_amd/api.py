@@ -335,6 +335,33 @@ def kv_layout(sizes, pair_elems: int, P: int) -> list[tuple[int, int, int, int]]
     return [(q.tensor, q.offset, q.length, q.server) for q in out[:n.value]]
 
 
+def kv_pack(grads: list, pair_elems: int, P: int, server: int, message: torch.Tensor | None = None,
+            stream=None) -> torch.Tensor:
+    """One worker's message to ``server`` (poseidon_kv_pack): its slices of
+    that server's pairs of the flat update tensors ``grads``, in pair order,
+    written into ``message`` (allocated when None) and returned."""
+    for g in grads:
+        _dev_f32("grad", g)
+    _same_device(*grads)
+    dev = grads[0].device if grads else torch.device("cuda", torch.cuda.current_device())
+    sizes = (ctypes.c_int64 * max(1, len(grads)))(*[g.numel() for g in grads])
+    ptrs = (ctypes.c_void_p * max(1, len(grads)))(*[g.data_ptr() for g in grads])
+    n = ctypes.c_int64()
+    h = _stream_handle(stream, dev)
+    with torch.cuda.device(dev):
+        _check("poseidon_kv_pack", L.lib().poseidon_kv_pack(sizes, ptrs, len(grads), int(pair_elems), int(P),
+                                                            int(server), None, 0, ctypes.byref(n), h))
+        if message is None:
+            message = torch.empty(n.value, dtype=torch.float32, device=dev)
+        _dev_f32("message", message)
+        if message.device != dev:
+            raise ValueError("message must be on the updates' device")
+        _check("poseidon_kv_pack", L.lib().poseidon_kv_pack(sizes, ptrs, len(grads), int(pair_elems), int(P),
+                                                            int(server), message.data_ptr(), message.numel(),
+                                                            ctypes.byref(n), h))
+    return message
+
+
 class KVStore:
     """Server ``rank``'s KV store over flat parameter tensors.
 
@@ -388,6 +415,26 @@ class KVStore:
                 self._h, int(worker), int(tensor), grad.data_ptr(), _stream_handle(stream, self.device)))
         self._grads[(worker, tensor)] = grad
         return done
+
+    def receive_message(self, worker: int, message: torch.Tensor, stream=None) -> int:
+        """Worker ``worker``'s message to this server (``kv_pack``) has arrived;
+        returns the number of pairs it completed."""
+        _dev_f32("message", message)
+        if message.numel() != self.message_size():
+            raise ValueError("message must have message_size() values")
+        if message.device != self.device:
+            raise ValueError("message must be on the store's device")
+        with torch.cuda.device(self.device):
+            done = _check("poseidon_kv_receive_message", L.lib().poseidon_kv_receive_message(
+                self._h, int(worker), message.data_ptr() if message.numel() else None,
+                _stream_handle(stream, self.device)))
+        self._grads[(worker, "message")] = message
+        return done
+
+    def message_size(self) -> int:
+        n = ctypes.c_int64()
+        _check("poseidon_kv_message_size", L.lib().poseidon_kv_message_size(self._h, ctypes.byref(n)))
+        return n.value
 
     def count(self, pair: int) -> int:
         c = ctypes.c_int32()

@@ -60,12 +60,21 @@ hipError_t launch_ps_apply_batch(const PsTensor* tensors, int32_t count, int32_t
                                  float momentum, hipStream_t stream);
 
 // KV-store apply of one tensor's pairs held by one server (arguments
-// validated; P <= KV_MAX_P; every range inside the tensor; grads[p] is worker
-// p's whole-tensor update).  Ranges beyond KV_MAX_RANGES take further launches.
+// validated; P <= KV_MAX_P; every range inside the tensor).  grads[p] is
+// worker p's whole-tensor update, or (bit p of msg_mask) its message, whose
+// values of range i sit deltas[i] elements past the tensor's indices.  Ranges
+// beyond KV_MAX_RANGES take further launches.
 constexpr int KV_MAX_P = 64;
 constexpr int KV_MAX_RANGES = 32;
-hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int32_t P, const int64_t* offsets,
-                           const int64_t* lengths, int32_t nranges, float lr, float momentum, hipStream_t stream);
+hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, uint64_t msg_mask, int32_t P,
+                           const int64_t* offsets, const int64_t* lengths, const int64_t* deltas, int32_t nranges,
+                           float lr, float momentum, hipStream_t stream);
+
+// A worker's message to one server: src[i][0 .. length[i]) copied to
+// message[dst[i] ..), in KV_PACK_MAX ranges per launch (arguments validated).
+constexpr int KV_PACK_MAX = 64;
+hipError_t launch_kv_pack(const float* const* src, const int64_t* dst, const int64_t* length, int32_t count,
+                          float* message, hipStream_t stream);
 
 // Argument checks of the public entry points (no device work).
 int check_sf_args(const float* W, const float* U, const float* V,

@@ -7,7 +7,11 @@
 // The bookkeeping (layout, counts, the update pointers) is host state, as in
 // the paper's KV store; the apply of a completed tensor's pairs is one kernel
 // launch on the stream of the receive that completed them, summing the P
-// workers' updates in worker order whatever the order they arrived in.
+// workers' updates in worker order whatever the order they arrived in.  An
+// update arrives either as a worker's whole tensor or inside the worker's
+// message to this server (poseidon_kv_pack: its slices of this server's
+// pairs, in pair order), and the apply reads each worker's values where they
+// are.
 #include <hip/hip_runtime.h>
 
 #include <vector>
@@ -25,6 +29,9 @@ struct poseidon_kv_store {
     std::vector<std::vector<int32_t>> owned;        // per tensor: this server's pairs
     std::vector<int32_t> count;                     // per pair, this iteration
     std::vector<std::vector<const float*>> grads;   // per tensor: worker p's update (or NULL)
+    std::vector<uint64_t> from_msg;                 // per tensor: bit p set when worker p's came in a message
+    std::vector<int64_t> msg_off;                   // per pair held here: its first element in a message
+    int64_t msg_len = 0;                            // elements of a message to this server
 };
 
 namespace {
@@ -42,6 +49,25 @@ int64_t count_pairs(const int64_t* sizes, int32_t count, int64_t pair_elems)
             return -1;
     }
     return total;
+}
+
+// Enqueue the apply of tensor t's pairs held by the store (their counts have
+// reached P).
+hipError_t apply_tensor(poseidon_kv_store* st, int32_t t, hipStream_t stream)
+{
+    const poseidon_kv_tensor& x = st->tensors[static_cast<size_t>(t)];
+    const std::vector<int32_t>& mine = st->owned[static_cast<size_t>(t)];
+    std::vector<int64_t> off, len, delta;
+    for (int32_t j : mine) {
+        const poseidon_kv_pair& q = st->pairs[static_cast<size_t>(j)];
+        off.push_back(q.offset);
+        len.push_back(q.length);
+        delta.push_back(st->msg_off[static_cast<size_t>(j)] - q.offset);
+    }
+    return poseidon::launch_kv_apply(x.W, x.buf, st->grads[static_cast<size_t>(t)].data(),
+                                     st->from_msg[static_cast<size_t>(t)], st->P, off.data(), len.data(),
+                                     delta.data(), static_cast<int32_t>(mine.size()), st->lr,
+                                     x.buf ? st->mu : 0.0f, stream);
 }
 
 void fill_layout(const int64_t* sizes, int32_t count, int64_t pair_elems, int32_t P, poseidon_kv_pair* out)
@@ -114,6 +140,13 @@ extern "C" int poseidon_kv_create(const poseidon_kv_tensor* tensors, int32_t cou
             st->owned[static_cast<size_t>(st->pairs[static_cast<size_t>(j)].tensor)].push_back(j);
     st->count.assign(static_cast<size_t>(total), 0);
     st->grads.assign(static_cast<size_t>(count), std::vector<const float*>(static_cast<size_t>(P), nullptr));
+    st->from_msg.assign(static_cast<size_t>(count), 0);
+    st->msg_off.assign(static_cast<size_t>(total), 0);
+    for (int32_t j = 0; j < static_cast<int32_t>(total); ++j)
+        if (st->pairs[static_cast<size_t>(j)].server == rank) {
+            st->msg_off[static_cast<size_t>(j)] = st->msg_len;
+            st->msg_len += st->pairs[static_cast<size_t>(j)].length;
+        }
     *out = st;
     return POSEIDON_OK;
 }
@@ -133,6 +166,8 @@ extern "C" int poseidon_kv_begin(poseidon_kv_store* store)
     for (auto& g : store->grads)
         for (const float*& p : g)
             p = nullptr;
+    for (uint64_t& m : store->from_msg)
+        m = 0;
     return POSEIDON_OK;
 }
 
@@ -165,17 +200,96 @@ extern "C" int poseidon_kv_receive(poseidon_kv_store* store, int32_t worker, int
         complete = ++store->count[static_cast<size_t>(j)] == store->P && complete;
     if (!complete)
         return 0;
-    std::vector<int64_t> off, len;
-    for (int32_t j : mine) {
-        off.push_back(store->pairs[static_cast<size_t>(j)].offset);
-        len.push_back(store->pairs[static_cast<size_t>(j)].length);
-    }
-    const hipError_t e = poseidon::launch_kv_apply(x.W, x.buf, g.data(), store->P, off.data(), len.data(),
-                                                   static_cast<int32_t>(mine.size()), store->lr,
-                                                   x.buf ? store->mu : 0.0f, stream);
-    if (e != hipSuccess)
+    if (apply_tensor(store, tensor, stream) != hipSuccess)
         return POSEIDON_ERR_HIP;
     return static_cast<int32_t>(mine.size());
+}
+
+extern "C" int poseidon_kv_receive_message(poseidon_kv_store* store, int32_t worker, const float* message,
+                                           hipStream_t stream)
+{
+    using poseidon::overlaps;
+    if (!store || worker < 0 || worker >= store->P || (store->msg_len > 0 && !message))
+        return POSEIDON_ERR_INVALID_ARG;
+    const size_t T = store->tensors.size();
+    for (size_t t = 0; t < T; ++t) {   // nothing of this worker's may have arrived yet this iteration
+        const poseidon_kv_tensor& x = store->tensors[t];
+        if (store->grads[t][static_cast<size_t>(worker)] != nullptr ||
+            overlaps(message, store->msg_len * 4, x.W, x.n * 4) || overlaps(message, store->msg_len * 4, x.buf, x.n * 4))
+            return POSEIDON_ERR_INVALID_ARG;
+    }
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess)
+        return POSEIDON_ERR_HIP;
+    if (dev != store->device)
+        return POSEIDON_ERR_INVALID_ARG;
+    int32_t done = 0;
+    for (size_t t = 0; t < T; ++t) {
+        const poseidon_kv_tensor& x = store->tensors[t];
+        // The message stands for this worker's update of every tensor; a
+        // tensor with no pair here is recorded with a marker (never read).
+        const bool held = !store->owned[t].empty();
+        store->grads[t][static_cast<size_t>(worker)] = held ? message : reinterpret_cast<const float*>(&x);
+        if (!held)
+            continue;
+        store->from_msg[t] |= uint64_t{1} << worker;
+        bool complete = true;
+        for (int32_t j : store->owned[t])
+            complete = ++store->count[static_cast<size_t>(j)] == store->P && complete;
+        if (complete) {
+            if (apply_tensor(store, static_cast<int32_t>(t), stream) != hipSuccess)
+                return POSEIDON_ERR_HIP;
+            done += static_cast<int32_t>(store->owned[t].size());
+        }
+    }
+    return done;
+}
+
+extern "C" int poseidon_kv_message_size(const poseidon_kv_store* store, int64_t* elems)
+{
+    if (!store || !elems)
+        return POSEIDON_ERR_INVALID_ARG;
+    *elems = store->msg_len;
+    return POSEIDON_OK;
+}
+
+extern "C" int poseidon_kv_pack(const int64_t* sizes, const float* const* grads, int32_t count, int64_t pair_elems,
+                                int32_t P, int32_t server, float* message, int64_t capacity, int64_t* length,
+                                hipStream_t stream)
+{
+    using poseidon::overlaps;
+    if (!length || count < 0 || (count > 0 && (!sizes || !grads)) || pair_elems < 1 || P < 1 || server < 0 ||
+        server >= P || capacity < 0)
+        return POSEIDON_ERR_INVALID_ARG;
+    const int64_t total = count_pairs(sizes, count, pair_elems);
+    if (total < 0)
+        return POSEIDON_ERR_INVALID_ARG;
+    std::vector<poseidon_kv_pair> pairs(static_cast<size_t>(total));
+    fill_layout(sizes, count, pair_elems, P, pairs.data());
+    std::vector<const float*> src;
+    std::vector<int64_t> dst, len;
+    int64_t n = 0;
+    for (const poseidon_kv_pair& q : pairs)
+        if (q.server == server) {
+            src.push_back(grads[q.tensor] + q.offset);
+            dst.push_back(n);
+            len.push_back(q.length);
+            n += q.length;
+        }
+    *length = n;
+    if (message == nullptr && capacity == 0)
+        return POSEIDON_OK;                       // size query
+    if (capacity < n || (n > 0 && !message))
+        return POSEIDON_ERR_INVALID_ARG;
+    for (int32_t t = 0; t < count; ++t)
+        if (sizes[t] > 0 && (!grads[t] || overlaps(message, n * 4, grads[t], sizes[t] * 4)))
+            return POSEIDON_ERR_INVALID_ARG;
+    if (n == 0)
+        return POSEIDON_OK;
+    return poseidon::launch_kv_pack(src.data(), dst.data(), len.data(), static_cast<int32_t>(src.size()), message,
+                                    stream) == hipSuccess
+               ? POSEIDON_OK
+               : POSEIDON_ERR_HIP;
 }
 
 extern "C" int poseidon_kv_pair_count(const poseidon_kv_store* store, int32_t pair, int32_t* count)

@@ -68,10 +68,14 @@ struct Contiguous {
     __device__ const float* operator()(int p) const { return G + static_cast<int64_t>(p) * n; }
 };
 
-// ... or one pointer per worker (the KV store).
+// ... or one pointer per worker (the KV store): a whole-tensor update, or a
+// message whose values for this range sit `delta` elements further on (bit p
+// of msg_mask set).
 struct PerWorker {
     const float* const* g;
-    __device__ const float* operator()(int p) const { return g[p]; }
+    uint64_t msg_mask;
+    int64_t delta;
+    __device__ const float* operator()(int p) const { return g[p] + (((msg_mask >> p) & 1) ? delta : 0); }
 };
 
 // Sum of the P values of elements e .. e+3, in increasing p.
@@ -262,12 +266,14 @@ void launch_batch_mom(const PsBatchArgs& a, int blocks, int grid, int32_t P, flo
 struct KvRange {
     int64_t offset;
     int64_t length;
+    int64_t delta;       // a message's values of element e are at message + delta + e
     int32_t first_block;
     int32_t pad;
 };
 
 struct KvArgs {
     const float* g[KV_MAX_P];
+    uint64_t msg_mask;                    // bit p: worker p's pointer is a message
     int32_t first_block[KV_MAX_RANGES];   // r[k].first_block, contiguous (as in the batched kernel)
     KvRange r[KV_MAX_RANGES];
     int32_t nranges;
@@ -285,8 +291,43 @@ __global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, in
     const int64_t j = static_cast<int64_t>(b - a.r[r].first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
     if (j >= a.r[r].length)
         return;
-    const PerWorker src{a.g};
+    const PerWorker src{a.g, a.msg_mask, a.r[r].delta};
     apply_group<PT, MOM, AL>(W, buf, src, P, a.r[r].offset + j, a.r[r].offset + a.r[r].length, lr, mu);
+}
+
+// ---------------------------------------------------------------------------
+// KV-store message: the slices [src_k, src_k + length_k) of one worker's
+// updates copied one after another into its message (range k starts at
+// element dst_k).  Each one-wave workgroup copies PS_BLOCK_ELEMS elements of
+// one range, 16 bytes per thread.
+// ---------------------------------------------------------------------------
+struct PackArgs {
+    const float* src[KV_PACK_MAX];
+    int64_t dst[KV_PACK_MAX];
+    int64_t length[KV_PACK_MAX];
+    int32_t first_block[KV_PACK_MAX];
+    int32_t count;
+};
+
+__global__ __launch_bounds__(PS_THREADS) void kv_pack_kernel(const PackArgs a, float* __restrict__ message)
+{
+    const int b = blockIdx.x;
+    int k = 0;
+#pragma unroll
+    for (int q = 1; q < KV_PACK_MAX; ++q)
+        k += (q < a.count && a.first_block[q] <= b) ? 1 : 0;
+    const int64_t j = static_cast<int64_t>(b - a.first_block[k]) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
+    const int64_t len = a.length[k];
+    if (j >= len)
+        return;
+    const float* __restrict__ src = a.src[k] + j;
+    float* __restrict__ dst = message + a.dst[k] + j;
+    if (j + 3 < len) {
+        st4<false>(dst, ld4<false>(src));
+    } else {
+        for (int64_t q = 0; q < len - j; ++q)
+            dst[q] = src[q];
+    }
 }
 
 template <bool MOM, bool AL>
@@ -362,23 +403,26 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
     return hipSuccess;
 }
 
-hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int32_t P, const int64_t* offsets,
-                           const int64_t* lengths, int32_t nranges, float lr, float momentum, hipStream_t stream)
+hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, uint64_t msg_mask, int32_t P,
+                           const int64_t* offsets, const int64_t* lengths, const int64_t* deltas, int32_t nranges,
+                           float lr, float momentum, hipStream_t stream)
 {
     bool al = aligned16(W) && (!buf || aligned16(buf));
     for (int32_t p = 0; p < P; ++p)
         al = al && aligned16(grads[p]);
     for (int32_t i = 0; i < nranges; ++i)
-        al = al && offsets[i] % 4 == 0;
+        al = al && offsets[i] % 4 == 0 && (msg_mask == 0 || deltas[i] % 4 == 0);
     for (int32_t i0 = 0; i0 < nranges; i0 += KV_MAX_RANGES) {
         KvArgs a{};
         for (int32_t p = 0; p < P; ++p)
             a.g[p] = grads[p];
+        a.msg_mask = msg_mask;
         int64_t blocks = 0;
         for (int32_t i = i0; i < nranges && i < i0 + KV_MAX_RANGES; ++i) {
             KvRange& r = a.r[a.nranges++];
             r.offset = offsets[i];
             r.length = lengths[i];
+            r.delta = deltas[i];
             r.first_block = static_cast<int32_t>(blocks);
             a.first_block[a.nranges - 1] = r.first_block;
             blocks += (lengths[i] + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
@@ -399,6 +443,32 @@ hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, int3
             else
                 launch_kv_al<false, false>(a, grid, P, W, nullptr, lr, 0.0f, stream);
         }
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_kv_pack(const float* const* src, const int64_t* dst, const int64_t* length, int32_t count,
+                          float* message, hipStream_t stream)
+{
+    for (int32_t i0 = 0; i0 < count; i0 += KV_PACK_MAX) {
+        PackArgs a{};
+        int64_t blocks = 0;
+        for (int32_t i = i0; i < count && i < i0 + KV_PACK_MAX; ++i) {
+            const int32_t k = a.count++;
+            a.src[k] = src[i];
+            a.dst[k] = dst[i];
+            a.length[k] = length[i];
+            a.first_block[k] = static_cast<int32_t>(blocks);
+            blocks += (length[i] + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
+            if (blocks > INT32_MAX)
+                return hipErrorInvalidValue;
+        }
+        if (blocks == 0)
+            continue;
+        kv_pack_kernel<<<static_cast<int>(blocks), PS_THREADS, 0, stream>>>(a, message);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;

@@ -199,3 +199,59 @@ def test_kv_store_vgg19_22k_server_share_full_size_sampled():
         else:
             assert np.array_equal(got, tens[t][0].numpy()[idx])
     st.close()
+
+
+@pytest.mark.parametrize("sizes,pair,P", [([1000, 17, 4, 333, 4096, 0, 2049], 256, 4), ([5000, 123, 7], 250, 3)])
+def test_kv_pack_matches_oracle_bitwise(sizes, pair, P):
+    d = dev()
+    g = [I.randn(1700 + t, (n,), 1e-3) for t, n in enumerate(sizes)]
+    dg = [x.to(d) for x in g]
+    log(f"kv_pack sizes={sizes} pair={pair} P={P}")
+    for q in range(P):
+        msg = api.kv_pack(dg, pair, P, q)
+        torch.cuda.synchronize()
+        ref = oracle.kv_pack([x.numpy() for x in g], pair, P, q)
+        assert msg.numel() == ref.size
+        assert np.array_equal(to_np(msg), ref)
+
+
+@pytest.mark.parametrize("pair", [256, 250])
+def test_kv_messages_equal_per_tensor_receives_bitwise(pair):
+    """A store fed messages from every worker, one fed whole tensors, and one
+    fed a mix (workers alternate) end bit-identical; all match the oracle."""
+    d = dev()
+    sizes, P, rank = [1000, 17, 4, 333, 4096, 0, 2049], 4, 1
+    tens, grads = _case(sizes, P, seed=1900)
+    stores, devs = [], []
+    for mode in ("message", "tensor", "mixed"):
+        dt, dg = _to_dev(tens, grads, d)
+        st = api.KVStore(dt, pair, P, rank, LR, MU)
+        log(f"kv_store receive by {mode}, pair={pair}")
+        done = 0
+        for p in range(P):
+            if mode == "message" or (mode == "mixed" and p % 2 == 0):
+                done += st.receive_message(p, api.kv_pack(dg[p], pair, P, rank))
+            else:
+                done += sum(st.receive(p, t, dg[p][t]) for t in range(len(sizes)))
+        assert done == sum(1 for *_, s in st.pairs if s == rank)
+        stores.append(st)
+        devs.append(dt)
+    torch.cuda.synchronize()
+    ref = oracle.KVStore([(W.numpy(), b.numpy()) for W, b in tens], pair, P, rank, LR, MU)
+    for p in range(P):
+        ref.receive_message(p, oracle.kv_pack([g.numpy() for g in grads[p]], pair, P, rank))
+    for t in range(len(sizes)):
+        for dt in devs[1:]:
+            assert torch.equal(devs[0][t][0], dt[t][0]) and torch.equal(devs[0][t][1], dt[t][1])
+        assert_close(to_np(devs[0][t][0]), ref.W[t], W_TOL, f"W {t}")
+        assert_close(to_np(devs[0][t][1]), ref.buf[t], BUF_TOL, f"buf {t}")
+    # a worker's message after one of its per-tensor updates is refused
+    st = stores[1]
+    st.begin()
+    st.receive(0, 0, _to_dev(tens, grads, d)[1][0][0])
+    with pytest.raises(api.PoseidonError):
+        st.receive_message(0, torch.zeros(st.message_size(), device=d))
+    with pytest.raises(ValueError):
+        st.receive_message(1, torch.zeros(st.message_size() + 1, device=d))
+    for s_ in stores:
+        s_.close()

@@ -65,3 +65,24 @@ def test_kv_store_argument_checks_before_device_work():
     assert lib.poseidon_kv_receive(None, 0, 0, None, None) == L.ERR_INVALID_ARG
     c = ctypes.c_int32()
     assert lib.poseidon_kv_pair_count(None, 0, ctypes.byref(c)) == L.ERR_INVALID_ARG
+
+
+def test_kv_pack_size_query_and_argument_checks():
+    lib = L.lib()
+    sizes_l = [37, 0, 100, 9]
+    sizes = (ctypes.c_int64 * 4)(*sizes_l)
+    fake = (ctypes.c_void_p * 4)(0x100000, None, 0x200000, 0x300000)
+    n = ctypes.c_int64(-1)
+    for q in range(3):
+        assert lib.poseidon_kv_pack(sizes, fake, 4, 16, 3, q, None, 0, ctypes.byref(n), None) == L.OK
+        assert n.value == sum(l for _, _, l, s in oracle.kv_layout(sizes_l, 16, 3) if s == q)
+    assert lib.poseidon_kv_pack(sizes, fake, 4, 16, 3, 3, None, 0, ctypes.byref(n), None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_kv_pack(sizes, fake, 4, 0, 3, 0, None, 0, ctypes.byref(n), None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_kv_pack(sizes, fake, 4, 16, 3, 0, None, 0, None, None) == L.ERR_INVALID_ARG
+    # capacity too small, and a message overlapping an update: refused before any launch
+    assert lib.poseidon_kv_pack(sizes, fake, 4, 16, 3, 0, ctypes.c_void_p(0x900000), 5, ctypes.byref(n),
+                                None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_kv_pack(sizes, fake, 4, 16, 3, 0, ctypes.c_void_p(0x100004), 1000, ctypes.byref(n),
+                                None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_kv_receive_message(None, 0, None, None) == L.ERR_INVALID_ARG
+    assert lib.poseidon_kv_message_size(None, ctypes.byref(n)) == L.ERR_INVALID_ARG
