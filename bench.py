@@ -330,10 +330,11 @@ def _ps_phase(wl, devt, schemes, launch_ms, time_fn, stream, pool, ksteps):
 
 
 def _kv_phase(wl, devt, time_fn, stream, ksteps):
-    """One node's server role through the KV store: the PS tensors cut into
-    2 MB pairs hashed over the P servers; server 0 receives all P workers'
-    updates of every tensor (worker p's update = shard p) and applies its
-    pairs as they complete."""
+    """One node's roles through the KV store: the PS tensors cut into 2 MB
+    pairs hashed over the P servers.  Server 0 receives every worker's
+    message (its slices of server 0's pairs; worker p's update = shard p) and
+    applies its pairs as they complete; the worker side packs one worker's
+    updates into its P messages, one per server."""
     from paper_1706_03292_amd import api
     import torch
     pair_elems = (2 << 20) // 4
@@ -343,45 +344,64 @@ def _kv_phase(wl, devt, time_fn, stream, ksteps):
     kv_elems = sum(l for _, l in owned)
     kv_bytes = float(kv_elems) * (4 * wl.P + 16)
     rows = [t["shards"].view(wl.P, -1) for t in kv_t]
+    msgs = [api.kv_pack([r[p] for r in rows], pair_elems, wl.P, 0, stream=stream) for p in range(wl.P)]
+    torch.cuda.synchronize()
 
     def one_iteration():
         store.begin()
         for p in range(wl.P):
-            for t in range(len(kv_t)):
-                store.receive(p, t, rows[t][p], stream=stream)
+            store.receive_message(p, msgs[p], stream=stream)
 
     it_ms = time_fn(one_iteration)
-    # The apply launches alone: the last worker's receives (which enqueue every
-    # apply) are issued while the stream is held by a ~1 ms device-side wait,
-    # so the events around them time the launches back to back, not the host.
+    # The apply launches alone: the last worker's message (its receive
+    # enqueues every apply) is received while the stream is held by a ~1 ms
+    # device-side wait, so the events around it time the launches back to
+    # back, not the host.
     apply = []
     for _ in range(ksteps):
         store.begin()
         for p in range(wl.P - 1):
-            for t in range(len(kv_t)):
-                store.receive(p, t, rows[t][p], stream=stream)
+            store.receive_message(p, msgs[p], stream=stream)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         with torch.cuda.stream(stream):
             torch.cuda._sleep(2_000_000)
         a.record(stream)
-        for t in range(len(kv_t)):
-            store.receive(wl.P - 1, t, rows[t][wl.P - 1], stream=stream)
+        store.receive_message(wl.P - 1, msgs[wl.P - 1], stream=stream)
         b.record(stream)
         torch.cuda.synchronize()
         apply.append(a.elapsed_time(b))
     apply_ms = sum(apply) / len(apply)
+    # The worker side: worker 0 packs its updates into its P messages (all
+    # servers' messages in one pass).
+    mine = [r[0] for r in rows]
+    out = api.kv_pack(mine, pair_elems, wl.P, -1, stream=stream)
+    pack = []
+    for _ in range(ksteps):          # queued behind a device-side wait, as for apply_ms
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(2_000_000)
+        a.record(stream)
+        api.kv_pack(mine, pair_elems, wl.P, -1, message=out, stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        pack.append(a.elapsed_time(b))
+    pack_ms = sum(pack) / len(pack)
+    pack_bytes = 8.0 * sum(r.shape[1] for r in rows)          # every value read once and written once
     npairs = len(store.pairs)
     store.close()
     return {
         "what": f"server 0 of {wl.P}: its {len(owned)} of {npairs} KV pairs (2 MB) of the {len(kv_t)} PS tensors, "
-                f"{kv_elems} elements, {(4 * wl.P + 16)} bytes each",
+                f"{kv_elems} elements, {(4 * wl.P + 16)} bytes each, received as {wl.P} messages",
         "bytes": kv_bytes,
         "iteration_ms": round(it_ms, 4),
         "apply_ms": round(apply_ms, 4),
         "apply_gbs": round(kv_bytes / apply_ms / 1e6, 1) if apply_ms else None,
-        "note": "iteration_ms: begin plus all P x tensors receives on one stream, paced by the host's calls; "
-                "apply_ms: HIP events around the last worker's receives, which enqueue every apply, queued "
-                "behind a device-side wait so that the applies run back to back"}
+        "pack_ms": round(pack_ms, 4),
+        "pack_gbs": round(pack_bytes / pack_ms / 1e6, 1) if pack_ms else None,
+        "note": "iteration_ms: begin plus the P message receives on one stream (the applies included); apply_ms: "
+                "HIP events around the last worker's receive, which enqueues every apply, queued behind a "
+                "device-side wait so that the applies run back to back; pack_ms: one worker's P messages "
+                "in one pass (each of its PS update values read and written once), queued the same way"}
 
 
 def main():

@@ -289,9 +289,11 @@ int poseidon_kv_message_size(const poseidon_kv_store* store, int64_t* elems);
  * poseidon_kv_layout(sizes, count, pair_elems, P) cuts them, and the slices of
  * the pairs held by `server` copied one after another, in pair order, into
  * `message` (device memory, capacity values) on `stream` -- the message that
- * worker sends to that server.  *length receives the message's length;
- * message == NULL with capacity 0 only queries it.  Returns POSEIDON_OK or
- * POSEIDON_ERR_INVALID_ARG (bad layout arguments, server outside 0..P-1, NULL
+ * worker sends to that server.  server == -1 writes every server's message,
+ * one after another in server order, in one pass.  *length receives the
+ * length written; message == NULL with capacity 0 only queries it.  Returns
+ * POSEIDON_OK or POSEIDON_ERR_INVALID_ARG (bad layout arguments, server
+ * outside -1..P-1, NULL
  * grads[t] with sizes[t] > 0, capacity too small, message overlapping an
  * update) or POSEIDON_ERR_HIP.
  */

@@ -339,7 +339,8 @@ def kv_pack(grads: list, pair_elems: int, P: int, server: int, message: torch.Te
             stream=None) -> torch.Tensor:
     """One worker's message to ``server`` (poseidon_kv_pack): its slices of
     that server's pairs of the flat update tensors ``grads``, in pair order,
-    written into ``message`` (allocated when None) and returned."""
+    written into ``message`` (allocated when None) and returned.  server = -1
+    gives every server's message, one after another in server order."""
     for g in grads:
         _dev_f32("grad", g)
     _same_device(*grads)

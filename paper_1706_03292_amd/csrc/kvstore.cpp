@@ -258,7 +258,7 @@ extern "C" int poseidon_kv_pack(const int64_t* sizes, const float* const* grads,
                                 hipStream_t stream)
 {
     using poseidon::overlaps;
-    if (!length || count < 0 || (count > 0 && (!sizes || !grads)) || pair_elems < 1 || P < 1 || server < 0 ||
+    if (!length || count < 0 || (count > 0 && (!sizes || !grads)) || pair_elems < 1 || P < 1 || server < -1 ||
         server >= P || capacity < 0)
         return POSEIDON_ERR_INVALID_ARG;
     const int64_t total = count_pairs(sizes, count, pair_elems);
@@ -269,13 +269,14 @@ extern "C" int poseidon_kv_pack(const int64_t* sizes, const float* const* grads,
     std::vector<const float*> src;
     std::vector<int64_t> dst, len;
     int64_t n = 0;
-    for (const poseidon_kv_pair& q : pairs)
-        if (q.server == server) {
-            src.push_back(grads[q.tensor] + q.offset);
-            dst.push_back(n);
-            len.push_back(q.length);
-            n += q.length;
-        }
+    for (int32_t to = (server < 0 ? 0 : server); to <= (server < 0 ? P - 1 : server); ++to)
+        for (const poseidon_kv_pair& q : pairs)
+            if (q.server == to) {
+                src.push_back(grads[q.tensor] + q.offset);
+                dst.push_back(n);
+                len.push_back(q.length);
+                n += q.length;
+            }
     *length = n;
     if (message == nullptr && capacity == 0)
         return POSEIDON_OK;                       // size query

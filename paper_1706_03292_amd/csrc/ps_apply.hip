@@ -298,9 +298,13 @@ __global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, in
 // ---------------------------------------------------------------------------
 // KV-store message: the slices [src_k, src_k + length_k) of one worker's
 // updates copied one after another into its message (range k starts at
-// element dst_k).  Each one-wave workgroup copies PS_BLOCK_ELEMS elements of
-// one range, 16 bytes per thread.
+// element dst_k).  Each one-wave workgroup copies PACK_BLOCK_ELEMS elements of
+// one range: four 16-byte groups per thread, all loads issued before the
+// stores (a copy moves few bytes per thread otherwise).
 // ---------------------------------------------------------------------------
+constexpr int PACK_UNROLL = 4;
+constexpr int PACK_BLOCK_ELEMS = PACK_UNROLL * PS_BLOCK_ELEMS;
+
 struct PackArgs {
     const float* src[KV_PACK_MAX];
     int64_t dst[KV_PACK_MAX];
@@ -316,17 +320,26 @@ __global__ __launch_bounds__(PS_THREADS) void kv_pack_kernel(const PackArgs a, f
 #pragma unroll
     for (int q = 1; q < KV_PACK_MAX; ++q)
         k += (q < a.count && a.first_block[q] <= b) ? 1 : 0;
-    const int64_t j = static_cast<int64_t>(b - a.first_block[k]) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
+    const int64_t j0 = static_cast<int64_t>(b - a.first_block[k]) * PACK_BLOCK_ELEMS + 4 * threadIdx.x;
     const int64_t len = a.length[k];
-    if (j >= len)
-        return;
-    const float* __restrict__ src = a.src[k] + j;
-    float* __restrict__ dst = message + a.dst[k] + j;
-    if (j + 3 < len) {
-        st4<false>(dst, ld4<false>(src));
-    } else {
-        for (int64_t q = 0; q < len - j; ++q)
-            dst[q] = src[q];
+    const float* __restrict__ src = a.src[k];
+    float* __restrict__ dst = message + a.dst[k];
+    f4 v[PACK_UNROLL];
+#pragma unroll
+    for (int u = 0; u < PACK_UNROLL; ++u) {
+        const int64_t j = j0 + u * PS_BLOCK_ELEMS;
+        if (j + 3 < len)
+            v[u] = ld4<false>(src + j);
+    }
+#pragma unroll
+    for (int u = 0; u < PACK_UNROLL; ++u) {
+        const int64_t j = j0 + u * PS_BLOCK_ELEMS;
+        if (j + 3 < len) {
+            st4<false>(dst + j, v[u]);
+        } else {
+            for (int64_t q = j; q < len; ++q)
+                dst[q] = src[q];
+        }
     }
 }
 
@@ -462,7 +475,7 @@ hipError_t launch_kv_pack(const float* const* src, const int64_t* dst, const int
             a.dst[k] = dst[i];
             a.length[k] = length[i];
             a.first_block[k] = static_cast<int32_t>(blocks);
-            blocks += (length[i] + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
+            blocks += (length[i] + PACK_BLOCK_ELEMS - 1) / PACK_BLOCK_ELEMS;
             if (blocks > INT32_MAX)
                 return hipErrorInvalidValue;
         }

@@ -255,3 +255,15 @@ def test_kv_messages_equal_per_tensor_receives_bitwise(pair):
         st.receive_message(1, torch.zeros(st.message_size() + 1, device=d))
     for s_ in stores:
         s_.close()
+
+
+def test_kv_pack_every_server_in_one_pass():
+    d = dev()
+    sizes, pair, P = [1000, 17, 4, 333, 4096, 0, 2049], 256, 4
+    g = [I.randn(1800 + t, (n,), 1e-3) for t, n in enumerate(sizes)]
+    dg = [x.to(d) for x in g]
+    log("kv_pack all servers")
+    allm = api.kv_pack(dg, pair, P, -1)
+    torch.cuda.synchronize()
+    ref = np.concatenate([oracle.kv_pack([x.numpy() for x in g], pair, P, q) for q in range(P)])
+    assert np.array_equal(to_np(allm), ref)
