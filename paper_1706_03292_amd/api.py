@@ -48,6 +48,17 @@ def _stream_handle(stream, device) -> int:
     return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
 
 
+def _uses(stream, *tensors) -> None:
+    """Tell torch's caching allocator that work on ``stream`` (a
+    torch.cuda.Stream) reads or writes these tensors, so that their memory is
+    not handed out again before that work has run.  With a raw stream handle
+    the caller keeps the tensors alive instead."""
+    if isinstance(stream, torch.cuda.Stream):
+        for t in tensors:
+            if t is not None:
+                t.record_stream(stream)
+
+
 def _same_device(*ts):
     devs = {t.device for t in ts if t is not None}
     if len(devs) > 1:
@@ -68,6 +79,7 @@ def sf_apply(W: torch.Tensor, U: torch.Tensor, V: torch.Tensor, lr: float, strea
     K = U.shape[0]
     if U.shape != (K, M) or V.shape != (K, N):
         raise ValueError(f"shapes: W {tuple(W.shape)}, U {tuple(U.shape)}, V {tuple(V.shape)}")
+    _uses(stream, W, U, V)
     with torch.cuda.device(W.device):
         _check("poseidon_sf_apply", L.lib().poseidon_sf_apply(
             W.data_ptr(), U.data_ptr(), V.data_ptr(), M, N, K, float(lr),
@@ -87,6 +99,7 @@ def sf_apply_momentum(W: torch.Tensor, buf: torch.Tensor, U: torch.Tensor, V: to
     if U.shape != (K, M) or V.shape != (K, N) or buf.numel() != M * N:
         raise ValueError(f"shapes: W {tuple(W.shape)}, buf {tuple(buf.shape)}, U {tuple(U.shape)}, "
                          f"V {tuple(V.shape)}")
+    _uses(stream, W, buf, U, V)
     with torch.cuda.device(W.device):
         _check("poseidon_sf_apply_momentum", L.lib().poseidon_sf_apply_momentum(
             W.data_ptr(), buf.data_ptr(), U.data_ptr(), V.data_ptr(), M, N, K, float(lr), float(momentum),
@@ -115,6 +128,7 @@ def sf_apply_batch(layers: list, lr: float, stream=None) -> None:
         if k != K or U.shape != (K, M) or V.shape != (K, N):
             raise ValueError(f"layer {i}: U must be {K} x {M} and V {K} x {N}")
         arr[i] = L.PoseidonSfTensor(W.data_ptr(), U.data_ptr(), V.data_ptr(), M, N)
+    _uses(stream, *[x for layer in layers for x in layer])
     with torch.cuda.device(dev):
         _check("poseidon_sf_apply_batch", L.lib().poseidon_sf_apply_batch(
             arr, len(layers), K, float(lr), _stream_handle(stream, dev)))
@@ -133,6 +147,7 @@ def ps_apply(W: torch.Tensor, shards: torch.Tensor, lr: float, momentum: float =
     P = shards.shape[0] if shards.dim() >= 1 else 0
     if shards.numel() != P * n or (buf is not None and buf.numel() != n):
         raise ValueError(f"shards must be P x {n} and buf must have {n} values")
+    _uses(stream, W, shards, buf)
     with torch.cuda.device(W.device):
         _check("poseidon_ps_apply", L.lib().poseidon_ps_apply(
             W.data_ptr(), shards.data_ptr(), P, n, float(lr), float(momentum),
@@ -165,6 +180,7 @@ def ps_apply_batch(tensors: list, lr: float, momentum: float = 0.0, stream=None)
         if p != P or shards.numel() != P * n or (buf is not None and buf.numel() != n):
             raise ValueError(f"tensor {i}: shards must be {P} x {n} and buf must have {n} values")
         arr[i] = L.PoseidonPsTensor(W.data_ptr(), shards.data_ptr(), buf.data_ptr() if buf is not None else None, n)
+    _uses(stream, *[x for t in tensors for x in t])
     with torch.cuda.device(dev):
         _check("poseidon_ps_apply_batch", L.lib().poseidon_ps_apply_batch(
             arr, len(tensors), P, float(lr), float(momentum), _stream_handle(stream, dev)))
@@ -357,6 +373,7 @@ def kv_pack(grads: list, pair_elems: int, P: int, server: int, message: torch.Te
         _dev_f32("message", message)
         if message.device != dev:
             raise ValueError("message must be on the updates' device")
+        _uses(stream, message, *grads)
         _check("poseidon_kv_pack", L.lib().poseidon_kv_pack(sizes, ptrs, len(grads), int(pair_elems), int(P),
                                                             int(server), message.data_ptr(), message.numel(),
                                                             ctypes.byref(n), h))
@@ -411,6 +428,7 @@ class KVStore:
             raise ValueError("grad must have the tensor's size")
         if grad.device != self.device:
             raise ValueError("grad must be on the store's device")
+        _uses(stream, grad, *[x for pair in self._keep for x in pair])
         with torch.cuda.device(self.device):
             done = _check("poseidon_kv_receive", L.lib().poseidon_kv_receive(
                 self._h, int(worker), int(tensor), grad.data_ptr(), _stream_handle(stream, self.device)))
@@ -425,6 +443,7 @@ class KVStore:
             raise ValueError("message must have message_size() values")
         if message.device != self.device:
             raise ValueError("message must be on the store's device")
+        _uses(stream, message, *[x for pair in self._keep for x in pair])
         with torch.cuda.device(self.device):
             done = _check("poseidon_kv_receive_message", L.lib().poseidon_kv_receive_message(
                 self._h, int(worker), message.data_ptr() if message.numel() else None,
