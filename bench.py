@@ -432,12 +432,27 @@ def main():
     print(f"[bench] inputs for config {wl.config} ({wl.name}) ready in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)
 
+    copy = None
     if args.calibration_copy_mib > 0:
+        # one plain device copy (the counter calibration reads its first
+        # launch), then a few more timed with events: the copy bandwidth that
+        # the PS rate is also compared with
         n = args.calibration_copy_mib * (1 << 20) // 4
         src = torch.ones(n, device=d)
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
+        cms = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            dst.copy_(src)
+            b.record()
+            torch.cuda.synchronize()
+            cms.append(a.elapsed_time(b))
+        cms.sort()
+        copy = {"bytes": 8 * n, "ms": round(cms[len(cms) // 2], 4),
+                "gbs": round(8 * n / (cms[len(cms) // 2] * 1e-3) / 1e9, 1)}
         del src, dst
 
     pool = api.StreamPool(args.streams, device=d)
@@ -459,6 +474,19 @@ def main():
     event_ms = ev0.elapsed_time(ev1) / args.steps
     print(f"[bench] timed {args.steps} steps: {wall_ms:.3f} ms/step (events {event_ms:.3f})",
           file=sys.stderr, flush=True)
+
+    # The spread: as many more steps, each between its own pair of events.
+    per_step = []
+    for _ in range(args.steps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        it(stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        per_step.append(a.elapsed_time(b))
+    per_step.sort()
+    step_spread = {"median": round(per_step[len(per_step) // 2], 4), "min": round(per_step[0], 4),
+                   "max": round(per_step[-1], 4), "steps": len(per_step)}
 
     # Per-kernel durations for the roofline: the same iteration, same streams,
     # with the library's timing events around each launch on its own stream.
@@ -511,6 +539,7 @@ def main():
                    "P": wl.P, "B": wl.B, "streams": args.streams},
         "roofline": dominant,
         "event_ms_per_step": round(event_ms, 4),
+        "step_ms": step_spread,
     }
     if sf:
         result["roofline_sf"] = sf["roofline"]
@@ -519,6 +548,11 @@ def main():
         result["layers_sfb_momentum"] = sf["layers_momentum"]
     if ps:
         result["roofline_ps"] = dict(ps["roofline"], step=ps["step"], batched_pass=ps["batched_pass"])
+        if copy:
+            result["roofline_ps"]["copy"] = dict(
+                copy, frac=round(ps["roofline"]["achieved"] / copy["gbs"], 4),
+                what=f"a plain {args.calibration_copy_mib} MiB device copy (read + write), median of 5; "
+                     "frac = this kernel's rate / the copy's")
         result["ps_gbs"] = ps["roofline"]["achieved"]
         result["kv_server_share"] = _kv_phase(wl, devt, _time, stream, ksteps)
         print(f"[bench] KV server share: {result['kv_server_share']}", file=sys.stderr, flush=True)

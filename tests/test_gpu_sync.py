@@ -60,7 +60,7 @@ def _to_dev(host, d):
     return out
 
 
-@pytest.mark.parametrize("cfg,streams", [(1, 1), (1, 4), (3, 4), (4, 4), (5, 4), (5, 1), (5, 8)])
+@pytest.mark.parametrize("cfg,streams", [(1, 1), (1, 4), (3, 4), (4, 4), (5, 2), (5, 4), (5, 1), (5, 8)])
 def test_sync_iteration_matches_oracle(cfg, streams):
     d = dev()
     wl = I.workload(cfg)
