@@ -222,10 +222,11 @@ typedef struct poseidon_kv_store poseidon_kv_store;
  * step's lr and momentum (used only for tensors that have a buf).  The store
  * keeps the tensor list, the layout, one count per pair and one update
  * pointer per (tensor, worker); it allocates no device memory.  All counts
- * start at 0 (as after poseidon_kv_begin).  P <= 64.  Returns POSEIDON_OK,
- * POSEIDON_ERR_INVALID_ARG (bad sizes, NULL W or buf/W overlap with n > 0,
- * rank outside 0..P-1, P outside 1..64, count < 0, NULL out) or
- * POSEIDON_ERR_HIP.
+ * start at 0 (as after poseidon_kv_begin).  P <= 64.  No two of the
+ * tensors' W and buf arrays may overlap (one launch may apply pairs of several
+ * tensors).  Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (bad sizes, NULL W
+ * with n > 0, overlapping arrays, rank outside 0..P-1, P outside 1..64,
+ * count < 0, NULL out) or POSEIDON_ERR_HIP.
  */
 int poseidon_kv_create(const poseidon_kv_tensor* tensors, int32_t count, int64_t pair_elems, int32_t P,
                        int32_t rank, float lr, float momentum, poseidon_kv_store** out);
@@ -267,9 +268,10 @@ int poseidon_kv_receive(poseidon_kv_store* store, int32_t worker, int32_t tensor
  * makes it; poseidon_kv_message_size elements of device memory, caller-owned,
  * not modified).  It stands for that worker's update of every tensor, as if
  * poseidon_kv_receive had been called for each: every count of this store's
- * pairs goes up by one, and each tensor whose pairs reach P is applied on
- * `stream`, reading every worker's values where they arrived (a message or a
- * whole-tensor update), summed in worker order.  The message must stay valid,
+ * pairs goes up by one, and the tensors whose pairs reach P are applied on
+ * `stream` (together: one launch for the tensors whose P updates all arrived
+ * the same way), reading every worker's values where they arrived (a message
+ * or a whole-tensor update), summed in worker order.  The message must stay valid,
  * and its data complete in the order of `stream`, until that work has run.
  * Returns the number of pairs completed, or POSEIDON_ERR_INVALID_ARG (NULL
  * store; worker out of range; NULL message when this store holds pairs; a

@@ -417,6 +417,7 @@ class KVStore:
                                                                     self.rank, float(lr), float(momentum),
                                                                     ctypes.byref(self._h)))
         self.pairs = kv_layout(self.sizes, pair_elems, P)
+        self._msg_len = self.message_size()
 
     def begin(self) -> None:
         _check("poseidon_kv_begin", L.lib().poseidon_kv_begin(self._h))
@@ -428,27 +429,32 @@ class KVStore:
             raise ValueError("grad must have the tensor's size")
         if grad.device != self.device:
             raise ValueError("grad must be on the store's device")
-        _uses(stream, grad, *[x for pair in self._keep for x in pair])
+        _uses(stream, grad)
         with torch.cuda.device(self.device):
             done = _check("poseidon_kv_receive", L.lib().poseidon_kv_receive(
                 self._h, int(worker), int(tensor), grad.data_ptr(), _stream_handle(stream, self.device)))
         self._grads[(worker, tensor)] = grad
+        if done:       # an apply was enqueued: it reads the tensor's updates and writes its W and buf
+            _uses(stream, *self._keep[tensor],
+                  *[g for (_, k), g in self._grads.items() if k == tensor or k == "message"])
         return done
 
     def receive_message(self, worker: int, message: torch.Tensor, stream=None) -> int:
         """Worker ``worker``'s message to this server (``kv_pack``) has arrived;
         returns the number of pairs it completed."""
         _dev_f32("message", message)
-        if message.numel() != self.message_size():
+        if message.numel() != self._msg_len:
             raise ValueError("message must have message_size() values")
         if message.device != self.device:
             raise ValueError("message must be on the store's device")
-        _uses(stream, message, *[x for pair in self._keep for x in pair])
+        _uses(stream, message)
         with torch.cuda.device(self.device):
             done = _check("poseidon_kv_receive_message", L.lib().poseidon_kv_receive_message(
                 self._h, int(worker), message.data_ptr() if message.numel() else None,
                 _stream_handle(stream, self.device)))
         self._grads[(worker, "message")] = message
+        if done:       # applies were enqueued: they read the updates and write W and buf
+            _uses(stream, *[x for pair in self._keep for x in pair], *self._grads.values())
         return done
 
     def message_size(self) -> int:

@@ -59,16 +59,23 @@ constexpr int PS_BATCH_MAX = 48;   // descriptors per batched launch (kernel-arg
 hipError_t launch_ps_apply_batch(const PsTensor* tensors, int32_t count, int32_t P, float lr,
                                  float momentum, hipStream_t stream);
 
-// KV-store apply of one tensor's pairs held by one server (arguments
-// validated; P <= KV_MAX_P; every range inside the tensor).  grads[p] is
-// worker p's whole-tensor update, or (bit p of msg_mask) its message, whose
-// values of range i sit deltas[i] elements past the tensor's indices.  Ranges
-// beyond KV_MAX_RANGES take further launches.
+// KV-store apply of pairs held by one server (arguments validated; P <=
+// KV_MAX_P; every range inside its tensor; the tensors do not overlap).
+// grads[p] is worker p's update, the same for every range: a whole-tensor
+// update, or (bit p of msg_mask) its message, whose values of a range sit
+// `delta` elements past the tensor's indices.  Ranges with a buf and ranges
+// without take separate launches, and beyond KV_MAX_RANGES further ones.
 constexpr int KV_MAX_P = 64;
 constexpr int KV_MAX_RANGES = 32;
-hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, uint64_t msg_mask, int32_t P,
-                           const int64_t* offsets, const int64_t* lengths, const int64_t* deltas, int32_t nranges,
-                           float lr, float momentum, hipStream_t stream);
+struct KvApplyRange {
+    float* W;
+    float* buf;       // momentum buffer, or NULL (plain SGD)
+    int64_t offset;
+    int64_t length;
+    int64_t delta;
+};
+hipError_t launch_kv_apply(const KvApplyRange* ranges, int32_t nranges, const float* const* grads,
+                           uint64_t msg_mask, int32_t P, float lr, float momentum, hipStream_t stream);
 
 // A worker's message to one server: src[i][0 .. length[i]) copied to
 // message[dst[i] ..), in KV_PACK_MAX ranges per launch (arguments validated).

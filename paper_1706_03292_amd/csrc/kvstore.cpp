@@ -14,6 +14,9 @@
 // are.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <cstdint>
+#include <utility>
 #include <vector>
 
 #include "common.h"
@@ -51,23 +54,38 @@ int64_t count_pairs(const int64_t* sizes, int32_t count, int64_t pair_elems)
     return total;
 }
 
-// Enqueue the apply of tensor t's pairs held by the store (their counts have
-// reached P).
-hipError_t apply_tensor(poseidon_kv_store* st, int32_t t, hipStream_t stream)
+// Enqueue the apply of the pairs held by the store of the tensors in `ts`
+// (their counts have reached P): one launch for all the tensors whose P
+// update pointers are the same (every update came in the same messages, the
+// usual case), one more for each other set of pointers.
+hipError_t apply_tensors(poseidon_kv_store* st, const std::vector<int32_t>& ts, hipStream_t stream)
 {
-    const poseidon_kv_tensor& x = st->tensors[static_cast<size_t>(t)];
-    const std::vector<int32_t>& mine = st->owned[static_cast<size_t>(t)];
-    std::vector<int64_t> off, len, delta;
-    for (int32_t j : mine) {
-        const poseidon_kv_pair& q = st->pairs[static_cast<size_t>(j)];
-        off.push_back(q.offset);
-        len.push_back(q.length);
-        delta.push_back(st->msg_off[static_cast<size_t>(j)] - q.offset);
+    std::vector<bool> done(ts.size(), false);
+    std::vector<poseidon::KvApplyRange> ranges;
+    for (size_t a = 0; a < ts.size(); ++a) {
+        if (done[a])
+            continue;
+        const size_t ta = static_cast<size_t>(ts[a]);
+        ranges.clear();
+        for (size_t b = a; b < ts.size(); ++b) {
+            const size_t tb = static_cast<size_t>(ts[b]);
+            if (done[b] || st->grads[tb] != st->grads[ta] || st->from_msg[tb] != st->from_msg[ta])
+                continue;
+            done[b] = true;
+            const poseidon_kv_tensor& x = st->tensors[tb];
+            for (int32_t j : st->owned[tb]) {
+                const poseidon_kv_pair& q = st->pairs[static_cast<size_t>(j)];
+                ranges.push_back(poseidon::KvApplyRange{x.W, x.buf, q.offset, q.length,
+                                                         st->msg_off[static_cast<size_t>(j)] - q.offset});
+            }
+        }
+        const hipError_t e = poseidon::launch_kv_apply(ranges.data(), static_cast<int32_t>(ranges.size()),
+                                                       st->grads[ta].data(), st->from_msg[ta], st->P, st->lr,
+                                                       st->mu, stream);
+        if (e != hipSuccess)
+            return e;
     }
-    return poseidon::launch_kv_apply(x.W, x.buf, st->grads[static_cast<size_t>(t)].data(),
-                                     st->from_msg[static_cast<size_t>(t)], st->P, off.data(), len.data(),
-                                     delta.data(), static_cast<int32_t>(mine.size()), st->lr,
-                                     x.buf ? st->mu : 0.0f, stream);
+    return hipSuccess;
 }
 
 void fill_layout(const int64_t* sizes, int32_t count, int64_t pair_elems, int32_t P, poseidon_kv_pair* out)
@@ -119,6 +137,21 @@ extern "C" int poseidon_kv_create(const poseidon_kv_tensor* tensors, int32_t cou
             return POSEIDON_ERR_INVALID_ARG;
         sizes[static_cast<size_t>(t)] = x.n;
     }
+    // No two arrays of the store may overlap: one launch may apply pairs of
+    // several tensors at once.
+    std::vector<std::pair<uintptr_t, uintptr_t>> spans;
+    for (int32_t t = 0; t < count; ++t) {
+        const poseidon_kv_tensor& x = tensors[t];
+        if (x.n == 0)
+            continue;
+        spans.emplace_back(reinterpret_cast<uintptr_t>(x.W), reinterpret_cast<uintptr_t>(x.W) + x.n * 4);
+        if (x.buf)
+            spans.emplace_back(reinterpret_cast<uintptr_t>(x.buf), reinterpret_cast<uintptr_t>(x.buf) + x.n * 4);
+    }
+    std::sort(spans.begin(), spans.end());
+    for (size_t i = 1; i < spans.size(); ++i)
+        if (spans[i].first < spans[i - 1].second)
+            return POSEIDON_ERR_INVALID_ARG;
     const int64_t total = count_pairs(sizes.data(), count, pair_elems);
     if (total < 0)
         return POSEIDON_ERR_INVALID_ARG;
@@ -200,7 +233,7 @@ extern "C" int poseidon_kv_receive(poseidon_kv_store* store, int32_t worker, int
         complete = ++store->count[static_cast<size_t>(j)] == store->P && complete;
     if (!complete)
         return 0;
-    if (apply_tensor(store, tensor, stream) != hipSuccess)
+    if (apply_tensors(store, std::vector<int32_t>{tensor}, stream) != hipSuccess)
         return POSEIDON_ERR_HIP;
     return static_cast<int32_t>(mine.size());
 }
@@ -224,6 +257,7 @@ extern "C" int poseidon_kv_receive_message(poseidon_kv_store* store, int32_t wor
     if (dev != store->device)
         return POSEIDON_ERR_INVALID_ARG;
     int32_t done = 0;
+    std::vector<int32_t> complete_ts;   // applied together after the counts
     for (size_t t = 0; t < T; ++t) {
         const poseidon_kv_tensor& x = store->tensors[t];
         // The message stands for this worker's update of every tensor; a
@@ -237,11 +271,12 @@ extern "C" int poseidon_kv_receive_message(poseidon_kv_store* store, int32_t wor
         for (int32_t j : store->owned[t])
             complete = ++store->count[static_cast<size_t>(j)] == store->P && complete;
         if (complete) {
-            if (apply_tensor(store, static_cast<int32_t>(t), stream) != hipSuccess)
-                return POSEIDON_ERR_HIP;
+            complete_ts.push_back(static_cast<int32_t>(t));
             done += static_cast<int32_t>(store->owned[t].size());
         }
     }
+    if (!complete_ts.empty() && apply_tensors(store, complete_ts, stream) != hipSuccess)
+        return POSEIDON_ERR_HIP;
     return done;
 }
 

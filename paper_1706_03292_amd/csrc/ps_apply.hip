@@ -257,18 +257,22 @@ void launch_batch_mom(const PsBatchArgs& a, int blocks, int grid, int32_t P, flo
 }
 
 // ---------------------------------------------------------------------------
-// KV-store apply: the pairs of one tensor that one server holds, with the P
-// workers' updates at separate addresses (one pointer per worker, passed in
-// worker order).  Range r covers tensor elements [offset, offset + length)
-// and owns the workgroups [first_block[r], first_block[r+1]); each workgroup
-// updates PS_BLOCK_ELEMS consecutive elements of its range.
+// KV-store apply: pairs that one server holds, of one or several tensors,
+// with the P workers' updates at separate addresses (one pointer per worker,
+// passed in worker order, the same for every range of the launch).  Range r
+// covers elements [offset, offset + length) of the tensor (W, buf) and owns
+// the workgroups [first_block[r], first_block[r+1]); each workgroup updates
+// PS_BLOCK_ELEMS consecutive elements of its range, with 16-byte accesses
+// that are aligned when the range's arrays allow it.
 // ---------------------------------------------------------------------------
 struct KvRange {
+    float* W;
+    float* buf;          // NULL on a launch without momentum
     int64_t offset;
     int64_t length;
     int64_t delta;       // a message's values of element e are at message + delta + e
     int32_t first_block;
-    int32_t pad;
+    int32_t aligned;
 };
 
 struct KvArgs {
@@ -279,20 +283,23 @@ struct KvArgs {
     int32_t nranges;
 };
 
-template <int PT, bool MOM, bool AL>
-__global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, int P, float* __restrict__ W,
-                                                               float* __restrict__ buf, float lr, float mu)
+template <int PT, bool MOM>
+__global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, int P, float lr, float mu)
 {
     const int b = blockIdx.x;
     int r = 0;                                  // as in the batched kernel: independent loads
 #pragma unroll
     for (int k = 1; k < KV_MAX_RANGES; ++k)
         r += (k < a.nranges && a.first_block[k] <= b) ? 1 : 0;
-    const int64_t j = static_cast<int64_t>(b - a.r[r].first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
-    if (j >= a.r[r].length)
+    const KvRange& q = a.r[r];
+    const int64_t j = static_cast<int64_t>(b - q.first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
+    if (j >= q.length)
         return;
-    const PerWorker src{a.g, a.msg_mask, a.r[r].delta};
-    apply_group<PT, MOM, AL>(W, buf, src, P, a.r[r].offset + j, a.r[r].offset + a.r[r].length, lr, mu);
+    const PerWorker src{a.g, a.msg_mask, q.delta};
+    if (q.aligned)
+        apply_group<PT, MOM, true>(q.W, q.buf, src, P, q.offset + j, q.offset + q.length, lr, mu);
+    else
+        apply_group<PT, MOM, false>(q.W, q.buf, src, P, q.offset + j, q.offset + q.length, lr, mu);
 }
 
 // ---------------------------------------------------------------------------
@@ -343,15 +350,15 @@ __global__ __launch_bounds__(PS_THREADS) void kv_pack_kernel(const PackArgs a, f
     }
 }
 
-template <bool MOM, bool AL>
-void launch_kv_al(const KvArgs& a, int grid, int32_t P, float* W, float* buf, float lr, float mu, hipStream_t stream)
+template <bool MOM>
+void launch_kv_mom(const KvArgs& a, int grid, int32_t P, float lr, float mu, hipStream_t stream)
 {
     switch (P) {
-    case 4:  kv_apply_kernel<4, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
-    case 8:  kv_apply_kernel<8, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
-    case 16: kv_apply_kernel<16, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
-    case 32: kv_apply_kernel<32, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
-    default: kv_apply_kernel<0, MOM, AL><<<grid, PS_THREADS, 0, stream>>>(a, P, W, buf, lr, mu); break;
+    case 4:  kv_apply_kernel<4, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    case 8:  kv_apply_kernel<8, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    case 16: kv_apply_kernel<16, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    case 32: kv_apply_kernel<32, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    default: kv_apply_kernel<0, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
     }
 }
 
@@ -416,47 +423,53 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
     return hipSuccess;
 }
 
-hipError_t launch_kv_apply(float* W, float* buf, const float* const* grads, uint64_t msg_mask, int32_t P,
-                           const int64_t* offsets, const int64_t* lengths, const int64_t* deltas, int32_t nranges,
-                           float lr, float momentum, hipStream_t stream)
+hipError_t launch_kv_apply(const KvApplyRange* ranges, int32_t nranges, const float* const* grads,
+                           uint64_t msg_mask, int32_t P, float lr, float momentum, hipStream_t stream)
 {
-    bool al = aligned16(W) && (!buf || aligned16(buf));
+    bool grads_al = true;
     for (int32_t p = 0; p < P; ++p)
-        al = al && aligned16(grads[p]);
-    for (int32_t i = 0; i < nranges; ++i)
-        al = al && offsets[i] % 4 == 0 && (msg_mask == 0 || deltas[i] % 4 == 0);
-    for (int32_t i0 = 0; i0 < nranges; i0 += KV_MAX_RANGES) {
+        grads_al = grads_al && aligned16(grads[p]);
+    // Ranges with a momentum buffer and ranges without take separate launches.
+    for (int mom = 1; mom >= 0; --mom) {
         KvArgs a{};
         for (int32_t p = 0; p < P; ++p)
             a.g[p] = grads[p];
         a.msg_mask = msg_mask;
         int64_t blocks = 0;
-        for (int32_t i = i0; i < nranges && i < i0 + KV_MAX_RANGES; ++i) {
-            KvRange& r = a.r[a.nranges++];
-            r.offset = offsets[i];
-            r.length = lengths[i];
-            r.delta = deltas[i];
+        auto flush = [&]() -> hipError_t {
+            if (blocks == 0)
+                return hipSuccess;
+            if (mom)
+                launch_kv_mom<true>(a, static_cast<int>(blocks), P, lr, momentum, stream);
+            else
+                launch_kv_mom<false>(a, static_cast<int>(blocks), P, lr, 0.0f, stream);
+            a.nranges = 0;
+            blocks = 0;
+            return hipGetLastError();
+        };
+        for (int32_t i = 0; i < nranges; ++i) {
+            const KvApplyRange& x = ranges[i];
+            if (x.length == 0 || (x.buf != nullptr) != (mom == 1))
+                continue;
+            const int64_t nb = (x.length + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
+            if (a.nranges == KV_MAX_RANGES || blocks + nb > INT32_MAX) {
+                const hipError_t e = flush();
+                if (e != hipSuccess)
+                    return e;
+            }
+            KvRange& r = a.r[a.nranges];
+            r.W = x.W;
+            r.buf = x.buf;
+            r.offset = x.offset;
+            r.length = x.length;
+            r.delta = x.delta;
             r.first_block = static_cast<int32_t>(blocks);
-            a.first_block[a.nranges - 1] = r.first_block;
-            blocks += (lengths[i] + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
-            if (blocks > INT32_MAX)
-                return hipErrorInvalidValue;
+            r.aligned = grads_al && aligned16(x.W) && (!x.buf || aligned16(x.buf)) && x.offset % 4 == 0 &&
+                        (msg_mask == 0 || x.delta % 4 == 0);
+            a.first_block[a.nranges++] = r.first_block;
+            blocks += nb;
         }
-        if (blocks == 0)
-            continue;
-        const int grid = static_cast<int>(blocks);
-        if (buf) {
-            if (al)
-                launch_kv_al<true, true>(a, grid, P, W, buf, lr, momentum, stream);
-            else
-                launch_kv_al<true, false>(a, grid, P, W, buf, lr, momentum, stream);
-        } else {
-            if (al)
-                launch_kv_al<false, true>(a, grid, P, W, nullptr, lr, 0.0f, stream);
-            else
-                launch_kv_al<false, false>(a, grid, P, W, nullptr, lr, 0.0f, stream);
-        }
-        const hipError_t e = hipGetLastError();
+        const hipError_t e = flush();
         if (e != hipSuccess)
             return e;
     }

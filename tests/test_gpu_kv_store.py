@@ -267,3 +267,48 @@ def test_kv_pack_every_server_in_one_pass():
     torch.cuda.synchronize()
     ref = np.concatenate([oracle.kv_pack([x.numpy() for x in g], pair, P, q) for q in range(P)])
     assert np.array_equal(to_np(allm), ref)
+
+
+def test_kv_message_applies_tensors_with_and_without_buffers_and_misaligned_together():
+    """One message completes every tensor at once, and they are applied
+    together: tensors with and without a momentum buffer, some with W or buf
+    4 bytes off a 16-byte boundary.  The result equals per-tensor receives bit
+    for bit and the oracle store."""
+    d = dev()
+    sizes, pair, P, rank = [1000, 17, 4, 333, 4096, 2049, 64], 256, 4, 0
+    tens, grads = _case(sizes, P, seed=2300)
+    tens = [(W, b if t % 3 != 1 else None) for t, (W, b) in enumerate(tens)]
+
+    def place(tens_):
+        out = []
+        for t, (W, b) in enumerate(tens_):
+            Wd = misaligned(W.to(d)) if t % 2 == 1 else W.to(d)
+            bd = None if b is None else (misaligned(b.to(d)) if t % 4 == 2 else b.to(d))
+            out.append((Wd, bd))
+        return out
+
+    dg = [[g.to(d) for g in gp] for gp in grads]
+    results = []
+    for mode in ("message", "tensor"):
+        dt = place(tens)
+        st = api.KVStore(dt, pair, P, rank, LR, MU)
+        log(f"kv_store mixed buffers/alignment by {mode}")
+        for p in range(P):
+            if mode == "message":
+                st.receive_message(p, api.kv_pack(dg[p], pair, P, rank))
+            else:
+                for t in range(len(sizes)):
+                    st.receive(p, t, dg[p][t])
+        torch.cuda.synchronize()
+        results.append(dt)
+        st.close()
+    ref = oracle.KVStore([(W.numpy(), None if b is None else b.numpy()) for W, b in tens], pair, P, rank, LR, MU)
+    for p in range(P):
+        ref.receive_message(p, oracle.kv_pack([g.numpy() for g in grads[p]], pair, P, rank))
+    for t in range(len(sizes)):
+        (Wm, bm), (Wt, bt) = results[0][t], results[1][t]
+        assert torch.equal(Wm, Wt), f"W {t}"
+        assert_close(to_np(Wm), ref.W[t], W_TOL, f"W {t}")
+        if bm is not None:
+            assert torch.equal(bm, bt), f"buf {t}"
+            assert_close(to_np(bm), ref.buf[t], BUF_TOL, f"buf {t}")

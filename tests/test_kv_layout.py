@@ -58,6 +58,14 @@ def test_kv_store_argument_checks_before_device_work():
     assert lib.poseidon_kv_create(t, 2, 16, 4, 0, 0.1, 0.9, None) == L.ERR_INVALID_ARG
     bad = (L.PoseidonKvTensor * 1)(L.PoseidonKvTensor(0x100000, 0x100010, 64))          # buf overlaps W
     assert lib.poseidon_kv_create(bad, 1, 16, 4, 0, 0.1, 0.9, ctypes.byref(h)) == L.ERR_INVALID_ARG
+    # arrays of different tensors must not overlap either (one launch may
+    # apply several tensors' pairs)
+    cross = (L.PoseidonKvTensor * 2)(L.PoseidonKvTensor(0x100000, 0x200000, 64),
+                                     L.PoseidonKvTensor(0x1000F0, None, 8))      # W_1 inside W_0
+    assert lib.poseidon_kv_create(cross, 2, 16, 4, 0, 0.1, 0.9, ctypes.byref(h)) == L.ERR_INVALID_ARG
+    cross = (L.PoseidonKvTensor * 2)(L.PoseidonKvTensor(0x100000, 0x200000, 64),
+                                     L.PoseidonKvTensor(0x300000, 0x2000FC, 8))  # buf_1 meets buf_0's last value
+    assert lib.poseidon_kv_create(cross, 2, 16, 4, 0, 0.1, 0.9, ctypes.byref(h)) == L.ERR_INVALID_ARG
     null_w = (L.PoseidonKvTensor * 1)(L.PoseidonKvTensor(None, None, 4))
     assert lib.poseidon_kv_create(null_w, 1, 16, 4, 0, 0.1, 0.9, ctypes.byref(h)) == L.ERR_INVALID_ARG
     assert lib.poseidon_kv_destroy(None) == L.OK
