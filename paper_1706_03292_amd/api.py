@@ -238,7 +238,8 @@ class StreamPool:
 
     def launch_times(self, capacity: int = 256) -> list[dict]:
         """Launch records of the last timed iteration (waits for it): dicts with
-        ``scheme`` (SFB/PS), ``tensor`` (index, -1 for the PS batch),
+        ``scheme`` (SFB/PS), ``tensor`` (index, or -1 for a launch shared by
+        several tensors: the batched small PS tensors, the grouped FC layers),
         ``stream`` and ``ms``."""
         recs = (L.PoseidonLaunchRecord * capacity)()
         n = ctypes.c_int32()
@@ -317,6 +318,10 @@ class SyncIteration:
         update then waits for ready[t] instead of for the work on ``stream``
         (wait-free backpropagation, poseidon_sync_iteration_wfbp)."""
         h = _stream_handle(stream, self.pool.device)
+        # Every update joins back into `stream`; work on another torch stream
+        # than the current one must be known to the caching allocator.
+        if isinstance(stream, torch.cuda.Stream) and stream != torch.cuda.current_stream(self.pool.device):
+            _uses(stream, *[x for keep in self._keep for x in keep])
         with torch.cuda.device(self.pool.device):
             if ready is None:
                 _check("poseidon_sync_iteration", L.lib().poseidon_sync_iteration(
