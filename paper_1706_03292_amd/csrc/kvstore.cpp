@@ -5,9 +5,10 @@
 // have arrived, applying a pair once every worker's update of it is there.
 //
 // The bookkeeping (layout, counts, the update pointers) is host state, as in
-// the paper's KV store; the apply of a completed tensor's pairs is one kernel
-// launch on the stream of the receive that completed them, summing the P
-// workers' updates in worker order whatever the order they arrived in.  An
+// the paper's KV store; the pairs of the tensors that one receive completes
+// are applied by one kernel launch (per set of update pointers) on that
+// receive's stream, summing the P workers' updates in worker order whatever
+// the order they arrived in.  An
 // update arrives either as a worker's whole tensor or inside the worker's
 // message to this server (poseidon_kv_pack: its slices of this server's
 // pairs, in pair order), and the apply reads each worker's values where they

@@ -25,7 +25,8 @@
 //
 // Three launch forms share the per-group update: one tensor with P
 // contiguous shards, many such tensors in one launch, and the KV store's
-// pairs of one tensor with the P workers' updates at separate addresses.
+// pairs (of one or several tensors) with the P workers' updates at separate
+// addresses.
 #include "common.h"
 
 namespace poseidon {
