@@ -226,3 +226,26 @@ def test_ps_apply_batch_misaligned_and_empty():
         w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, 0.9, b.numpy())
         assert_close(to_np(Wd), w_ref, W_TOL, "W")
         assert_close(to_np(bd), b_ref, BUF_TOL, "buf")
+
+
+def test_ps_apply_shards_beyond_32bit_offsets():
+    """P = 16 shards of 40,000,001 values (2.56 GB; the last shard starts
+    2.4 GB in, past 2^31 bytes), ragged length, momentum, through the single
+    and the batched launch; sampled against the oracle."""
+    d = dev()
+    P, n = 16, 40_000_001
+    W, G, buf = _draw(P, n, seed=7100, buf_std=1e-3)
+    idx = np.concatenate([np.random.default_rng(7).integers(0, n, 4000), np.arange(n - 67, n), np.arange(4)])
+    w_ref, b_ref = oracle.ps_apply_points(W.numpy(), G.numpy(), 0.01, 0.9, buf.numpy(), idx)
+    Gd = G.to(d)
+    del G
+    for how in ("single", "batch"):
+        Wd, bd = W.to(d), buf.to(d)
+        log(f"ps_apply P={P} n={n} ({how})")
+        if how == "single":
+            api.ps_apply(Wd, Gd, 0.01, 0.9, bd)
+        else:
+            api.ps_apply_batch([(Wd, Gd, bd)], 0.01, 0.9)
+        torch.cuda.synchronize()
+        assert_close(to_np(Wd)[idx], w_ref, W_TOL, f"W ({how})")
+        assert_close(to_np(bd)[idx], b_ref, BUF_TOL, f"buf ({how})")
