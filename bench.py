@@ -488,9 +488,9 @@ def main():
     print(f"[bench] timed {args.steps} steps: {wall_ms:.3f} ms/step (events {event_ms:.3f})",
           file=sys.stderr, flush=True)
 
-    # The spread: as many more steps, each between its own pair of events.
+    # The spread: at least 30 more steps, each between its own pair of events.
     per_step = []
-    for _ in range(args.steps):
+    for _ in range(max(30, args.steps)):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
         it(stream)
