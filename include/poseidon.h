@@ -414,13 +414,18 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * arithmetic of the single-tensor calls, so the same results): PS tensors of
  * fewer than 2^17 values, which a launch of their own would leave
  * latency-bound, are applied together, in backpropagation order, by one
- * batched pass (poseidon_ps_apply_batch) after the other PS launches; and the
- * SFB tensors without a momentum buffer, when there are several, are rebuilt
- * by one grouped launch (poseidon_sf_apply_batch) at the place of the first
- * of them, so that the layers' tiles share one work list.  SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
+ * batched pass (poseidon_ps_apply_batch) after the other PS launches -- and
+ * when the PS applies are the iteration's critical path (the SFB rebuilds
+ * come to fewer than 26 flops per PS byte, 2*M*N*P*B flops against
+ * n*(4P+16) bytes, or 4P+8 without a buffer), so do PS tensors of fewer than
+ * 2^21 values; and the SFB tensors without a momentum buffer, when there are
+ * several, are rebuilt by one grouped launch (poseidon_sf_apply_batch) at the
+ * place of the first of them, so that the layers' tiles share one work list.
+ * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
  * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
  * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,
- * momentum, buf) (momentum is used only when buf != NULL).  Every pool stream first waits for the work already
+ * momentum, buf) (momentum is used only when buf != NULL).  Every pool
+ * stream first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so
  * the call behaves like one asynchronous operation on `stream` (the
  * bulk-synchronous barrier of Sec. 4.1 "Managing Consistency").
@@ -447,8 +452,9 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
  * tensors of one layer may share an event.  Issue order, streams, schemes,
  * payload rules and results are those of poseidon_sync_iteration (bitwise:
  * the same kernels), except that every SFB tensor keeps a launch of its own
- * (no grouped launch), so that each starts after its own event; `stream`
- * waits for every update at the end.
+ * (no grouped launch) and only PS tensors of fewer than 2^17 values share the
+ * batched pass, so that each other update starts after its own event;
+ * `stream` waits for every update at the end.
  * ready: count non-NULL events, caller-owned, not retained after the call.
  * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (also for NULL ready or a NULL
  * entry), POSEIDON_ERR_PAYLOAD or POSEIDON_ERR_HIP.

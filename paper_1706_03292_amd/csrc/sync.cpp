@@ -124,10 +124,20 @@ extern "C" int poseidon_pool_destroy(poseidon_stream_pool* pool)
 
 namespace {
 
-// PS tensors below this many elements are launch-bound on their own (a launch
-// costs a few microseconds; 2^17 elements at P = 32 move 19 MB, about 4 us of
-// HBM time): the iteration gathers them into batched launches.
+// PS tensors below SMALL_PS_ELEMS elements are launch-bound on their own (a
+// launch costs a few microseconds; 2^17 elements at P = 32 move 19 MB, about
+// 4 us of HBM time): the iteration gathers them into a batched pass.  When
+// the PS applies are the iteration's critical path -- the SF rebuilds would
+// take less time than them, judged by the ratio of the two kernels' rates on
+// this GPU (about 130 TFLOP/s over 5 TB/s, 26 flops per PS byte) -- every
+// launch saved shortens the iteration, and tensors below PS_CRITICAL_ELEMS
+// join the pass too (Inception-shaped workload, 95 tensors at P = 32:
+// 0.69 vs 0.77 ms per iteration); when the SF chain is the critical path,
+// large PS tensors keep launches of their own, which interleave with it
+// (VGG19-22K: neutral to 0.8% slower with the larger threshold).
 constexpr int64_t SMALL_PS_ELEMS = int64_t{1} << 17;
+constexpr int64_t PS_CRITICAL_ELEMS = int64_t{1} << 21;
+constexpr double SF_FLOPS_PER_PS_BYTE = 26.0;
 
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
 // for the work enqueued on `stream` before the call) and of
@@ -147,9 +157,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
 
     // Validate everything and fix every scheme before enqueueing anything.
     std::vector<int32_t> plan(static_cast<size_t>(count));
-    int32_t active = 0;
-    int32_t small_ps = 0;
-    int32_t plain_sf = 0;     // SFB layers without a momentum buffer
+    double sf_flops = 0.0, ps_bytes = 0.0;
     for (int32_t t = 0; t < count; ++t) {
         const poseidon_tensor& x = tensors[t];
         if ((x.kind != POSEIDON_KIND_FC && x.kind != POSEIDON_KIND_OTHER) || x.reserved != 0 ||
@@ -168,18 +176,12 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
                 return POSEIDON_ERR_PAYLOAD;
             rc = x.buf ? check_sf_momentum_args(x.W, x.buf, x.U, x.V, x.M, x.N, K)
                        : check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
-            if (n > 0 && (K > 0 || x.buf))
-                ++active;
-            if (n > 0 && K > 0 && !x.buf)
-                ++plain_sf;
+            sf_flops += 2.0 * static_cast<double>(n) * static_cast<double>(K);
         } else {
             if (n > 0 && !x.shards)
                 return POSEIDON_ERR_PAYLOAD;
             rc = check_ps_args(x.W, x.shards, P, n, x.buf ? momentum : 0.0f, x.buf);
-            if (n > 0 && n < SMALL_PS_ELEMS)
-                ++small_ps;
-            else if (n > 0)
-                ++active;
+            ps_bytes += static_cast<double>(n) * (4.0 * P + (x.buf ? 16.0 : 8.0));
         }
         if (rc != POSEIDON_OK)
             return rc;
@@ -190,6 +192,29 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
             schemes[t] = plan[static_cast<size_t>(t)];
+    // With ready events each large tensor keeps its own launch, so that it
+    // starts as soon as its own backward pass has run.
+    const int64_t small_elems =
+        (!ready && sf_flops < SF_FLOPS_PER_PS_BYTE * ps_bytes) ? PS_CRITICAL_ELEMS : SMALL_PS_ELEMS;
+    int32_t active = 0;
+    int32_t small_ps = 0;
+    int32_t plain_sf = 0;     // SFB layers without a momentum buffer
+    for (int32_t t = 0; t < count; ++t) {
+        const poseidon_tensor& x = tensors[t];
+        const int64_t n = x.M * x.N;
+        if (n == 0)
+            continue;
+        if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
+            if (K > 0 || x.buf)
+                ++active;
+            if (K > 0 && !x.buf)
+                ++plain_sf;
+        } else if (n < small_elems) {
+            ++small_ps;
+        } else {
+            ++active;
+        }
+    }
     // One launch per tensor with work, except: small PS tensors share one
     // batched pass after the other PS launches; and without ready events the
     // SFB layers without a momentum buffer share one grouped launch, at the
@@ -260,7 +285,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         const int64_t n = x.M * x.N;
         if (n == 0)
             continue;
-        if (plan[static_cast<size_t>(t)] == POSEIDON_PS && n < SMALL_PS_ELEMS) {
+        if (plan[static_cast<size_t>(t)] == POSEIDON_PS && n < small_elems) {
             small.push_back(PsTensor{x.W, x.shards, x.buf, n});
             small_idx.push_back(t);
             continue;

@@ -187,3 +187,31 @@ def test_sync_iteration_groups_the_fc_layers_and_wfbp_does_not():
     for x, y in zip(a, b):
         assert torch.equal(x["W"], y["W"]), x["spec"].name
     pool.close()
+
+
+def test_sync_iteration_batches_more_when_the_ps_applies_are_the_critical_path():
+    """When the PS applies outweigh the SF rebuilds (26 flops per PS byte),
+    PS tensors below 2^21 values join the batched pass; larger ones keep
+    their own launches.  Records and results (against the oracle) checked on
+    Inception-shaped tensors around the threshold."""
+    d = dev()
+    wl = I.workload(4)
+    names = ["fc.W", "conv46", "conv44", "conv43", "conv38", "conv10", "conv5"]
+    host = I.make_tensors(wl, only=names)
+    devt = _to_dev(host, d)
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    pool.set_timing(True)
+    log("sync_iteration PS-critical batching")
+    schemes = it()
+    recs = [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()]
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    sizes = {i: h["spec"].numel for i, h in enumerate(host)}
+    want = [(api.SFB, i, 0) if h["spec"].kind == I.FC else (api.PS, i, 1)
+            for i, h in reversed(list(enumerate(host)))
+            if h["spec"].kind == I.FC or h["spec"].numel >= 1 << 21] + [(api.PS, -1, 1)]
+    assert recs == want, (recs, sizes)
+    assert sum(1 for i, s in sizes.items() if host[i]["spec"].kind != I.FC and s >= 1 << 21) == 2
+    _oracle_check(host, devt, wl, schemes)
+    pool.close()
