@@ -242,7 +242,7 @@ def _sf_phase(wl, host, devt, schemes, launch_ms, time_fn, stream):
         spec, t = host[i]["spec"], devt[i]
         W, U, V = t["W"], t["U"], t["V"]
         f = _sf_flops(spec, wl.K)
-        ms = time_fn(lambda: api.sf_apply(W, U, V, wl.lr, stream=stream))
+        ms = time_fn(lambda: api.sf_apply(W, U, V, wl.lr, stream=stream), queued=True)
         it_ms = launch_ms.get((api.SFB, i))
         flops += f
         layers.append({"tensor": spec.name, "scheme": "SFB",
@@ -251,7 +251,7 @@ def _sf_phase(wl, host, devt, schemes, launch_ms, time_fn, stream):
                        "alone_ms": round(ms, 4), "alone_tflops": round(f / ms / 1e9, 2)})
         # the same layer with a momentum buffer: W and buf each read and written once
         mbuf = torch.zeros_like(W)
-        ms = time_fn(lambda: api.sf_apply_momentum(W, mbuf, U, V, wl.lr, wl.momentum, stream=stream))
+        ms = time_fn(lambda: api.sf_apply_momentum(W, mbuf, U, V, wl.lr, wl.momentum, stream=stream), queued=True)
         M, N = spec.shape
         layers_mom.append({"tensor": spec.name, "alone_ms": round(ms, 4), "tflops": round(f / ms / 1e9, 2),
                            "gbs": round(4.0 * (4 * M * N + wl.K * (M + N)) / ms / 1e6, 1)})
@@ -289,7 +289,7 @@ def _ps_phase(wl, devt, schemes, launch_ms, time_fn, stream, pool, ksteps):
         return None
     ps_list = [(devt[i]["W"], devt[i]["shards"], devt[i].get("buf")) for i in reversed(ps_idx)]
     ps_it = api.SyncIteration(pool, [devt[i] for i in ps_idx], wl.B, wl.P, wl.lr, wl.momentum)
-    seq_ms = time_fn(lambda: ps_it(stream))
+    seq_ms = time_fn(lambda: ps_it(stream), queued=True)
     pool.set_timing(True)
     per = {}
     for _ in range(ksteps):
@@ -298,7 +298,7 @@ def _ps_phase(wl, devt, schemes, launch_ms, time_fn, stream, pool, ksteps):
             per[r["tensor"]] = per.get(r["tensor"], 0.0) + r["ms"] / ksteps
     pool.set_timing(False)
     torch.cuda.synchronize()
-    batch_ms = time_fn(lambda: api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream))
+    batch_ms = time_fn(lambda: api.ps_apply_batch(ps_list, wl.lr, wl.momentum, stream=stream), queued=True)
     step_bytes = sum(_ps_bytes(devt[i]["spec"], wl.P, "buf" in devt[i]) for i in ps_idx)
     in_iter = sum(launch_ms.get((api.PS, i), 0.0) for i in ps_idx) + launch_ms.get((api.PS, -1), 0.0)
     # The dominant PS launches: the tensors of the largest size (in VGG19 the
@@ -318,7 +318,7 @@ def _ps_phase(wl, devt, schemes, launch_ms, time_fn, stream, pool, ksteps):
             api.ps_apply(t["W"].view(-1), t["shards"].view(wl.P, -1), wl.lr, wl.momentum if "buf" in t else 0.0,
                          t.get("buf"), stream=stream)
 
-    b2b_ms = time_fn(big_seq) / len(bigs)
+    b2b_ms = time_fn(big_seq, queued=True) / len(bigs)
     gbs = big_bytes / b2b_ms / 1e6 if b2b_ms else None
     return {
         "roofline": {"bound": "hbm", "kernel": "ps_apply",
@@ -330,7 +330,8 @@ def _ps_phase(wl, devt, schemes, launch_ms, time_fn, stream, pool, ksteps):
                              f"the average duration of the {len(j_bigs)} launches of that size ({b2b_ms:.4f} ms; "
                              f"the largest PS tensors, {len(j_bigs) * big_bytes / step_bytes:.0%} of the step's PS "
                              f"bytes), launched back to back on one stream with nothing else running, as the "
-                             f"iteration issues them, between two HIP events on that stream",
+                             f"iteration issues them, between two HIP events on that stream (queued behind a "
+                             f"device-side wait, so that the events time the launches, not the host)",
                      "bracketed_ms": round(big_ms, 4) if big_ms else None,
                      "bracketed_note": "the same launches inside the library's PS-only iteration, each between "
                                        "its own pair of timing events (adds the events' own time)"},
@@ -514,10 +515,17 @@ def main():
     pool.set_timing(False)
     torch.cuda.synchronize()
 
-    def _time(fn):
+    def _time(fn, queued=False):
+        # queued: the events and fn's launches wait behind a device-side spin
+        # of about a millisecond, so that the events time the launches on the
+        # GPU and not the host enqueueing them (a Python call takes tens of
+        # microseconds; a batched call over 95 tensors, hundreds)
         out = []
         for rep in range(ksteps + 1):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            if queued:
+                with torch.cuda.stream(stream):
+                    torch.cuda._sleep(2_000_000)
             a.record(stream)
             fn()
             b.record(stream)
