@@ -70,9 +70,17 @@ def _ps_bytes(spec, P, momentum: bool):
 
 
 def _kernel_source_hash(name: str) -> str:
+    """sha256[:16] of a kernel source's code: comments and blank lines are
+    dropped and runs of whitespace collapsed, so that the stored counter
+    figures stay valid across edits of comments only."""
     import hashlib
+    import re
     path = os.path.join(ROOT, "paper_1706_03292_amd", "csrc", name)
-    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    src = open(path).read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    code = "\n".join(" ".join(line.split()) for line in src.splitlines() if line.strip())
+    return hashlib.sha256(code.encode()).hexdigest()[:16]
 
 
 def _stored_traffic(kernel: str, source: str):

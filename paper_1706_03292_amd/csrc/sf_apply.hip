@@ -593,7 +593,7 @@ __device__ __forceinline__ void sf_tile_staged(float* As, float* Bs, float* __re
 }
 
 // ---------------------------------------------------------------------------
-// Kernels.  OCC waves per SIMD: 4 for both tile shapes (128 VGPRs).
+// Kernels, compiled for at least 4 waves per SIMD (at most 128 VGPRs a wave).
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int BK, int WM, int WN, bool MOM>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
