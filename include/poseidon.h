@@ -409,8 +409,9 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * other kinds: PS).  Every tensor with work is one launch, in
  * backpropagation order: the SFB updates (bound by the matrix cores) on the
  * pool's first stream, the PS updates (bound by memory bandwidth) on its
- * second, so that the two kinds overlap; a one-stream pool runs everything in
- * order.  Two kinds of tensors share launches instead (with the kernels and
+ * second, so that the two kinds overlap; a one-stream pool, or an iteration
+ * whose work would take under 30 us at the kernels' rates (130 TFLOP/s for
+ * SFB, 5 TB/s for PS), runs everything in order on the first.  Two kinds of tensors share launches instead (with the kernels and
  * arithmetic of the single-tensor calls, so the same results): PS tensors of
  * fewer than 2^17 values, which a launch of their own would leave
  * latency-bound, are applied together, in backpropagation order, by one

@@ -137,7 +137,14 @@ namespace {
 // (VGG19-22K: neutral to 0.8% slower with the larger threshold).
 constexpr int64_t SMALL_PS_ELEMS = int64_t{1} << 17;
 constexpr int64_t PS_CRITICAL_ELEMS = int64_t{1} << 21;
-constexpr double SF_FLOPS_PER_PS_BYTE = 26.0;
+constexpr double SF_FLOPS_PER_S = 1.3e14;   // the two kernels' rates on this GPU
+constexpr double PS_BYTES_PER_S = 5.0e12;
+constexpr double SF_FLOPS_PER_PS_BYTE = SF_FLOPS_PER_S / PS_BYTES_PER_S;
+// An iteration whose work would take less than this on one stream is bound
+// by launch latency: the second stream's fork and join cost more than the
+// overlap gains (a 1024 x 512 FC layer and a 1M-value PS layer at P = 4:
+// 0.033 ms on one stream, 0.043-0.053 ms on two).
+constexpr double ONE_STREAM_BELOW_S = 30e-6;
 
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
 // for the work enqueued on `stream` before the call) and of
@@ -237,9 +244,11 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // Stream assignment: the compute-bound SF reconstructions go to the pool's
     // first stream, the bandwidth-bound PS applies to the second, in
     // backpropagation order, so that the two kinds overlap on the GPU instead
-    // of queueing behind each other.  A one-stream pool serialises everything.
+    // of queueing behind each other.  A one-stream pool, or an iteration too
+    // small to gain from the overlap, serialises everything on the first.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
-    const int32_t used = (S > 1 && launches > 1) ? 2 : 1;
+    const bool tiny = sf_flops / SF_FLOPS_PER_S + ps_bytes / PS_BYTES_PER_S < ONE_STREAM_BELOW_S;
+    const int32_t used = (S > 1 && launches > 1 && !tiny) ? 2 : 1;
     hipEvent_t waited[2] = {nullptr, nullptr};   // last ready event each used stream waits on
     if (!ready) {
         if (hipEventRecord(pool->fork, stream) != hipSuccess)

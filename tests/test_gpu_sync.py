@@ -215,3 +215,24 @@ def test_sync_iteration_batches_more_when_the_ps_applies_are_the_critical_path()
     assert sum(1 for i, s in sizes.items() if host[i]["spec"].kind != I.FC and s >= 1 << 21) == 2
     _oracle_check(host, devt, wl, schemes)
     pool.close()
+
+
+def test_sync_iteration_runs_a_latency_bound_iteration_on_one_stream():
+    """An iteration whose work would take under 30 us (the 1024 x 512 FC layer
+    and the 1M-value PS layer at P = 4) runs every launch on the pool's first
+    stream; results as the oracle's."""
+    d = dev()
+    wl = I.workload(1)
+    host = I.make_tensors(wl)
+    devt = _to_dev(host, d)
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    pool.set_timing(True)
+    log("sync_iteration latency-bound workload")
+    schemes = it()
+    recs = pool.launch_times()
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    assert len(recs) == 2 and all(r["stream"] == 0 for r in recs)
+    _oracle_check(host, devt, wl, schemes)
+    pool.close()
