@@ -430,7 +430,7 @@ def main():
     args = _parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        msg = ("bench.py measures one GPU: this build has no multi-GPU path "
+        msg = ("bench.py measures one GPU: the library has no multi-GPU path "
                f"(asked for --gpus {args.gpus}, WORLD_SIZE {world}). Run with --gpus 1.")
         print(msg, file=sys.stderr, flush=True)
         print(json.dumps({"metric": METRIC, "error": msg, "n_gpus": args.gpus}), flush=True)
