@@ -1,0 +1,78 @@
+"""Seeded random cases against the oracle: SF reconstruction (both tile
+paths, momentum or not, aligned or misaligned pointers) and PS applies (any
+P up to 40, sizes of every residue mod 4, single and batched launch), sized
+so that the oracle finishes each in well under a second."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from _helpers import BUF_TOL, W_TOL, assert_close, dev, log, misaligned, to_np
+from paper_1706_03292_amd import api
+from paper_1706_03292_amd import inputs as I
+
+pytestmark = pytest.mark.gpu
+
+
+def _sf_case(seed):
+    rng = np.random.default_rng(seed)
+    M, N = (int(x) for x in rng.integers(1, 700, 2))
+    K = int(rng.integers(1, 300))
+    if seed % 5 == 0:                      # 128 x 128 tiles need >= 2 tiles per CU
+        M, N = int(rng.integers(2049, 2300)), int(rng.integers(4097, 4300))
+        K = int(rng.integers(1, 40))
+    return M, N, K, bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_sf_random_shapes(seed):
+    d = dev()
+    M, N, K, mom, mis = _sf_case(seed)
+    W = I.randn(9000 + 5 * seed, (M, N), 0.01)
+    U = I.randn(9001 + 5 * seed, (K, M))
+    V = I.randn(9002 + 5 * seed, (K, N))
+    buf = I.randn(9003 + 5 * seed, (M, N), 1e-3)
+    log(f"sf random seed={seed} M={M} N={N} K={K} momentum={mom} misaligned={mis}")
+    place = (lambda t: misaligned(t.to(d))) if mis else (lambda t: t.to(d))
+    Wd, Ud, Vd = place(W), place(U), place(V)
+    if mom:
+        bd = place(buf)
+        api.sf_apply_momentum(Wd, bd, Ud, Vd, 0.01, 0.9)
+        w_ref, b_ref = oracle.sf_apply_momentum(W.numpy(), buf.numpy(), U.numpy(), V.numpy(), 0.01, 0.9)
+        torch.cuda.synchronize()
+        assert_close(to_np(bd), b_ref, BUF_TOL, "buf")
+    else:
+        api.sf_apply(Wd, Ud, Vd, 0.01)
+        w_ref = oracle.sf_apply(W.numpy(), U.numpy(), V.numpy(), 0.01)
+        torch.cuda.synchronize()
+    assert_close(to_np(Wd), w_ref, W_TOL, "W")
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_ps_random_shapes(seed):
+    d = dev()
+    rng = np.random.default_rng(500 + seed)
+    P = int(rng.integers(1, 41))
+    sizes = [int(x) for x in rng.integers(1, 20000, int(rng.integers(1, 6)))]
+    mu = float(rng.choice([0.0, 0.9]))
+    tens = []
+    for t, n in enumerate(sizes):
+        W = I.randn(9500 + 40 * seed + 4 * t, (n,), 0.01)
+        G = I.randn(9501 + 40 * seed + 4 * t, (P, n), 1e-3)
+        b = I.randn(9502 + 40 * seed + 4 * t, (n,), 1e-3) if mu else None
+        tens.append((W, G, b))
+    log(f"ps random seed={seed} P={P} sizes={sizes} momentum={mu}")
+    refs = [oracle.ps_apply(W.numpy(), G.numpy(), 0.01, mu, None if b is None else b.numpy()) for W, G, b in tens]
+    for how in ("single", "batch"):
+        dt = [(W.to(d) if t % 2 == 0 else misaligned(W.to(d)), G.to(d), None if b is None else b.to(d))
+              for t, (W, G, b) in enumerate(tens)]
+        if how == "single":
+            for W, G, b in dt:
+                api.ps_apply(W, G, 0.01, mu, b)
+        else:
+            api.ps_apply_batch(dt, 0.01, mu)
+        torch.cuda.synchronize()
+        for (W, G, b), (w_ref, b_ref) in zip(dt, refs):
+            assert_close(to_np(W), w_ref, W_TOL, f"W ({how})")
+            if b is not None:
+                assert_close(to_np(b), b_ref, BUF_TOL, f"buf ({how})")
