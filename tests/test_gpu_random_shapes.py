@@ -76,3 +76,50 @@ def test_ps_random_shapes(seed):
             assert_close(to_np(W), w_ref, W_TOL, f"W ({how})")
             if b is not None:
                 assert_close(to_np(b), b_ref, BUF_TOL, f"buf ({how})")
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_sync_iteration_random_networks(seed):
+    """Random layer lists (FC layers with factors and shards, with or without
+    a momentum buffer; PS tensors on both sides of the batching thresholds),
+    random P, B and pool size, with or without ready events: schemes exactly,
+    and every update, as the oracle's iteration."""
+    d = dev()
+    rng = np.random.default_rng(700 + seed)
+    P, B = int(rng.integers(2, 21)), int(rng.integers(1, 17))
+    K = P * B
+    host = []
+    for t in range(int(rng.integers(1, 9))):
+        base = 20000 + 100 * seed + 10 * t
+        if rng.random() < 0.4:
+            M, N = (int(x) for x in rng.integers(1, 600, 2))
+            host.append({"fc": True, "W": I.randn(base, (M, N), 0.01), "U": I.randn(base + 1, (K, M), 0.1),
+                         "V": I.randn(base + 2, (K, N), 0.1), "shards": I.randn(base + 3, (P, M * N), 1e-3),
+                         "buf": I.randn(base + 4, (M, N), 1e-3) if rng.random() < 0.3 else None})
+        else:
+            n = int(rng.choice([rng.integers(1, 5000), rng.integers(100000, 300000)]))
+            host.append({"fc": False, "W": I.randn(base, (n,), 0.01), "shards": I.randn(base + 3, (P, n), 1e-3),
+                         "buf": I.randn(base + 4, (n,), 1e-3) if rng.random() < 0.7 else None})
+    streams = int(rng.choice([1, 2, 4]))
+    wfbp = bool(rng.random() < 0.3)
+    devt = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items() if v is not None}
+            for h in host]
+    log(f"sync random seed={seed} P={P} B={B} layers={len(host)} streams={streams} wfbp={wfbp}")
+    pool = api.StreamPool(streams)
+    it = api.SyncIteration(pool, devt, B, P, 0.01, 0.9)
+    cs = torch.cuda.current_stream(d)
+    if wfbp:
+        ev = torch.cuda.Event()
+        ev.record(cs)
+        schemes = it(cs, ready=[ev] * len(devt))
+    else:
+        schemes = it(cs)
+    torch.cuda.synchronize()
+    ref = oracle.sync_iteration([{k: (v.numpy() if isinstance(v, torch.Tensor) else v) for k, v in h.items()}
+                                 for h in host], B, P, 0.01, 0.9)
+    for t, (g, r) in enumerate(zip(devt, ref)):
+        assert schemes[t] == r["scheme"], f"layer {t}: scheme"
+        assert_close(to_np(g["W"]).reshape(-1), r["W"].reshape(-1), W_TOL, f"layer {t} W")
+        if r["buf"] is not None:
+            assert_close(to_np(g["buf"]).reshape(-1), np.asarray(r["buf"]).reshape(-1), BUF_TOL, f"layer {t} buf")
+    pool.close()
