@@ -123,3 +123,50 @@ def test_sync_iteration_random_networks(seed):
         if r["buf"] is not None:
             assert_close(to_np(g["buf"]).reshape(-1), np.asarray(r["buf"]).reshape(-1), BUF_TOL, f"layer {t} buf")
     pool.close()
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_kv_store_random_layouts(seed):
+    """Random tensor lists, pair sizes, worker counts and ranks; each worker
+    delivers either one message or its per-tensor updates in a random order;
+    some tensors without a momentum buffer.  The store's pairs end as the
+    oracle store's, every other server's untouched."""
+    d = dev()
+    rng = np.random.default_rng(900 + seed)
+    P = int(rng.integers(1, 21))
+    rank = int(rng.integers(0, P))
+    pair = int(rng.integers(1, 3000))
+    sizes = [int(x) for x in rng.integers(0, 12000, int(rng.integers(1, 7)))]
+    tens = [(I.randn(30000 + 50 * seed + 3 * t, (n,), 0.01),
+             I.randn(30001 + 50 * seed + 3 * t, (n,), 1e-3) if rng.random() < 0.7 else None)
+            for t, n in enumerate(sizes)]
+    grads = [[I.randn(31000 + 500 * seed + 20 * p + t, (n,), 1e-3) for t, n in enumerate(sizes)] for p in range(P)]
+    by_msg = [bool(rng.random() < 0.5) for _ in range(P)]
+    events = [(p, None) for p in range(P) if by_msg[p]] + \
+             [(p, t) for p in range(P) if not by_msg[p] for t in range(len(sizes))]
+    rng.shuffle(events)
+    dt = [(W.to(d), None if b is None else b.to(d)) for W, b in tens]
+    dg = [[g.to(d) for g in gp] for gp in grads]
+    st = api.KVStore(dt, pair, P, rank, 0.01, 0.9)
+    ref = oracle.KVStore([(W.numpy(), None if b is None else b.numpy()) for W, b in tens], pair, P, rank, 0.01, 0.9)
+    log(f"kv random seed={seed} P={P} rank={rank} pair={pair} sizes={sizes} messages={sum(by_msg)}")
+    done = ref_done = 0
+    for p, t in events:
+        if t is None:
+            done += st.receive_message(p, api.kv_pack(dg[p], pair, P, rank))
+            ref_done += ref.receive_message(p, oracle.kv_pack([g.numpy() for g in grads[p]], pair, P, rank))
+        else:
+            done += st.receive(p, t, dg[p][t])
+            ref_done += ref.receive(p, t, grads[p][t].numpy())
+    torch.cuda.synchronize()
+    assert done == ref_done == sum(1 for *_, s in st.pairs if s == rank)
+    for j, (t, o, l, s) in enumerate(st.pairs):
+        sl = slice(o, o + l)
+        W, b = dt[t]
+        if s == rank:
+            assert_close(to_np(W)[sl], ref.W[t][sl], W_TOL, f"W pair {j}")
+            if b is not None:
+                assert_close(to_np(b)[sl], ref.buf[t][sl], BUF_TOL, f"buf pair {j}")
+        else:
+            assert np.array_equal(to_np(W)[sl], tens[t][0].numpy()[sl])
+    st.close()
