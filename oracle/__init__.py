@@ -38,7 +38,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# POSEIDON_ORACLE_LIB: another build of the same source (the mutation tests
+# load deliberately broken builds to show that the pins catch them).
+_LIB_PATH = os.environ.get("POSEIDON_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 _lib = None
 
 PS = 0
