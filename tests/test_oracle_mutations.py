@@ -38,6 +38,19 @@ MUTATIONS = [
 ]
 
 
+# The same for the oracle's Python side (the KV store's bookkeeping), planted
+# in a copy of oracle/__init__.py that the pin files import in a scratch tree.
+PY_MUTATIONS = [
+    ("pairs hashed per tensor instead of per pair",
+     "pairs.append((t, off, length, len(pairs) % P))", "pairs.append((t, off, length, t % P))"),
+    ("message slices read in the wrong order",
+     "mine = [j for j, pr in enumerate(self.pairs) if pr[3] == self.rank]\n        if message.size",
+     "mine = [j for j, pr in enumerate(self.pairs) if pr[3] == self.rank][::-1]\n        if message.size"),
+    ("the store drops the momentum buffer's decay",
+     "self.mu if buf is not None else 0.0", "0.0"),
+]
+
+
 def _build(src_text, out_dir):
     src = os.path.join(out_dir, "oracle.c")
     lib = os.path.join(out_dir, "liboracle.so")
@@ -66,4 +79,42 @@ def test_pins_catch_a_planted_mistake(name, edits, every, tmp_path):
         assert old in text, f"{name}: the source no longer contains {old!r}"
         text = text.replace(old, new) if every else text.replace(old, new, 1)
     r = _run_pins(_build(text, str(tmp_path)))
+    assert r.returncode == 1, f"{name}: no pin failed\n{r.stdout[-2000:]}"
+
+
+def _scratch_tree(tmp_path, init_text):
+    """tmp/oracle (the given __init__.py, the real C library), tmp/tests (the
+    pin files, conftest, golden fixtures) and the package, so that the pins
+    import this oracle."""
+    import shutil
+    root = tmp_path / "tree"
+    (root / "oracle").mkdir(parents=True)
+    (root / "oracle" / "__init__.py").write_text(init_text)
+    shutil.copy(os.path.join(ROOT, "oracle", "build.py"), root / "oracle" / "build.py")
+    (root / "tests").mkdir()
+    for f in ["conftest.py", *[os.path.basename(p) for p in PINS]]:
+        shutil.copy(os.path.join(ROOT, "tests", f), root / "tests" / f)
+    shutil.copytree(os.path.join(ROOT, "tests", "golden"), root / "tests" / "golden")
+    shutil.copy(os.path.join(ROOT, "pytest.ini"), root / "pytest.ini")
+    os.symlink(os.path.join(ROOT, "paper_1706_03292_amd"), root / "paper_1706_03292_amd")
+    return str(root)
+
+
+def _run_pins_in(tree):
+    env = dict(os.environ, POSEIDON_ORACLE_LIB=os.path.join(ROOT, "oracle", "liboracle.so"))
+    return subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider", *PINS],
+                          cwd=tree, env=env, capture_output=True, text=True, timeout=600)
+
+
+def test_unmodified_python_oracle_passes_the_pins_in_a_scratch_tree(tmp_path):
+    init = open(os.path.join(ROOT, "oracle", "__init__.py")).read()
+    r = _run_pins_in(_scratch_tree(tmp_path, init))
+    assert r.returncode == 0, r.stdout[-2000:]
+
+
+@pytest.mark.parametrize("name,old,new", PY_MUTATIONS, ids=[m[0] for m in PY_MUTATIONS])
+def test_pins_catch_a_planted_mistake_in_the_kv_store(name, old, new, tmp_path):
+    init = open(os.path.join(ROOT, "oracle", "__init__.py")).read()
+    assert old in init, f"{name}: the source no longer contains {old!r}"
+    r = _run_pins_in(_scratch_tree(tmp_path, init.replace(old, new, 1)))
     assert r.returncode == 1, f"{name}: no pin failed\n{r.stdout[-2000:]}"
