@@ -14,7 +14,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 SRC = os.path.join(ROOT, "oracle", "poseidon_oracle.c")
 PINS = ["tests/test_oracle_sfb.py", "tests/test_oracle_ps.py", "tests/test_oracle_hybcomm.py",
-        "tests/test_oracle_kv.py"]
+        "tests/test_oracle_kv.py", "tests/test_oracle_sync.py"]
 
 # (name, [(text in the source, replacement)], replace every occurrence)
 MUTATIONS = [
@@ -38,7 +38,8 @@ MUTATIONS = [
 ]
 
 
-# The same for the oracle's Python side (the KV store's bookkeeping), planted
+# The same for the oracle's Python side (the KV store's bookkeeping and the
+# whole-iteration routing), planted
 # in a copy of oracle/__init__.py that the pin files import in a scratch tree.
 PY_MUTATIONS = [
     ("pairs hashed per tensor instead of per pair",
@@ -48,6 +49,17 @@ PY_MUTATIONS = [
      "mine = [j for j, pr in enumerate(self.pairs) if pr[3] == self.rank][::-1]\n        if message.size"),
     ("the store drops the momentum buffer's decay",
      "self.mu if buf is not None else 0.0", "0.0"),
+    # the whole-iteration routing (Alg. 1 / Alg. 2)
+    ("every FC layer goes to SFB",
+     "scheme = best_scheme(True, M, N, B, P)", "scheme = SFB"),
+    ("an SFB layer's momentum buffer is ignored",
+     'if L.get("buf") is None:\n                out[l] = {"scheme": SFB',
+     'if True:\n                out[l] = {"scheme": SFB'),
+    ("a PS layer's momentum buffer is ignored",
+     'mu if L.get("buf") is not None else 0.0,\n                              L.get("buf"))',
+     '0.0, None)'),
+    ("layers synchronised in forward order",
+     "for l in range(len(layers) - 1, -1, -1):", "for l in range(len(layers)):"),
 ]
 
 
@@ -113,7 +125,7 @@ def test_unmodified_python_oracle_passes_the_pins_in_a_scratch_tree(tmp_path):
 
 
 @pytest.mark.parametrize("name,old,new", PY_MUTATIONS, ids=[m[0] for m in PY_MUTATIONS])
-def test_pins_catch_a_planted_mistake_in_the_kv_store(name, old, new, tmp_path):
+def test_pins_catch_a_planted_mistake_in_the_python_oracle(name, old, new, tmp_path):
     init = open(os.path.join(ROOT, "oracle", "__init__.py")).read()
     assert old in init, f"{name}: the source no longer contains {old!r}"
     r = _run_pins_in(_scratch_tree(tmp_path, init.replace(old, new, 1)))
