@@ -159,9 +159,11 @@ typedef struct poseidon_ps_tensor {
  * buf); tensors with n = 0 are skipped.  The work is issued as one launch per
  * group of up to 48 tensors of the same kind (with / without buffer), so that
  * small tensors do not each pay a kernel launch.  All tensors are validated
- * before anything is enqueued.  Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG
- * (as for poseidon_ps_apply, for any tensor; count < 0; NULL tensors with
- * count > 0) or POSEIDON_ERR_HIP.
+ * before anything is enqueued; the tensors are applied in parallel, so no
+ * tensor's W or buf may overlap another tensor's W, buf or shards (tensors may
+ * share shards).  Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (as for
+ * poseidon_ps_apply, for any tensor; count < 0; NULL tensors with count > 0;
+ * a W or buf overlapping another tensor's arrays) or POSEIDON_ERR_HIP.
  */
 int poseidon_ps_apply_batch(const poseidon_ps_tensor* tensors, int32_t count, int32_t P,
                             float lr, float momentum, hipStream_t stream);
@@ -409,9 +411,12 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * other kinds: PS).  Every tensor with work is one launch, in
  * backpropagation order: the SFB updates (bound by the matrix cores) on the
  * pool's first stream, the PS updates (bound by memory bandwidth) on its
- * second, so that the two kinds overlap; a one-stream pool, or an iteration
+ * second, so that the two kinds overlap; a one-stream pool, an iteration
  * whose work would take under 30 us at the kernels' rates (130 TFLOP/s for
- * SFB, 5 TB/s for PS), runs everything in order on the first.  Two kinds of tensors share launches instead (with the kernels and
+ * SFB, 5 TB/s for PS), or one whose two kinds would take comparable times at
+ * those rates (the smaller above 0.35 of the larger: neither leaves gaps the
+ * other could fill, so co-running only delays both) runs everything in order
+ * on the first.  Two kinds of tensors share launches instead (with the kernels and
  * arithmetic of the single-tensor calls, so the same results): PS tensors of
  * fewer than 2^17 values, which a launch of their own would leave
  * latency-bound, are applied together, in backpropagation order, by one
@@ -431,9 +436,12 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * the call behaves like one asynchronous operation on `stream` (the
  * bulk-synchronous barrier of Sec. 4.1 "Managing Consistency").
  * schemes (optional, count entries) receives each tensor's scheme.
- * All arguments are validated before anything is enqueued.  Returns
- * POSEIDON_OK, POSEIDON_ERR_INVALID_ARG, POSEIDON_ERR_PAYLOAD (the chosen
- * scheme's payload is NULL) or POSEIDON_ERR_HIP.
+ * All arguments are validated before anything is enqueued.  The updates run
+ * concurrently, so no tensor may write (W; buf when it has one) where another
+ * tensor reads or writes (W, buf, and the payload of its chosen scheme: U and
+ * V, or shards); tensors may share a payload.  Returns POSEIDON_OK,
+ * POSEIDON_ERR_INVALID_ARG (also for such an overlap), POSEIDON_ERR_PAYLOAD
+ * (the chosen scheme's payload is NULL) or POSEIDON_ERR_HIP.
  */
 int poseidon_sync_iteration(poseidon_stream_pool* pool,
                             const poseidon_tensor* tensors, int32_t count,

@@ -21,7 +21,8 @@ ADAM = 2
 KIND_FC = 0
 KIND_OTHER = 1
 
-EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply_batch", "poseidon_ps_apply", "poseidon_ps_apply_batch",
+EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply_batch",
+           "poseidon_ps_apply", "poseidon_ps_apply_batch",
            "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_hybcomm_cost_adam",
            "poseidon_hybcomm_choose3", "poseidon_pool_create",
            "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_sync_iteration_wfbp",

@@ -19,7 +19,7 @@ LIB = os.path.join(HERE, "libposeidon.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["sf_apply.hip", "ps_apply.hip", "sync.cpp", "hybcomm.cpp", "kvstore.cpp"]
+SOURCES = ["sf_apply.hip", "ps_apply.hip", "entry.cpp", "sync.cpp", "hybcomm.cpp", "kvstore.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-ffp-contract=off",

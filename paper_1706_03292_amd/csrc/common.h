@@ -4,6 +4,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+#include <vector>
+
 #include "poseidon.h"
 
 namespace poseidon {
@@ -19,6 +22,39 @@ inline bool overlaps(const void* a, int64_t abytes, const void* b, int64_t bbyte
     if (!a || !b || abytes <= 0 || bbytes <= 0) return false;
     const uintptr_t a0 = reinterpret_cast<uintptr_t>(a), b0 = reinterpret_cast<uintptr_t>(b);
     return a0 < b0 + static_cast<uintptr_t>(bbytes) && b0 < a0 + static_cast<uintptr_t>(abytes);
+}
+
+// A byte range [lo, hi) that a call reads or writes.
+struct Span {
+    uintptr_t lo;
+    uintptr_t hi;
+};
+
+inline void add_span(std::vector<Span>& v, const void* p, int64_t bytes)
+{
+    if (p && bytes > 0)
+        v.push_back(Span{reinterpret_cast<uintptr_t>(p), reinterpret_cast<uintptr_t>(p) + static_cast<uintptr_t>(bytes)});
+}
+
+// True when two written ranges overlap, or a read range overlaps a written
+// one.  Read ranges may overlap each other (several tensors may share an
+// input).  Sorting the written ranges makes it O((w + r) log w).
+inline bool writes_collide(std::vector<Span> writes, const std::vector<Span>& reads)
+{
+    std::sort(writes.begin(), writes.end(), [](const Span& a, const Span& b) { return a.lo < b.lo; });
+    for (size_t i = 1; i < writes.size(); ++i)
+        if (writes[i].lo < writes[i - 1].hi)
+            return true;
+    // The written ranges are now disjoint and sorted, so their ends are
+    // sorted too: a read range meets one iff it meets the last one that
+    // starts before the read range ends.
+    for (const Span& r : reads) {
+        auto it = std::lower_bound(writes.begin(), writes.end(), r.hi,
+                                   [](const Span& w, uintptr_t hi) { return w.lo < hi; });
+        if (it != writes.begin() && std::prev(it)->hi > r.lo)
+            return true;
+    }
+    return false;
 }
 
 // Number of compute units of the current device (cached per device).

@@ -503,50 +503,4 @@ hipError_t launch_kv_pack(const float* const* src, const int64_t* dst, const int
     return hipSuccess;
 }
 
-int check_ps_args(const float* W, const float* shards, int32_t P, int64_t n,
-                  float momentum, const float* buf)
-{
-    if (P < 1 || n < 0)
-        return POSEIDON_ERR_INVALID_ARG;
-    if (n == 0)
-        return POSEIDON_OK;
-    if (!W || !shards || (!buf && momentum != 0.0f))
-        return POSEIDON_ERR_INVALID_ARG;
-    if (n > (INT64_MAX / 4) / P)
-        return POSEIDON_ERR_INVALID_ARG;
-    const int64_t wb = n * 4, gb = n * 4 * static_cast<int64_t>(P);
-    if (overlaps(W, wb, shards, gb) || overlaps(buf, wb, shards, gb) || overlaps(W, wb, buf, wb))
-        return POSEIDON_ERR_INVALID_ARG;
-    return POSEIDON_OK;
-}
-
 }  // namespace poseidon
-
-extern "C" int poseidon_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
-                                 float lr, float momentum, float* buf, hipStream_t stream)
-{
-    const int rc = poseidon::check_ps_args(W, shards, P, n, momentum, buf);
-    if (rc != POSEIDON_OK || n == 0)
-        return rc;
-    return poseidon::launch_ps_apply(W, shards, P, n, lr, momentum, buf, stream) == hipSuccess
-               ? POSEIDON_OK
-               : POSEIDON_ERR_HIP;
-}
-
-extern "C" int poseidon_ps_apply_batch(const poseidon_ps_tensor* tensors, int32_t count, int32_t P,
-                                       float lr, float momentum, hipStream_t stream)
-{
-    if (count < 0 || (count > 0 && !tensors) || P < 1)
-        return POSEIDON_ERR_INVALID_ARG;
-    for (int32_t i = 0; i < count; ++i) {
-        const poseidon_ps_tensor& x = tensors[i];
-        const int rc = poseidon::check_ps_args(x.W, x.shards, P, x.n, x.buf ? momentum : 0.0f, x.buf);
-        if (rc != POSEIDON_OK)
-            return rc;
-    }
-    static_assert(sizeof(poseidon_ps_tensor) == sizeof(poseidon::PsTensor), "descriptor layout");
-    return poseidon::launch_ps_apply_batch(reinterpret_cast<const poseidon::PsTensor*>(tensors), count, P, lr,
-                                           momentum, stream) == hipSuccess
-               ? POSEIDON_OK
-               : POSEIDON_ERR_HIP;
-}

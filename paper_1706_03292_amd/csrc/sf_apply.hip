@@ -781,88 +781,4 @@ hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, fl
     return hipSuccess;
 }
 
-int check_sf_args(const float* W, const float* U, const float* V,
-                  int64_t M, int64_t N, int64_t K)
-{
-    if (M < 0 || N < 0 || K < 0)
-        return POSEIDON_ERR_INVALID_ARG;
-    if (M == 0 || N == 0 || K == 0)
-        return POSEIDON_OK;
-    if (!W || !U || !V)
-        return POSEIDON_ERR_INVALID_ARG;
-    if (M > INT64_MAX / 4 / N || K > INT64_MAX / 4 / M || K > INT64_MAX / 4 / N)
-        return POSEIDON_ERR_INVALID_ARG;
-    const int64_t wb = M * N * 4;
-    if (overlaps(W, wb, U, K * M * 4) || overlaps(W, wb, V, K * N * 4))
-        return POSEIDON_ERR_INVALID_ARG;
-    return POSEIDON_OK;
-}
-
-int check_sf_momentum_args(const float* W, const float* buf, const float* U, const float* V,
-                           int64_t M, int64_t N, int64_t K)
-{
-    if (M < 0 || N < 0 || K < 0)
-        return POSEIDON_ERR_INVALID_ARG;
-    if (M == 0 || N == 0)
-        return POSEIDON_OK;
-    if (!W || !buf || (K > 0 && (!U || !V)))
-        return POSEIDON_ERR_INVALID_ARG;
-    if (M > INT64_MAX / 4 / N || K > INT64_MAX / 4 / M || K > INT64_MAX / 4 / N)
-        return POSEIDON_ERR_INVALID_ARG;
-    const int64_t wb = M * N * 4;
-    if (overlaps(W, wb, buf, wb) || overlaps(W, wb, U, K * M * 4) || overlaps(W, wb, V, K * N * 4) ||
-        overlaps(buf, wb, U, K * M * 4) || overlaps(buf, wb, V, K * N * 4))
-        return POSEIDON_ERR_INVALID_ARG;
-    return POSEIDON_OK;
-}
-
 }  // namespace poseidon
-
-extern "C" int poseidon_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M,
-                                          int64_t N, int64_t K, float lr, float momentum, hipStream_t stream)
-{
-    const int rc = poseidon::check_sf_momentum_args(W, buf, U, V, M, N, K);
-    if (rc != POSEIDON_OK || M == 0 || N == 0)
-        return rc;
-    return poseidon::launch_sf_apply_momentum(W, buf, U, V, M, N, K, lr, momentum, stream) == hipSuccess
-               ? POSEIDON_OK
-               : POSEIDON_ERR_HIP;
-}
-
-extern "C" int poseidon_sf_apply(float* W, const float* U, const float* V,
-                                 int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream)
-{
-    const int rc = poseidon::check_sf_args(W, U, V, M, N, K);
-    if (rc != POSEIDON_OK || M == 0 || N == 0 || K == 0)
-        return rc;
-    return poseidon::launch_sf_apply(W, U, V, M, N, K, lr, stream) == hipSuccess
-               ? POSEIDON_OK
-               : POSEIDON_ERR_HIP;
-}
-
-extern "C" int poseidon_sf_apply_batch(const poseidon_sf_tensor* layers, int32_t count, int64_t K, float lr,
-                                       hipStream_t stream)
-{
-    if (count < 0 || (count > 0 && !layers) || K < 0)
-        return POSEIDON_ERR_INVALID_ARG;
-    for (int32_t i = 0; i < count; ++i) {
-        const poseidon_sf_tensor& x = layers[i];
-        const int rc = poseidon::check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
-        if (rc != POSEIDON_OK)
-            return rc;
-        for (int32_t j = 0; j < count; ++j) {   // no W may overlap another layer's W, U or V
-            if (j == i)
-                continue;
-            const poseidon_sf_tensor& y = layers[j];
-            const int64_t wb = x.M * x.N * 4;
-            if (poseidon::overlaps(x.W, wb, y.W, y.M * y.N * 4) || poseidon::overlaps(x.W, wb, y.U, K * y.M * 4) ||
-                poseidon::overlaps(x.W, wb, y.V, K * y.N * 4))
-                return POSEIDON_ERR_INVALID_ARG;
-        }
-    }
-    static_assert(sizeof(poseidon_sf_tensor) == sizeof(poseidon::SfTensor), "descriptor layout");
-    return poseidon::launch_sf_apply_batch(reinterpret_cast<const poseidon::SfTensor*>(layers), count, K, lr,
-                                           stream) == hipSuccess
-               ? POSEIDON_OK
-               : POSEIDON_ERR_HIP;
-}

@@ -7,6 +7,7 @@
 // stream (the bulk-synchronous barrier).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <vector>
 
@@ -145,6 +146,17 @@ constexpr double SF_FLOPS_PER_PS_BYTE = SF_FLOPS_PER_S / PS_BYTES_PER_S;
 // overlap gains (a 1024 x 512 FC layer and a 1M-value PS layer at P = 4:
 // 0.033 ms on one stream, 0.043-0.053 ms on two).
 constexpr double ONE_STREAM_BELOW_S = 30e-6;
+// Two streams pay when one kind of update is small next to the other: the
+// small one's launches fill the gaps the large one leaves (its tile rounds'
+// ends, the last partial round), and take little from it.  When the two are
+// of comparable size neither has gaps to fill, and the co-running launches
+// only delay each other: the 4096 x 4096 layer rebuilt at K = 256 (one round
+// of tiles, 0.083 ms alone) beside 805 MB of PS applies (0.139 ms alone)
+// took 0.236 ms on two streams against 0.222 ms one after the other.  Below
+// this ratio of the smaller estimated time to the larger the iteration uses
+// two streams (VGG19-22K: 0.19; the Inception-shaped workload: 0.05;
+// that 4096 x 4096 layer through both schemes: 0.41).
+constexpr double CORUN_MAX_RATIO = 0.35;
 
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
 // for the work enqueued on `stream` before the call) and of
@@ -195,6 +207,30 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         if (ready && !ready[t])
             return POSEIDON_ERR_INVALID_ARG;
         plan[static_cast<size_t>(t)] = scheme;
+    }
+    // The tensors' updates run concurrently (two streams, batched and grouped
+    // launches): no tensor may write where another one reads or writes.
+    {
+        std::vector<Span> writes, reads;
+        for (int32_t t = 0; t < count; ++t) {
+            const poseidon_tensor& x = tensors[t];
+            const int64_t n = x.M * x.N;
+            if (n == 0)
+                continue;
+            add_span(writes, x.W, n * 4);
+            if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
+                if (x.buf)
+                    add_span(writes, x.buf, n * 4);
+                add_span(reads, x.U, K * x.M * 4);
+                add_span(reads, x.V, K * x.N * 4);
+            } else {
+                if (x.buf)
+                    add_span(writes, x.buf, n * 4);
+                add_span(reads, x.shards, n * 4 * static_cast<int64_t>(P));
+            }
+        }
+        if (writes_collide(std::move(writes), reads))
+            return POSEIDON_ERR_INVALID_ARG;
     }
     if (schemes)
         for (int32_t t = 0; t < count; ++t)
@@ -247,8 +283,12 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // of queueing behind each other.  A one-stream pool, or an iteration too
     // small to gain from the overlap, serialises everything on the first.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
-    const bool tiny = sf_flops / SF_FLOPS_PER_S + ps_bytes / PS_BYTES_PER_S < ONE_STREAM_BELOW_S;
-    const int32_t used = (S > 1 && launches > 1 && !tiny) ? 2 : 1;
+    const double t_sf = sf_flops / SF_FLOPS_PER_S, t_ps = ps_bytes / PS_BYTES_PER_S;
+    const bool tiny = t_sf + t_ps < ONE_STREAM_BELOW_S;
+    // With ready events the second stream also lets the updates start while
+    // the caller's backward pass still runs, so it is kept.
+    const bool balanced = !ready && std::min(t_sf, t_ps) > CORUN_MAX_RATIO * std::max(t_sf, t_ps);
+    const int32_t used = (S > 1 && launches > 1 && !tiny && !balanced) ? 2 : 1;
     hipEvent_t waited[2] = {nullptr, nullptr};   // last ready event each used stream waits on
     if (!ready) {
         if (hipEventRecord(pool->fork, stream) != hipSuccess)

@@ -249,3 +249,27 @@ def test_ps_apply_shards_beyond_32bit_offsets():
         torch.cuda.synchronize()
         assert_close(to_np(Wd)[idx], w_ref, W_TOL, f"W ({how})")
         assert_close(to_np(bd)[idx], b_ref, BUF_TOL, f"buf ({how})")
+
+
+def test_ps_apply_batch_rejects_tensors_that_write_into_each_other():
+    """The tensors of a batched launch are applied in parallel: a W or buf
+    overlapping another tensor's W, buf or shards is an argument error;
+    shards shared between tensors are fine."""
+    d = dev()
+    P, n = 4, 1000
+    base = torch.zeros(4 * n, device=d)
+    G = torch.randn(P, n, device=d)
+    log("ps_apply_batch overlap checks")
+    api.ps_apply_batch([(base[:n], G, None), (base[n:2 * n], G, None)], 0.1)        # shared shards
+    torch.cuda.synchronize()
+    bad = [
+        [(base[:n], G, None), (base[n - 1:2 * n - 1], torch.zeros(P, n, device=d), None)],
+        [(base[:n], G, base[2 * n:3 * n]), (base[2 * n + 3:3 * n + 3], torch.zeros(P, n, device=d), None)],
+        [(base[:n], G, None), (G.view(-1)[n:2 * n], torch.zeros(P, n, device=d), None)],
+        [(base[:n], G, None), (base[n:2 * n], torch.zeros(P, n, device=d), G.view(-1)[:n])],
+    ]
+    for i, ts in enumerate(bad):
+        with pytest.raises(api.PoseidonError) as e:
+            api.ps_apply_batch(ts, 0.1, 0.9 if any(b is not None for _, _, b in ts) else 0.0)
+        assert e.value.status == api.ERR_INVALID_ARG, i
+    torch.cuda.synchronize()

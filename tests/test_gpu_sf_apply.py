@@ -121,19 +121,21 @@ def test_sf_apply_rejects_cpu_and_bad_shapes():
         api.sf_apply(W.to(d).double(), U.to(d), V.to(d), 0.1)
 
 
-@pytest.mark.parametrize("name", ["fc6.W", "fc7.W", "fc8.W"])
-def test_sf_apply_vgg19_22k_full_size_sampled(name):
-    """The VGG19-22K FC layers at full size (P=16, B=32, K=512), checked at
-    sampled points, the corners and stretches of the ragged last row/column."""
+@pytest.mark.parametrize("cfg,name", [(5, "fc6.W"), (5, "fc7.W"), (5, "fc8.W"), (2, "fc7.W")])
+def test_sf_apply_full_size_sampled(cfg, name):
+    """The VGG19-22K FC layers at full size (P=16, B=32, K=512), and the
+    4096 x 4096 layer of Sec. 3.2's worked example at P=8, B=32 (K=256, factors
+    ~N(0,1) unscaled), checked at sampled points, the corners and stretches of
+    the ragged last row/column; then the raw gradient at the same points."""
     d = dev()
-    wl = I.workload(5)
+    wl = I.workload(cfg)
     t = I.make_tensors(wl, only=[name])[0]
     W, U, V = t["W"], t["U"], t["V"]
     M, N = W.shape
     rows, cols = sample_points(M, N, 4000, seed=M + N)
     ref = oracle.sf_apply_points(W.numpy(), U.numpy(), V.numpy(), wl.lr, rows, cols)
     Wd = W.to(d)
-    log(f"sf_apply full {name} {M}x{N} K={wl.K}")
+    log(f"sf_apply full config {cfg} {name} {M}x{N} K={wl.K}")
     api.sf_apply(Wd, U.to(d), V.to(d), wl.lr)
     torch.cuda.synchronize()
     got = to_np(Wd)[rows, cols]

@@ -60,7 +60,8 @@ def _to_dev(host, d):
     return out
 
 
-@pytest.mark.parametrize("cfg,streams", [(1, 1), (1, 4), (3, 4), (4, 4), (5, 2), (5, 4), (5, 1), (5, 8)])
+@pytest.mark.parametrize("cfg,streams", [(1, 1), (1, 4), (2, 2), (2, 1), (3, 4), (4, 4), (5, 2), (5, 4), (5, 1),
+                                         (5, 8)])
 def test_sync_iteration_matches_oracle(cfg, streams):
     d = dev()
     wl = I.workload(cfg)
@@ -234,5 +235,66 @@ def test_sync_iteration_runs_a_latency_bound_iteration_on_one_stream():
     pool.set_timing(False)
     torch.cuda.synchronize()
     assert len(recs) == 2 and all(r["stream"] == 0 for r in recs)
+    _oracle_check(host, devt, wl, schemes)
+    pool.close()
+
+
+def test_sync_iteration_rejects_tensors_that_write_into_each_other():
+    """The updates of one iteration run concurrently (two streams, batched
+    and grouped launches), so no tensor may write where another reads or
+    writes; tensors may share a read-only payload."""
+    d = dev()
+    pool = api.StreamPool(2)
+    P, B = 4, 16
+    n = 1 << 12
+    G = torch.zeros(P, n, device=d)
+    base = torch.zeros(4 * n, device=d)
+    W1, W2 = base[:n], base[n:2 * n]
+    U, V = torch.zeros(P * B, 1024, device=d), torch.zeros(P * B, 512, device=d)
+    Wfc = torch.zeros(1024, 512, device=d)
+    ok = [{"fc": False, "W": W1, "shards": G}, {"fc": False, "W": W2, "shards": G}]   # shared shards: fine
+    log("sync_iteration overlap checks")
+    api.SyncIteration(pool, ok, B, P, 0.01)()
+    torch.cuda.synchronize()
+    cases = {
+        "two tensors share W": [{"fc": False, "W": W1, "shards": G}, {"fc": False, "W": base[n // 2:n // 2 + n],
+                                                                       "shards": G}],
+        "W inside another tensor's shards": [{"fc": False, "W": W1, "shards": G},
+                                             {"fc": False, "W": G.view(-1)[:n], "shards": G[:, :].clone()}],
+        "buf inside another tensor's W": [{"fc": False, "W": W1, "shards": G, "buf": base[2 * n:3 * n]},
+                                          {"fc": False, "W": base[2 * n + 8:3 * n + 8],
+                                           "shards": torch.zeros(P, n, device=d)}],
+        "PS W inside an SFB layer's U": [{"fc": True, "W": Wfc, "U": U, "V": V},
+                                         {"fc": False, "W": U.view(-1)[:n], "shards": G}],
+        "SFB W over a PS tensor's buf": [{"fc": True, "W": Wfc, "U": U, "V": V},
+                                         {"fc": False, "W": W1, "shards": G, "buf": Wfc.view(-1)[:n]}],
+    }
+    for name, ts in cases.items():
+        it = api.SyncIteration(pool, ts, B, P, 0.01, 0.9)
+        with pytest.raises(api.PoseidonError) as e:
+            it()
+        assert e.value.status == api.ERR_INVALID_ARG, name
+    torch.cuda.synchronize()
+    pool.close()
+
+
+def test_sync_iteration_runs_comparable_kinds_on_one_stream():
+    """The 4096 x 4096 layer rebuilt from its factors beside the same layer's
+    805 MB of dense shards: the two kinds are of comparable size, so co-running
+    them only delays both, and the iteration issues them one after the other
+    on the pool's first stream; results as the oracle's."""
+    d = dev()
+    wl = I.workload(2)
+    host = I.make_tensors(wl)
+    devt = _to_dev(host, d)
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    pool.set_timing(True)
+    log("sync_iteration comparable SFB and PS work")
+    schemes = it()
+    recs = pool.launch_times()
+    pool.set_timing(False)
+    torch.cuda.synchronize()
+    assert [(r["scheme"], r["stream"]) for r in recs] == [(api.PS, 0), (api.SFB, 0)]
     _oracle_check(host, devt, wl, schemes)
     pool.close()
