@@ -1,0 +1,128 @@
+// The per-group update of the parameter-server apply (Sec. 2.1 "Parameter
+// Server"; Sec. 4.1 "KV Store"), shared by every kernel that applies dense
+// updates: the single-tensor, batched and KV-store launches and the grouped
+// launch that co-schedules the applies with the SF reconstruction.
+//
+//   s_i = sum_{p<P} G_p[i]   (p increasing, fp32)
+//   buf_i = fma(mu, buf_i, s_i);  W_i = fma(-lr, buf_i, W_i)
+//
+// A thread owns one group of four consecutive elements and issues all of its
+// shard loads before the dependent adds; 16-byte accesses, aligned (AL) or at
+// 4-byte alignment, all non-temporal (each array is touched once).
+#pragma once
+
+#include "common.h"
+
+namespace poseidon {
+
+constexpr int PS_CHUNK = 8;   // shard loads in flight per step when P is a runtime value
+
+typedef float f4u __attribute__((ext_vector_type(4), aligned(4)));   // 16 bytes at a 4-byte boundary
+
+__device__ inline f4 fma4(float a, f4 b, f4 c)
+{
+    return f4{fmaf(a, b.x, c.x), fmaf(a, b.y, c.y), fmaf(a, b.z, c.z), fmaf(a, b.w, c.w)};
+}
+
+template <bool AL>
+__device__ inline f4 ld4(const float* p)
+{
+    if constexpr (AL)
+        return __builtin_nontemporal_load(reinterpret_cast<const f4*>(p));
+    else
+        return __builtin_nontemporal_load(reinterpret_cast<const f4u*>(p));
+}
+
+template <bool AL>
+__device__ inline void st4(float* p, f4 v)
+{
+    if constexpr (AL)
+        __builtin_nontemporal_store(v, reinterpret_cast<f4*>(p));
+    else
+        __builtin_nontemporal_store(v, reinterpret_cast<f4u*>(p));
+}
+
+// Where worker p's values of a tensor start: P contiguous shards ...
+struct Contiguous {
+    const float* G;
+    int64_t n;
+    __device__ const float* operator()(int p) const { return G + static_cast<int64_t>(p) * n; }
+};
+
+// ... or one pointer per worker (the KV store): a whole-tensor update, or a
+// message whose values for this range sit `delta` elements further on (bit p
+// of msg_mask set).
+struct PerWorker {
+    const float* const* g;
+    uint64_t msg_mask;
+    int64_t delta;
+    __device__ const float* operator()(int p) const { return g[p] + (((msg_mask >> p) & 1) ? delta : 0); }
+};
+
+// Sum of the P values of elements e .. e+3, in increasing p.
+template <int PT, bool AL, class Src>
+__device__ inline f4 sum4(const Src& src, int P, int64_t e)
+{
+    if constexpr (PT > 0) {
+        f4 g[PT];
+#pragma unroll
+        for (int p = 0; p < PT; ++p)
+            g[p] = ld4<AL>(src(p) + e);
+        f4 s = g[0];
+#pragma unroll
+        for (int p = 1; p < PT; ++p)
+            s += g[p];
+        return s;
+    } else {
+        f4 s = ld4<AL>(src(0) + e);
+        int p = 1;
+        for (; p + PS_CHUNK <= P; p += PS_CHUNK) {
+            f4 g[PS_CHUNK];
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                g[c] = ld4<AL>(src(p + c) + e);
+#pragma unroll
+            for (int c = 0; c < PS_CHUNK; ++c)
+                s += g[c];
+        }
+        for (; p < P; ++p)
+            s += ld4<AL>(src(p) + e);
+        return s;
+    }
+}
+
+// The update of elements e .. min(e + 4, end) - 1 of one tensor.
+template <int PT, bool MOM, bool AL, class Src>
+__device__ inline void apply_group(float* __restrict__ W, float* __restrict__ buf, const Src& src, int P, int64_t e,
+                                   int64_t end, float lr, float mu)
+{
+    if (e + 3 < end) {
+        const f4 s = sum4<PT, AL>(src, P, e);
+        f4 w = ld4<AL>(W + e);
+        if constexpr (MOM) {
+            const f4 b = fma4(mu, ld4<AL>(buf + e), s);
+            st4<AL>(buf + e, b);
+            w = fma4(-lr, b, w);
+        } else {
+            w = fma4(-lr, s, w);
+        }
+        st4<AL>(W + e, w);
+    } else {
+        for (int64_t k = e; k < end; ++k) {
+            float s = src(0)[k];
+            for (int p = 1; p < (PT > 0 ? PT : P); ++p)
+                s += src(p)[k];
+            float w = W[k];
+            if constexpr (MOM) {
+                const float b = fmaf(mu, buf[k], s);
+                buf[k] = b;
+                w = fmaf(-lr, b, w);
+            } else {
+                w = fmaf(-lr, s, w);
+            }
+            W[k] = w;
+        }
+    }
+}
+
+}  // namespace poseidon

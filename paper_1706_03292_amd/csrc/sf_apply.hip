@@ -117,7 +117,7 @@ __device__ __forceinline__ void load_w_block(float (&wv)[16], __amdgpu_buffer_rs
 
 // Interior tile: one shared lane offset (voff) and uniform row offsets, one
 // MFMA block at a time; the first W_PRE values of block 0 are already in wv.
-template <int TM, int TN>
+template <int TM, int TN, int PRE>
 __device__ __forceinline__ void epi_interior(const f16v (&acc)[TM][TN], float (&wv)[16], __amdgpu_buffer_rsrc_t wr,
                                              int voff, int n4, float lr)
 {
@@ -125,7 +125,7 @@ __device__ __forceinline__ void epi_interior(const f16v (&acc)[TM][TN], float (&
     for (int c = 0; c < TM * TN; ++c) {
         const int i = c / TN, j = c % TN;
 #pragma unroll
-        for (int r = (c == 0 ? W_PRE : 0); r < 16; ++r)
+        for (int r = (c == 0 ? PRE : 0); r < 16; ++r)
             wv[r] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
                 wr, voff + 128 * j, acc_row(i, r) * n4, 0));
 #pragma unroll
@@ -250,9 +250,9 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(float* base, int64_t
                                              BUF_RSRC_WORD3);
 }
 
-// The epilogue of one tile for offsets that fit 31 bits.  PREF: the caller
-// has loaded block 0 of an interior tile into wv.
-template <int TM, int TN, bool MOM>
+// The epilogue of one tile for offsets that fit 31 bits.  On an interior
+// tile the caller has loaded the first PRE values of block 0 into wv.
+template <int TM, int TN, bool MOM, int PRE = W_PRE>
 __device__ __forceinline__ void epilogue(const f16v (&acc)[TM][TN], float (&wv)[16], __amdgpu_buffer_rsrc_t wr,
                                          float* __restrict__ buf, int64_t M, int64_t N, int64_t m0, int64_t n0,
                                          int BM, int BN, int wm, int wn, int lrow, int lcol, bool interior,
@@ -268,7 +268,7 @@ __device__ __forceinline__ void epilogue(const f16v (&acc)[TM][TN], float (&wv)[
         else
             epi_momentum<TM, TN>(acc, wr, br, ni, wm, wn, lrow, lcol, rows_left, cols_left, lr, mu);
     } else if (interior) {
-        epi_interior<TM, TN>(acc, wv, wr, ((wm + 4 * lrow) * ni + wn + lcol) * 4, ni * 4, lr);
+        epi_interior<TM, TN, PRE>(acc, wv, wr, ((wm + 4 * lrow) * ni + wn + lcol) * 4, ni * 4, lr);
     } else {
         epi_edge<TM, TN>(acc, wr, ni, wm, wn, lrow, lcol, rows_left, cols_left, lr);
     }
@@ -393,8 +393,9 @@ struct Direct {
 
 // One BM x BN tile of W: the whole K loop and the fused update.  Slice kt
 // lives in stage (nkt-1-kt) & 1, so the last slice is always in stage 0 and
-// the loop body and the final step are each emitted once.
-template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+// the loop body and the final step are each emitted once.  An interior tile
+// loads PRE values of W ahead of the last K step.
+template <int BM, int BN, int BK, int WM, int WN, bool MOM, int PRE = W_PRE>
 __device__ __forceinline__ void sf_tile_direct(float* __restrict__ W, const float* __restrict__ U,
                                                const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
                                                float lr, int tm, int tn, float* __restrict__ buf, float mu)
@@ -441,10 +442,10 @@ __device__ __forceinline__ void sf_tile_direct(float* __restrict__ W, const floa
         wait_loads();
         __syncthreads();
         if (!MOM && interior)
-            load_w_block(wv, wr, voff, ni * 4, 0, W_PRE);
+            load_w_block(wv, wr, voff, ni * 4, 0, PRE);
         D::template mma<0>(acc, wm, wn, lane);
     }
-    epilogue<T::TM, T::TN, MOM>(acc, wv, wr, buf, M, N, m0, n0, BM, BN, wm, wn, lrow, lcol, interior, lr, mu);
+    epilogue<T::TM, T::TN, MOM, PRE>(acc, wv, wr, buf, M, N, m0, n0, BM, BN, wm, wn, lrow, lcol, interior, lr, mu);
 }
 
 // ---------------------------------------------------------------------------
@@ -645,14 +646,11 @@ struct SfBatchArgs {
     int32_t total_tiles;
 };
 
-template <int BM, int BN, int BK, int WM, int WN>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K, float lr)
+// Tile t of the combined list (layer by layer; inside a layer tile rows
+// walked 8 at a time).
+template <int BM, int BN, int BK, int WM, int WN, int PRE = W_PRE>
+__device__ __forceinline__ void batch_tile(const SfBatchArgs& args, int t, int64_t K, float lr)
 {
-    const int tiles = args.total_tiles;
-    const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
-    const int x = blockIdx.x % NUM_XCD, j = blockIdx.x / NUM_XCD;
-    const int t = x * q + (x < r ? x : r) + j;
     int l = 0;
     while (l + 1 < args.count && t >= args.item[l + 1].first_tile)
         ++l;
@@ -665,8 +663,18 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_batch_kernel(const SfBa
     const int rows = (tiles_m - first_m) < G ? (tiles_m - first_m) : G;
     const int in = local - g * per_group;
     const SfBatchItem& it = args.item[l];
-    sf_tile_direct<BM, BN, BK, WM, WN, false>(it.W, it.U, it.V, it.M, it.N, K, lr, first_m + in % rows, in / rows,
-                                              nullptr, 0.f);
+    sf_tile_direct<BM, BN, BK, WM, WN, false, PRE>(it.W, it.U, it.V, it.M, it.N, K, lr, first_m + in % rows,
+                                                   in / rows, nullptr, 0.f);
+}
+
+template <int BM, int BN, int BK, int WM, int WN>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K, float lr)
+{
+    const int tiles = args.total_tiles;
+    const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
+    const int x = blockIdx.x % NUM_XCD, j = blockIdx.x / NUM_XCD;
+    batch_tile<BM, BN, BK, WM, WN>(args, x * q + (x < r ? x : r) + j, K, lr);
 }
 
 // True when the LDS-direct tile's 32-bit buffer offsets cover the layer: the
@@ -780,5 +788,6 @@ hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, fl
     }
     return hipSuccess;
 }
+
 
 }  // namespace poseidon

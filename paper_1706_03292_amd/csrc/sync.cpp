@@ -237,6 +237,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
             schemes[t] = plan[static_cast<size_t>(t)];
     // With ready events each large tensor keeps its own launch, so that it
     // starts as soon as its own backward pass has run.
+    const double t_sf = sf_flops / SF_FLOPS_PER_S, t_ps = ps_bytes / PS_BYTES_PER_S;
     const int64_t small_elems =
         (!ready && sf_flops < SF_FLOPS_PER_PS_BYTE * ps_bytes) ? PS_CRITICAL_ELEMS : SMALL_PS_ELEMS;
     int32_t active = 0;
@@ -267,6 +268,13 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // next layer's (VGG19-22K iteration: 1.75 vs 1.78 ms, A/B in alternating
     // processes).  With ready events every SFB layer keeps its own launch, so
     // that each starts as soon as its own backward pass has run.
+    std::vector<SfTensor> grouped;   // in backpropagation order
+    if (!ready)
+        for (int32_t t = count - 1; t >= 0; --t) {
+            const poseidon_tensor& x = tensors[t];
+            if (plan[static_cast<size_t>(t)] == POSEIDON_SFB && x.M * x.N > 0 && K > 0 && !x.buf)
+                grouped.push_back(SfTensor{x.W, x.U, x.V, x.M, x.N});
+        }
     const bool group_sf = !ready && plain_sf > 1;
     const int32_t launches = active - (group_sf ? plain_sf - 1 : 0) + (small_ps > 0 ? 1 : 0);
     if (pool->timing) {
@@ -283,7 +291,6 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // of queueing behind each other.  A one-stream pool, or an iteration too
     // small to gain from the overlap, serialises everything on the first.
     const int32_t S = static_cast<int32_t>(pool->streams.size());
-    const double t_sf = sf_flops / SF_FLOPS_PER_S, t_ps = ps_bytes / PS_BYTES_PER_S;
     const bool tiny = t_sf + t_ps < ONE_STREAM_BELOW_S;
     // With ready events the second stream also lets the updates start while
     // the caller's backward pass still runs, so it is kept.
@@ -319,13 +326,6 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         }
         return true;
     };
-    std::vector<SfTensor> grouped;   // in backpropagation order
-    if (group_sf)
-        for (int32_t t = count - 1; t >= 0; --t) {
-            const poseidon_tensor& x = tensors[t];
-            if (plan[static_cast<size_t>(t)] == POSEIDON_SFB && x.M * x.N > 0 && K > 0 && !x.buf)
-                grouped.push_back(SfTensor{x.W, x.U, x.V, x.M, x.N});
-        }
     bool grouped_issued = false;
     std::vector<PsTensor> small;     // in backpropagation order
     std::vector<int32_t> small_idx;
