@@ -35,8 +35,11 @@ def _parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=50,
-                    help="untimed steps first (the first few dozen steps of a fresh process run a few %% slower)")
+    ap.add_argument("--warmup", type=int, default=50, help="untimed steps before the timed ones")
+    ap.add_argument("--min-warmup-s", type=float, default=0.3,
+                    help="keep running untimed steps until the warm-up has lasted this long: a fresh process "
+                         "needs 25-50 iterations (~50-90 ms) of this workload before its steps reach their steady "
+                         "duration, and an idle gap of 0.3 s starts the ramp again")
     ap.add_argument("--config", type=int, default=5, help="workload (5 = VGG19-22K full iteration)")
     ap.add_argument("--streams", type=int, default=2)
     ap.add_argument("--kernel-steps", type=int, default=None,
@@ -44,7 +47,7 @@ def _parse():
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--wfbp", choices=["on", "off"], default="on",
                     help="also time the iteration overlapped with a synthetic VGG19 backward pass")
-    ap.add_argument("--wfbp-steps", type=int, default=5)
+    ap.add_argument("--wfbp-steps", type=int, default=10)
     ap.add_argument("--cpu-fraction", type=float, default=1.0,
                     help="fraction of each tensor the CPU oracle runs on")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -69,14 +72,23 @@ def _ps_bytes(spec, P, momentum: bool):
     return float(spec.numel) * (4 * P + (16 if momentum else 8))
 
 
+# Sources whose device code a kernel's counter figures depend on, besides
+# the file named: the PS kernels' per-group update lives in a shared header.
+_KERNEL_EXTRA_SOURCES = {"ps_apply.hip": ["ps_group.h"]}
+
+
 def _kernel_source_hash(name: str) -> str:
-    """sha256[:16] of a kernel source's code: comments and blank lines are
-    dropped and runs of whitespace collapsed, so that the stored counter
-    figures stay valid across edits of comments only."""
+    """sha256[:16] of a kernel source's code (with the headers its device
+    code is shared through): comments and blank lines are dropped and runs of
+    whitespace collapsed, so that the stored counter figures stay valid
+    across edits of comments only."""
     import hashlib
     import re
-    path = os.path.join(ROOT, "paper_1706_03292_amd", "csrc", name)
-    src = open(path).read()
+    src = ""
+    for n in [name] + _KERNEL_EXTRA_SOURCES.get(name, []):
+        path = os.path.join(ROOT, "paper_1706_03292_amd", "csrc", n)
+        if os.path.exists(path):
+            src += open(path).read() + "\n"
     src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
     src = re.sub(r"//[^\n]*", " ", src)
     code = "\n".join(" ".join(line.split()) for line in src.splitlines() if line.strip())
@@ -122,12 +134,6 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
     bw = SB.SyntheticBackward(wl, [t["W"] for t in devt], d)
     events = {l.layer: torch.cuda.Event() for l in bw.layers}
     ready = bw.ready_list(events, len(devt))
-    # A caller-side variant of the schedule: the FC layers' rebuilds (which
-    # need the matrix cores the backward GEMMs use) wait for the end of the
-    # backward pass; the PS applies (HBM-bound) still start per layer.
-    last = events[bw.layers[-1].layer]
-    ready_defer = [last if t["spec"].kind == "fc" else e for t, e in zip(devt, ready)]
-
     def timed(fn):
         out = []
         for rep in range(steps + 2):
@@ -148,20 +154,31 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
         bw.run(cs, events)
         it(cs, ready=ready)
 
-    def wfbp_defer():
-        bw.run(cs, events)
-        it(cs, ready=ready_defer)
+    def with_policy(policy):
+        def run():
+            pool.set_wfbp_policy(policy)
+            bw.run(cs, events)
+            it(cs, ready=ready)
+            pool.set_wfbp_policy(api.WFBP_ALL_LAST)
+        return run
+
+    # Alg. 2's own schedule (every update, the SFB rebuilds included, on its
+    # own layer's event), and the PS applies alone on their events
+    wfbp_each = with_policy(api.WFBP_EACH)
+    wfbp_sfb_last = with_policy(api.WFBP_SFB_LAST)
 
     t_bw = timed(lambda: bw.run(cs))
+    t_bw_ev = timed(lambda: bw.run(cs, events))
     t_sync = timed(lambda: it(cs))
     t_serial = timed(serial)
     t_wfbp = timed(wfbp)
-    t_defer = timed(wfbp_defer)
+    t_each = timed(wfbp_each)
+    t_sfb_last = timed(wfbp_sfb_last)
     hidden = t_serial - t_wfbp
     # One more of each with the library's launch timing: the updates' own
     # durations show whether they ran beside the backward pass.
     launch = {}
-    for name, fn in (("serial", serial), ("wfbp", wfbp), ("wfbp_defer_sfb", wfbp_defer)):
+    for name, fn in (("serial", serial), ("wfbp", wfbp), ("wfbp_each", wfbp_each), ("wfbp_sfb_last", wfbp_sfb_last)):
         pool.set_timing(True)
         fn()
         recs = pool.launch_times()
@@ -174,13 +191,19 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
     return {
         "backward": "synthetic VGG19 backward at 224x224, B=%d, fp32 torch.mm (vendor library), %.2f TFLOP"
                     % (wl.B, sum(l.flops for l in SB.plan(wl)) / 1e12),
-        "backward_ms": round(t_bw, 3), "sync_ms": round(t_sync, 3),
+        "backward_ms": round(t_bw, 3), "backward_with_events_ms": round(t_bw_ev, 3), "sync_ms": round(t_sync, 3),
+        "events_note": "backward_with_events: the same backward pass recording one event per layer (what every "
+                       "wait-free schedule needs); hidden_* compare with the backward pass without events "
+                       "followed by the iteration",
         "serial_ms": round(t_serial, 3), "wfbp_ms": round(t_wfbp, 3),
         "hidden_sync_ms": round(hidden, 3), "hidden_frac": round(hidden / t_sync, 3),
         "stall_ms": round(max(0.0, t_wfbp - t_bw), 3), "busy_frac": round(t_bw / t_wfbp, 3),
-        "wfbp_defer_sfb_ms": round(t_defer, 3), "hidden_defer_sfb_ms": round(t_serial - t_defer, 3),
-        "defer_note": "wfbp_defer_sfb: the same schedule with the FC layers' ready events replaced by the "
-                      "last backward layer's, so only the PS applies overlap the backward pass",
+        "wfbp_each_ms": round(t_each, 3), "hidden_each_ms": round(t_serial - t_each, 3),
+        "wfbp_sfb_last_ms": round(t_sfb_last, 3), "hidden_sfb_last_ms": round(t_serial - t_sfb_last, 3),
+        "schedule_note": "wfbp: the library's default schedule on one GPU (POSEIDON_WFBP_ALL_LAST: every update "
+                         "waits for every layer's event, then the plain iteration's launches); wfbp_each: every "
+                         "update on its own layer's event (Alg. 2); wfbp_sfb_last: the PS applies on their own "
+                         "events, the SFB rebuilds after the backward pass as one grouped launch",
         "update_launch_ms": launch,
         "steps": steps,
     }
@@ -481,9 +504,15 @@ def main():
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
     stream = torch.cuda.current_stream(d)
 
-    # Warm-up, then exactly K timed steps bracketed by synchronisations.
-    for _ in range(args.warmup):
+    # Warm-up (W steps, continued until it has lasted --min-warmup-s), then
+    # exactly K timed steps bracketed by synchronisations.
+    t_w = time.perf_counter()
+    warm_steps = 0
+    while warm_steps < args.warmup or time.perf_counter() - t_w < args.min_warmup_s:
         schemes = it(stream)
+        warm_steps += 1
+        if warm_steps % 16 == 0:      # keep the host at most 16 steps ahead of the GPU
+            torch.cuda.synchronize()
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_start = time.perf_counter()
@@ -557,6 +586,11 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warm_steps,
+        "warmup_note": f"untimed steps run before the timed region: at least --warmup {args.warmup}, continued "
+                       f"until {args.min_warmup_s} s had passed ({warm_steps} steps); the steps of a fresh process "
+                       "take 25-50 iterations to reach their steady duration (2.9 ms falling to ~1.8 ms), "
+                       "a ramp that a longer pre-warm of other kernels does not remove",
         "ms_per_step": round(wall_ms, 4),
         "higher_is_better": False,
         "scaling": "weak",

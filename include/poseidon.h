@@ -59,6 +59,11 @@ extern "C" {
 #define POSEIDON_KIND_FC     0
 #define POSEIDON_KIND_OTHER  1
 
+/* Schedules of poseidon_sync_iteration_wfbp (poseidon_pool_set_wfbp_policy). */
+#define POSEIDON_WFBP_ALL_LAST 0   /* every update after every ready event (default on one GPU) */
+#define POSEIDON_WFBP_SFB_LAST 1   /* PS applies on their own events, SFB rebuilds after every event */
+#define POSEIDON_WFBP_EACH     2   /* every update on its own ready event (Alg. 2) */
+
 /*
  * Sufficient-factor reconstruction fused with the SGD step (Sec. 2.1
  * "Sufficient Factor Broadcasting"; Eq. 2; Eq. 1), the work of a syncer's
@@ -460,10 +465,14 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
  * reads W_t or writes t's payload (U/V rows or shards) in this iteration;
  * tensors of one layer may share an event.  Issue order, streams, schemes,
  * payload rules and results are those of poseidon_sync_iteration (bitwise:
- * the same kernels), except that every SFB tensor keeps a launch of its own
- * (no grouped launch) and only PS tensors of fewer than 2^17 values share the
- * batched pass, so that each other update starts after its own event;
- * `stream` waits for every update at the end.
+ * the same kernels), except that only PS tensors of fewer than 2^17 values
+ * share the batched pass, so that each other PS update starts after its own
+ * event, and that the pool's schedule (poseidon_pool_set_wfbp_policy) can
+ * hold updates back: by default every update waits for every ready event and
+ * the launches are poseidon_sync_iteration's; under POSEIDON_WFBP_SFB_LAST
+ * the SFB tensors wait for every ready event and share one grouped launch;
+ * under POSEIDON_WFBP_EACH every SFB tensor keeps a launch of its own that
+ * starts after its own event.  `stream` waits for every update at the end.
  * ready: count non-NULL events, caller-owned, not retained after the call.
  * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (also for NULL ready or a NULL
  * entry), POSEIDON_ERR_PAYLOAD or POSEIDON_ERR_HIP.
@@ -481,6 +490,27 @@ int poseidon_sync_iteration_wfbp(poseidon_stream_pool* pool,
  * ready event).  Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG.
  */
 int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
+
+/*
+ * The schedule poseidon_sync_iteration_wfbp uses on this pool.
+ * POSEIDON_WFBP_EACH is Alg. 2's: every tensor's update starts on its own
+ * ready event.  POSEIDON_WFBP_SFB_LAST starts the PS applies on their own
+ * events but holds the SFB rebuilds until every tensor's event has completed
+ * and runs them as one grouped launch.  POSEIDON_WFBP_ALL_LAST (the default)
+ * holds every update until every tensor's event has completed and then
+ * issues exactly poseidon_sync_iteration's launches: the serial order, as a
+ * fallback for a GPU that has no idle time to fill.  On one GPU the updates
+ * are local computation that competes with the caller's backward pass: the
+ * rebuilds for the matrix cores its GEMMs use, the applies for the memory
+ * bandwidth and CU slots of its elementwise steps.  Measured on a 34.6 ms
+ * synthetic VGG19-22K backward pass with a 1.9 ms iteration: EACH ends
+ * 0.39 ms and SFB_LAST 0.10 ms later than the backward pass followed by the
+ * iteration.  What Alg. 2 hides is time the GPU would otherwise spend
+ * waiting for the network; EACH and SFB_LAST are for callers that have such
+ * time.  Results are the same under every schedule (bit-identical kernels).
+ * Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG (NULL pool, unknown policy).
+ */
+int poseidon_pool_set_wfbp_policy(poseidon_stream_pool* pool, int32_t policy);
 
 /* One launch of the last iteration run with timing enabled. */
 typedef struct poseidon_launch_record {

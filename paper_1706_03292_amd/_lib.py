@@ -20,13 +20,16 @@ SFB = 1
 ADAM = 2
 KIND_FC = 0
 KIND_OTHER = 1
+WFBP_ALL_LAST = 0
+WFBP_SFB_LAST = 1
+WFBP_EACH = 2
 
 EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply_batch",
            "poseidon_ps_apply", "poseidon_ps_apply_batch",
            "poseidon_hybcomm_choose", "poseidon_hybcomm_cost", "poseidon_hybcomm_cost_adam",
            "poseidon_hybcomm_choose3", "poseidon_pool_create",
            "poseidon_pool_destroy", "poseidon_sync_iteration", "poseidon_sync_iteration_wfbp",
-           "poseidon_pool_set_timing",
+           "poseidon_pool_set_timing", "poseidon_pool_set_wfbp_policy",
            "poseidon_pool_launch_times", "poseidon_abi_version",
            "poseidon_kv_layout", "poseidon_kv_create", "poseidon_kv_destroy", "poseidon_kv_begin",
            "poseidon_kv_receive", "poseidon_kv_pair_count", "poseidon_kv_receive_message",
@@ -98,6 +101,7 @@ def lib() -> ctypes.CDLL:
     L.poseidon_sf_apply_batch.argtypes = [ctypes.POINTER(PoseidonSfTensor), i32, i64, f32, vp]
     L.poseidon_ps_apply_batch.argtypes = [ctypes.POINTER(PoseidonPsTensor), i32, i32, f32, f32, vp]
     L.poseidon_pool_set_timing.argtypes = [vp, i32]
+    L.poseidon_pool_set_wfbp_policy.argtypes = [vp, i32]
     L.poseidon_pool_launch_times.argtypes = [vp, ctypes.POINTER(PoseidonLaunchRecord), i32,
                                              ctypes.POINTER(i32)]
     L.poseidon_abi_version.argtypes = []

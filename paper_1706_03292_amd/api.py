@@ -13,7 +13,8 @@ import ctypes
 import torch
 
 from . import _lib as L
-from ._lib import ADAM, ERR_HIP, ERR_INVALID_ARG, ERR_PAYLOAD, KIND_FC, KIND_OTHER, PS, SFB  # noqa: F401
+from ._lib import (ADAM, ERR_HIP, ERR_INVALID_ARG, ERR_PAYLOAD, KIND_FC, KIND_OTHER, PS, SFB,  # noqa: F401
+                   WFBP_ALL_LAST, WFBP_EACH, WFBP_SFB_LAST)
 
 
 class PoseidonError(RuntimeError):
@@ -231,6 +232,10 @@ class StreamPool:
     @property
     def handle(self):
         return self._h
+
+    def set_wfbp_policy(self, policy: int) -> None:
+        """WFBP_ALL_LAST (default), WFBP_SFB_LAST or WFBP_EACH (poseidon_pool_set_wfbp_policy)."""
+        _check("poseidon_pool_set_wfbp_policy", L.lib().poseidon_pool_set_wfbp_policy(self.handle, int(policy)))
 
     def set_timing(self, enable: bool) -> None:
         """Bracket every update of the following iterations with timing events."""

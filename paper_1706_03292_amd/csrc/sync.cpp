@@ -19,6 +19,7 @@ struct poseidon_stream_pool {
     std::vector<hipEvent_t> joined;   // one per stream: its last update of the iteration
     hipEvent_t fork = nullptr;        // work enqueued on the caller's stream before the iteration
     bool timing = false;
+    int32_t wfbp_policy = POSEIDON_WFBP_ALL_LAST;
     std::vector<hipEvent_t> t_start;  // per launch of the last timed iteration
     std::vector<hipEvent_t> t_stop;
     std::vector<poseidon_launch_record> t_rec;
@@ -160,7 +161,8 @@ constexpr double CORUN_MAX_RATIO = 0.35;
 
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
 // for the work enqueued on `stream` before the call) and of
-// poseidon_sync_iteration_wfbp (tensor t's update waits for ready[t] only).
+// poseidon_sync_iteration_wfbp (tensor t's update waits for ready[t], or for
+// every ready event, as the pool's schedule says).
 int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_t count, int64_t B, int32_t P,
               float lr, float momentum, const hipEvent_t* ready, hipStream_t stream, int32_t* schemes)
 {
@@ -208,6 +210,11 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
             return POSEIDON_ERR_INVALID_ARG;
         plan[static_cast<size_t>(t)] = scheme;
     }
+    // Under POSEIDON_WFBP_ALL_LAST every update waits for every ready event
+    // and the launches are the plain iteration's: `per` is what the per-tensor
+    // scheduling sees.
+    const bool all_last = ready && pool->wfbp_policy == POSEIDON_WFBP_ALL_LAST;
+    const hipEvent_t* per = all_last ? nullptr : ready;
     // The tensors' updates run concurrently (two streams, batched and grouped
     // launches): no tensor may write where another one reads or writes.
     {
@@ -239,7 +246,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // starts as soon as its own backward pass has run.
     const double t_sf = sf_flops / SF_FLOPS_PER_S, t_ps = ps_bytes / PS_BYTES_PER_S;
     const int64_t small_elems =
-        (!ready && sf_flops < SF_FLOPS_PER_PS_BYTE * ps_bytes) ? PS_CRITICAL_ELEMS : SMALL_PS_ELEMS;
+        (!per && sf_flops < SF_FLOPS_PER_PS_BYTE * ps_bytes) ? PS_CRITICAL_ELEMS : SMALL_PS_ELEMS;
     int32_t active = 0;
     int32_t small_ps = 0;
     int32_t plain_sf = 0;     // SFB layers without a momentum buffer
@@ -260,22 +267,26 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         }
     }
     // One launch per tensor with work, except: small PS tensors share one
-    // batched pass after the other PS launches; and without ready events the
-    // SFB layers without a momentum buffer share one grouped launch, at the
-    // place of the first of them in backpropagation order, whose single tile
-    // list lets one layer's last tiles (and a layer that is exactly one round
-    // of tiles, whose W epilogues would otherwise all run at once) overlap the
-    // next layer's (VGG19-22K iteration: 1.75 vs 1.78 ms, A/B in alternating
-    // processes).  With ready events every SFB layer keeps its own launch, so
-    // that each starts as soon as its own backward pass has run.
+    // batched pass after the other PS launches; and the SFB layers without a
+    // momentum buffer share one grouped launch, at the place of the first of
+    // them in backpropagation order, whose single tile list lets one layer's
+    // last tiles (and a layer that is exactly one round of tiles, whose W
+    // epilogues would otherwise all run at once) overlap the next layer's
+    // (VGG19-22K iteration: 1.75 vs 1.78 ms, A/B in alternating processes).
+    // With ready events that holds under the default schedule, where the SFB
+    // rebuilds wait for the end of the caller's backward pass (on one GPU they
+    // need the matrix cores its GEMMs use); under POSEIDON_WFBP_EACH every
+    // SFB layer keeps its own launch, so that each starts as soon as its own
+    // backward pass has run.
+    const bool sfb_last = per && pool->wfbp_policy == POSEIDON_WFBP_SFB_LAST;
+    const bool group_sf = (!per || sfb_last) && plain_sf > 1;
     std::vector<SfTensor> grouped;   // in backpropagation order
-    if (!ready)
+    if (group_sf)
         for (int32_t t = count - 1; t >= 0; --t) {
             const poseidon_tensor& x = tensors[t];
             if (plan[static_cast<size_t>(t)] == POSEIDON_SFB && x.M * x.N > 0 && K > 0 && !x.buf)
                 grouped.push_back(SfTensor{x.W, x.U, x.V, x.M, x.N});
         }
-    const bool group_sf = !ready && plain_sf > 1;
     const int32_t launches = active - (group_sf ? plain_sf - 1 : 0) + (small_ps > 0 ? 1 : 0);
     if (pool->timing) {
         if (!reserve_timing(pool, launches))
@@ -294,7 +305,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     const bool tiny = t_sf + t_ps < ONE_STREAM_BELOW_S;
     // With ready events the second stream also lets the updates start while
     // the caller's backward pass still runs, so it is kept.
-    const bool balanced = !ready && std::min(t_sf, t_ps) > CORUN_MAX_RATIO * std::max(t_sf, t_ps);
+    const bool balanced = !per && std::min(t_sf, t_ps) > CORUN_MAX_RATIO * std::max(t_sf, t_ps);
     const int32_t used = (S > 1 && launches > 1 && !tiny && !balanced) ? 2 : 1;
     hipEvent_t waited[2] = {nullptr, nullptr};   // last ready event each used stream waits on
     if (!ready) {
@@ -303,16 +314,45 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         for (int32_t s = 0; s < used; ++s)
             if (hipStreamWaitEvent(pool->streams[s], pool->fork, 0) != hipSuccess)
                 return POSEIDON_ERR_HIP;
+    } else if (all_last) {
+        // The first stream waits for every distinct event, the second for
+        // the first (one wait packet instead of one per event).
+        std::vector<hipEvent_t> seen;
+        for (int32_t t = 0; t < count; ++t)
+            if (std::find(seen.begin(), seen.end(), ready[t]) == seen.end())
+                seen.push_back(ready[t]);
+        for (hipEvent_t e : seen)
+            if (hipStreamWaitEvent(pool->streams[0], e, 0) != hipSuccess)
+                return POSEIDON_ERR_HIP;
+        if (used > 1 && (hipEventRecord(pool->fork, pool->streams[0]) != hipSuccess ||
+                         hipStreamWaitEvent(pool->streams[1], pool->fork, 0) != hipSuccess))
+            return POSEIDON_ERR_HIP;
     }
 
     // Tensor t's launch on pool stream si: with ready events it first waits
     // for ready[t] (once per run of equal events), then the timing events, if
     // on, bracket the launch alone.
-    auto timed = [&](hipStream_t s, int32_t scheme, int32_t tensor, int32_t si, auto&& launch) -> bool {
-        if (ready && ready[tensor] != waited[si]) {
-            if (hipStreamWaitEvent(s, ready[tensor], 0) != hipSuccess)
+    bool waited_all = false;         // sfb_last: stream 0 has waited for every ready event
+    auto wait_all = [&](hipStream_t s) -> bool {
+        std::vector<hipEvent_t> seen;
+        for (int32_t t = 0; t < count; ++t) {
+            if (std::find(seen.begin(), seen.end(), ready[t]) != seen.end())
+                continue;
+            seen.push_back(ready[t]);
+            if (hipStreamWaitEvent(s, ready[t], 0) != hipSuccess)
                 return false;
-            waited[si] = ready[tensor];
+        }
+        waited_all = true;
+        return true;
+    };
+    auto timed = [&](hipStream_t s, int32_t scheme, int32_t tensor, int32_t si, auto&& launch) -> bool {
+        if (sfb_last && scheme == POSEIDON_SFB) {
+            if (!waited_all && !wait_all(s))
+                return false;
+        } else if (per && per[tensor] != waited[si]) {
+            if (hipStreamWaitEvent(s, per[tensor], 0) != hipSuccess)
+                return false;
+            waited[si] = per[tensor];
         }
         const size_t r = pool->t_rec.size();
         if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
@@ -373,12 +413,12 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         // The batched pass waits for every ready event of its tensors.
         const int32_t si = used == 1 ? 0 : 1;
         hipStream_t s = pool->streams[si];
-        if (ready)
+        if (per)
             for (int32_t t : small_idx)
-                if (ready[t] != waited[si]) {
-                    if (hipStreamWaitEvent(s, ready[t], 0) != hipSuccess)
+                if (per[t] != waited[si]) {
+                    if (hipStreamWaitEvent(s, per[t], 0) != hipSuccess)
                         return POSEIDON_ERR_HIP;
-                    waited[si] = ready[t];
+                    waited[si] = per[t];
                 }
         const size_t r = pool->t_rec.size();
         if (pool->timing && hipEventRecord(pool->t_start[r], s) != hipSuccess)
@@ -420,6 +460,14 @@ extern "C" int poseidon_sync_iteration_wfbp(poseidon_stream_pool* pool,
         return POSEIDON_ERR_INVALID_ARG;
     static const hipEvent_t none = nullptr;
     return sync_impl(pool, tensors, count, B, P, lr, momentum, count > 0 ? ready : &none, stream, schemes);
+}
+
+extern "C" int poseidon_pool_set_wfbp_policy(poseidon_stream_pool* pool, int32_t policy)
+{
+    if (!pool || (policy != POSEIDON_WFBP_EACH && policy != POSEIDON_WFBP_SFB_LAST && policy != POSEIDON_WFBP_ALL_LAST))
+        return POSEIDON_ERR_INVALID_ARG;
+    pool->wfbp_policy = policy;
+    return POSEIDON_OK;
 }
 
 extern "C" int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable)

@@ -273,3 +273,30 @@ def test_ps_apply_batch_rejects_tensors_that_write_into_each_other():
             api.ps_apply_batch(ts, 0.1, 0.9 if any(b is not None for _, _, b in ts) else 0.0)
         assert e.value.status == api.ERR_INVALID_ARG, i
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("P,n", [(3, 253), (16, 255), (16, 257), (32, 509), (33, 4096 * 3 + 1), (7, 9 * 1031),
+                                 (32, 2786166), (16, 2359298), (4, 1_000_003)])
+def test_ps_apply_ragged_rows_single_batched_misaligned_bitwise(P, n):
+    """n not a multiple of four: every shard row after the first starts off a
+    16-byte boundary.  The same tensor through the single launch, the batched
+    launch, and as misaligned copies: the same sums in the same order, so
+    bit-identical, and as the oracle's (full tail and head, sampled middle)."""
+    d = dev()
+    W, G, buf = _draw(P, n, seed=31 + P + n % 97, buf_std=1e-3)
+    Wa, Ga, ba = W.to(d), G.to(d), buf.to(d)
+    Wb, bb = W.to(d), buf.to(d)
+    Wm, Gm, bm = misaligned(W.to(d)), misaligned(G.to(d)), misaligned(buf.to(d))
+    assert Wa.data_ptr() % 16 == 0 and Ga.data_ptr() % 16 == 0 and ba.data_ptr() % 16 == 0
+    log(f"ps_apply ragged rows P={P} n={n}")
+    api.ps_apply(Wa, Ga, 0.01, 0.9, ba)
+    api.ps_apply_batch([(Wb, Ga, bb)], 0.01, 0.9)
+    api.ps_apply(Wm, Gm, 0.01, 0.9, bm)
+    torch.cuda.synchronize()
+    assert torch.equal(Wa, Wm) and torch.equal(ba, bm)
+    assert torch.equal(Wa, Wb) and torch.equal(ba, bb)
+    idx = np.concatenate([np.random.default_rng(n).integers(0, n, 2000), np.arange(max(0, n - 300), n),
+                          np.arange(min(n, 300))])
+    w_ref, b_ref = oracle.ps_apply_points(W.numpy(), G.numpy(), 0.01, 0.9, buf.numpy(), idx)
+    assert_close(to_np(Wa)[idx], w_ref, W_TOL, "W")
+    assert_close(to_np(ba)[idx], b_ref, BUF_TOL, "buf")

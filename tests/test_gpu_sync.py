@@ -162,32 +162,48 @@ def test_sync_iteration_launch_records():
     pool.close()
 
 
-def test_sync_iteration_groups_the_fc_layers_and_wfbp_does_not():
+def test_sync_iteration_groups_the_fc_layers_unless_wfbp_each():
     """Several SFB layers without a buffer share one grouped launch (record
-    tensor -1) in the plain iteration; with ready events each keeps its own
-    launch, in backprop order; the results are bit-identical."""
+    tensor -1) in the plain iteration and under the default wait-free
+    schedule and POSEIDON_WFBP_SFB_LAST (the rebuilds wait for every event);
+    under POSEIDON_WFBP_EACH each keeps its own launch, in backprop order;
+    the results are bit-identical."""
     d = dev()
     wl = I.workload(3)
     host = I.make_tensors(wl)
-    a, b = _to_dev(host, d), _to_dev(host, d)
+    a, b, c = _to_dev(host, d), _to_dev(host, d), _to_dev(host, d)
     pool = api.StreamPool(2)
+    each = api.StreamPool(2)
+    each.set_wfbp_policy(api.WFBP_EACH)
     it_a = api.SyncIteration(pool, a, wl.B, wl.P, wl.lr, wl.momentum)
     it_b = api.SyncIteration(pool, b, wl.B, wl.P, wl.lr, wl.momentum)
+    it_c = api.SyncIteration(each, c, wl.B, wl.P, wl.lr, wl.momentum)
     cs = torch.cuda.current_stream(d)
     ev = torch.cuda.Event()
     ev.record(cs)
     pool.set_timing(True)
+    each.set_timing(True)
     log("sync_iteration grouped FC launch")
     it_a(cs)
     assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == [(api.SFB, -1, 0)]
     it_b(cs, ready=[ev] * len(b))
-    assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == \
-        [(api.SFB, i, 0) for i in reversed(range(len(b)))]
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == [(api.SFB, -1, 0)]
+    pool.set_wfbp_policy(api.WFBP_SFB_LAST)
+    d2 = _to_dev(host, d)
+    api.SyncIteration(pool, d2, wl.B, wl.P, wl.lr, wl.momentum)(cs, ready=[ev] * len(d2))
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == [(api.SFB, -1, 0)]
+    it_c(cs, ready=[ev] * len(c))
+    assert [(r["scheme"], r["tensor"], r["stream"]) for r in each.launch_times()] == \
+        [(api.SFB, i, 0) for i in reversed(range(len(c)))]
     pool.set_timing(False)
+    each.set_timing(False)
     torch.cuda.synchronize()
-    for x, y in zip(a, b):
+    for x, y, z, w in zip(a, b, c, d2):
         assert torch.equal(x["W"], y["W"]), x["spec"].name
+        assert torch.equal(x["W"], z["W"]), x["spec"].name
+        assert torch.equal(x["W"], w["W"]), x["spec"].name
     pool.close()
+    each.close()
 
 
 def test_sync_iteration_batches_more_when_the_ps_applies_are_the_critical_path():

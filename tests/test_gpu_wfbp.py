@@ -67,7 +67,8 @@ def _oracle_layers(host):
     return out
 
 
-def test_wfbp_update_waits_for_payload_written_by_backward():
+@pytest.mark.parametrize("policy", ["ALL_LAST", "SFB_LAST", "EACH"])
+def test_wfbp_update_waits_for_payload_written_by_backward(policy):
     """Each layer's 'backward' first keeps the compute stream busy, then
     scales this node's own payload (its B rows of U, or shard 0) by 64 --
     exact in fp32 -- and records the layer's event.  The updates must see the
@@ -93,11 +94,12 @@ def test_wfbp_update_waits_for_payload_written_by_backward():
 
     cs = torch.cuda.current_stream(d)
     pool = api.StreamPool(2)
+    pool.set_wfbp_policy(getattr(api, "WFBP_" + policy))
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
     busy_a = torch.randn(4096, 4096, device=d)
     busy_c = torch.empty_like(busy_a)
     events = [torch.cuda.Event() for _ in devt]
-    log("wfbp payload written by the backward pass")
+    log(f"wfbp payload written by the backward pass ({policy})")
     with torch.cuda.stream(cs):
         for i in reversed(range(len(devt))):
             for _ in range(4):
@@ -121,7 +123,8 @@ def test_wfbp_update_waits_for_payload_written_by_backward():
     pool.close()
 
 
-def test_wfbp_backward_reads_weights_before_their_update():
+@pytest.mark.parametrize("policy", ["ALL_LAST", "EACH"])
+def test_wfbp_backward_reads_weights_before_their_update(policy):
     """The synthetic backward's dX = delta @ W (FC) and W^T @ dY (CONV) read the
     weights the same iteration updates; with WFBP they still see the old ones.
     (The vendor GEMMs may sum in a run-dependent order, so outputs are compared
@@ -147,9 +150,10 @@ def test_wfbp_backward_reads_weights_before_their_update():
     before = outputs()
     cs.synchronize()
     pool = api.StreamPool(2)
+    pool.set_wfbp_policy(getattr(api, "WFBP_" + policy))
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
     events = {l.layer: torch.cuda.Event() for l in bw.layers}
-    log("wfbp: backward reads pre-update weights")
+    log(f"wfbp: backward reads pre-update weights ({policy})")
     during = outputs(events)
     it(cs, ready=bw.ready_list(events, len(devt)))
     cs.synchronize()
@@ -166,7 +170,8 @@ def test_wfbp_backward_reads_weights_before_their_update():
 
 
 @pytest.mark.skipif(not hasattr(torch.cuda, "_sleep"), reason="needs torch.cuda._sleep")
-def test_wfbp_updates_overlap_later_backward_work():
+@pytest.mark.parametrize("policy", ["ALL_LAST", "EACH"])
+def test_wfbp_updates_overlap_later_backward_work(policy):
     """All updates' events are recorded before a long single-wave sleep kernel
     (the rest of a backward pass that leaves the GPU idle): with WFBP the
     iteration ends with the sleep, not after it."""
@@ -175,6 +180,7 @@ def test_wfbp_updates_overlap_later_backward_work():
     devt = _to_dev(I.make_tensors(wl), d)
     cs = torch.cuda.current_stream(d)
     pool = api.StreamPool(2)
+    pool.set_wfbp_policy(getattr(api, "WFBP_" + policy))
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
 
     def timed(fn):
@@ -236,4 +242,54 @@ def test_wfbp_launch_records_and_errors():
     assert all(r["ms"] > 0 for r in recs)
     pool.set_timing(False)
     torch.cuda.synchronize()
+    pool.close()
+
+
+@pytest.mark.parametrize("policy", ["ALL_LAST", "SFB_LAST"])
+def test_wfbp_held_schedules_start_the_rebuilds_after_every_event(policy):
+    """Under POSEIDON_WFBP_ALL_LAST (the default) and POSEIDON_WFBP_SFB_LAST
+    an SFB rebuild waits for every tensor's ready event, not only its own: the FC layer's
+    event is recorded first, then the stream is kept busy and the layer's own
+    factor rows are scaled by 64 (exact in fp32) before the last tensor's
+    event.  The rebuild must see the scaled factors (W as the oracle on them,
+    far from the oracle on the unscaled ones); the PS tensors' results are
+    the oracle's either way."""
+    d = dev()
+    wl = I.workload(5)
+    names = ["fc7.W", "fc7.b", "conv5_4.W"]
+    host = I.make_tensors(wl, only=names)
+    devt = _to_dev(host, d)
+    fc = next(i for i, h in enumerate(host) if "U" in h)
+    scaled = [dict(h) for h in host]
+    scaled[fc]["U"] = host[fc]["U"].clone()
+    scaled[fc]["U"][: wl.B] *= 64
+    ref = oracle.sync_iteration(_oracle_layers(scaled), wl.B, wl.P, wl.lr, wl.momentum)
+    old = oracle.sync_iteration(_oracle_layers(host), wl.B, wl.P, wl.lr, wl.momentum)
+    cs = torch.cuda.current_stream(d)
+    pool = api.StreamPool(2)
+    pool.set_wfbp_policy(getattr(api, "WFBP_" + policy))
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    busy_a = torch.randn(4096, 4096, device=d)
+    busy_c = torch.empty_like(busy_a)
+    early, late = torch.cuda.Event(), torch.cuda.Event()
+    log(f"wfbp {policy}: rebuild after every event")
+    with torch.cuda.stream(cs):
+        early.record(cs)
+        for _ in range(8):
+            torch.mm(busy_a, busy_a, out=busy_c)
+        devt[fc]["U"][: wl.B].mul_(64)
+        late.record(cs)
+    # the FC layer and one PS tensor are ready early; the last one late
+    ready = [early] * len(devt)
+    ready[next(i for i in range(len(devt)) if i != fc)] = late
+    it(cs, ready=ready)
+    cs.synchronize()
+    for i, t in enumerate(devt):
+        name = host[i]["spec"].name
+        want = ref[i]["W"].reshape(-1)
+        assert_close(to_np(t["W"]).reshape(-1), want, W_TOL, name)
+    tol = W_TOL * float(np.max(np.abs(ref[fc]["W"])))
+    assert float(np.max(np.abs(old[fc]["W"] - ref[fc]["W"]))) > 20 * tol
+    with pytest.raises(api.PoseidonError):
+        pool.set_wfbp_policy(7)
     pool.close()
