@@ -146,3 +146,47 @@ class SyntheticBackward:
             for t in l.tensors:
                 out[t] = events[l.layer]
         return out
+
+
+def main(argv=None) -> None:
+    """Run the VGG19-22K iteration after this backward pass, then under each
+    wait-free schedule, a few passes each: a short program for profilers.
+
+        python -m paper_1706_03292_amd.synthetic_backward [--passes 3]
+    """
+    import argparse
+
+    from . import api
+
+    ap = argparse.ArgumentParser(description=main.__doc__)
+    ap.add_argument("--passes", type=int, default=3)
+    ap.add_argument("--schedules", default="serial,each",
+                    help="comma-separated: serial (backward, then the iteration), all_last, sfb_last, each")
+    args = ap.parse_args(argv)
+    d = torch.device("cuda", 0)
+    wl = I.workload(5)
+    devt = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in I.make_tensors(wl)]
+    pool = api.StreamPool(2, device=d)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    cs = torch.cuda.current_stream(d)
+    bw = SyntheticBackward(wl, [t["W"] for t in devt], d)
+    events = {l.layer: torch.cuda.Event() for l in bw.layers}
+    ready = bw.ready_list(events, len(devt))
+    policies = {"all_last": api.WFBP_ALL_LAST, "sfb_last": api.WFBP_SFB_LAST, "each": api.WFBP_EACH}
+    for name in args.schedules.split(","):
+        if name != "serial":
+            pool.set_wfbp_policy(policies[name])
+        for _ in range(args.passes):
+            if name == "serial":
+                bw.run(cs)
+                it(cs)
+            else:
+                bw.run(cs, events)
+                it(cs, ready=ready)
+            torch.cuda.synchronize()
+        print(f"[synthetic_backward] {name}: {args.passes} passes done", flush=True)
+    pool.close()
+
+
+if __name__ == "__main__":
+    main()
