@@ -421,8 +421,10 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * SFB, 5 TB/s for PS), or one whose two kinds would take comparable times at
  * those rates (the smaller above 0.35 of the larger: neither leaves gaps the
  * other could fill, so co-running only delays both) runs everything in order
- * on the first.  Two kinds of tensors share launches instead (with the kernels and
- * arithmetic of the single-tensor calls, so the same results): PS tensors of
+ * on one stream (without ready events the caller's `stream` itself, with no
+ * fork and join events).  Two kinds of tensors share launches instead (with
+ * the kernels and arithmetic of the single-tensor calls, so the same
+ * results): PS tensors of
  * fewer than 2^17 values, which a launch of their own would leave
  * latency-bound, are applied together, in backpropagation order, by one
  * batched pass (poseidon_ps_apply_batch) after the other PS launches -- and

@@ -308,7 +308,14 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     const bool balanced = !per && std::min(t_sf, t_ps) > CORUN_MAX_RATIO * std::max(t_sf, t_ps);
     const int32_t used = (S > 1 && launches > 1 && !tiny && !balanced) ? 2 : 1;
     hipEvent_t waited[2] = {nullptr, nullptr};   // last ready event each used stream waits on
-    if (!ready) {
+    // An iteration issued on one stream that waits for nothing but the
+    // caller's earlier work runs on the caller's stream itself: no fork and
+    // join events (two fewer packets per iteration for latency-bound ones).
+    const bool direct = !ready && used == 1;
+    std::vector<hipStream_t> st(pool->streams.begin(), pool->streams.end());
+    if (direct)
+        st[0] = stream;
+    if (!direct && !ready) {
         if (hipEventRecord(pool->fork, stream) != hipSuccess)
             return POSEIDON_ERR_HIP;
         for (int32_t s = 0; s < used; ++s)
@@ -382,7 +389,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         if (plan[static_cast<size_t>(t)] == POSEIDON_SFB) {
             if (K == 0 && !x.buf)
                 continue;
-            hipStream_t s = pool->streams[0];
+            hipStream_t s = st[0];
             if (group_sf && !x.buf) {
                 if (!grouped_issued) {
                     grouped_issued = true;
@@ -401,7 +408,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
                 return POSEIDON_ERR_HIP;
         } else {
             const int32_t si = used == 1 ? 0 : 1;
-            hipStream_t s = pool->streams[si];
+            hipStream_t s = st[si];
             if (!timed(s, POSEIDON_PS, t, si, [&] {
                     return launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
                 }))
@@ -412,7 +419,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (!small.empty()) {
         // The batched pass waits for every ready event of its tensors.
         const int32_t si = used == 1 ? 0 : 1;
-        hipStream_t s = pool->streams[si];
+        hipStream_t s = st[si];
         if (per)
             for (int32_t t : small_idx)
                 if (per[t] != waited[si]) {
@@ -433,7 +440,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         }
     }
 
-    for (int32_t s = 0; s < used; ++s) {
+    for (int32_t s = 0; s < used && !direct; ++s) {
         if (hipEventRecord(pool->joined[s], pool->streams[s]) != hipSuccess ||
             hipStreamWaitEvent(stream, pool->joined[s], 0) != hipSuccess)
             return POSEIDON_ERR_HIP;

@@ -314,3 +314,61 @@ def test_sync_iteration_runs_comparable_kinds_on_one_stream():
     assert [(r["scheme"], r["stream"]) for r in recs] == [(api.PS, 0), (api.SFB, 0)]
     _oracle_check(host, devt, wl, schemes)
     pool.close()
+
+
+@pytest.mark.parametrize("cfg,only", [(1, None), (5, ["fc7.W", "fc7.b", "conv5_4.W"])])
+def test_sync_iteration_is_ordered_on_the_callers_stream(cfg, only):
+    """The iteration behaves as one operation on the caller's stream, whether
+    it runs there directly (the one-stream, latency-bound workload 1) or
+    forks to the pool's two streams (an FC layer beside a conv kernel): work
+    enqueued on that stream before it is seen by the updates (a payload
+    scaled by 64 first), and work enqueued after it sees the updated weights
+    (a copy taken right after the call, with no synchronisation between)."""
+    d = dev()
+    wl = I.workload(cfg)
+    host = I.make_tensors(wl, only=only)
+    devt = _to_dev(host, d)
+    scaled = []
+    for h in host:
+        h2 = dict(h)
+        if "U" in h:
+            h2["U"] = h["U"].clone()
+            h2["U"][: wl.B] *= 64
+        else:
+            h2["shards"] = h["shards"].clone()
+            h2["shards"][0] *= 64
+        scaled.append(h2)
+    side = torch.cuda.Stream(d)
+    pool = api.StreamPool(2)
+    it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
+    busy = torch.randn(4096, 4096, device=d)
+    torch.cuda.synchronize()
+    log(f"sync_iteration ordered on the caller's stream, config {cfg}")
+    pool.set_timing(True)
+    with torch.cuda.stream(side):
+        for _ in range(4):
+            busy = busy @ busy / 64
+        for t in devt:
+            if "U" in t:
+                t["U"][: wl.B].mul_(64)
+            else:
+                t["shards"][0].mul_(64)
+        it(side)
+        copies = [t["W"].clone() for t in devt]
+    side.synchronize()
+    streams = {r["stream"] for r in pool.launch_times()}
+    pool.set_timing(False)
+    assert streams == ({0} if cfg == 1 else {0, 1})
+    for i, (c, h) in enumerate(zip(copies, scaled)):
+        name = h["spec"].name
+        if "U" in h:
+            M, N = h["W"].shape
+            rr, cc = sample_points(M, N, 2000, seed=M)
+            want = oracle.sf_apply_points(h["W"].numpy(), h["U"].numpy(), h["V"].numpy(), wl.lr, rr, cc)
+            assert_close(to_np(c)[rr, cc], want, W_TOL, name)
+        else:
+            b0 = h["buf"].numpy() if h.get("buf") is not None else None
+            want, _ = oracle.ps_apply(h["W"].numpy().reshape(-1), h["shards"].numpy(), wl.lr,
+                                      wl.momentum if b0 is not None else 0.0, b0)
+            assert_close(to_np(c).reshape(-1), want, W_TOL, name)
+    pool.close()
