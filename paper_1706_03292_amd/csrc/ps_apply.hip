@@ -16,12 +16,13 @@
 // shards: 5.0 TB/s this way against 3.9 TB/s with 4-byte accesses).  Every
 // array is touched once per launch (shards read; W and buf read, then
 // written), so all accesses are non-temporal (1-2% faster than cached W/buf
-// accesses on 2.4M-16.8M elements).  One-wave workgroups, one group per
-// thread, as many workgroups as groups: a launch-shape sweep over 37K-16.8M
+// accesses on 2.4M-16.8M elements).  One group per thread and as many
+// workgroups as needed (one pass): a launch-shape sweep over 37K-16.8M
 // elements (block size 64-1024, one or two groups per thread, grid-stride
 // loops capped at 4-16 workgroups per CU) found this within 3% of the best
 // everywhere and 10% faster than a capped grid-stride loop on large tensors,
-// whose last partial pass leaves the chip half idle.
+// whose last partial pass leaves the chip half idle; of the block sizes,
+// 256 threads (PS_THREADS) is the best beside the SF rebuild.
 //
 // Three launch forms share the per-group update: one tensor with P
 // contiguous shards, many such tensors in one launch, and the KV store's
@@ -33,8 +34,19 @@
 namespace poseidon {
 namespace {
 
-constexpr int PS_THREADS = 64;                  // one wave per workgroup
+// Four waves per workgroup: against one-wave workgroups, as fast on aligned
+// tensors alone (5.86 vs 5.94 TB/s on 2,359,296 values at P = 16), faster on
+// rows off 16-byte boundaries (6.0 vs 5.6 TB/s on 2,786,166 values at P =
+// 32), and beside the SF rebuild a workgroup the size of a rebuild
+// workgroup's slot gives that slot back whole (the Inception-shaped
+// iteration 0.657 vs 0.681 ms; VGG19-22K 1.739 vs 1.745 ms).
+constexpr int PS_THREADS = 256;
 constexpr int PS_BLOCK_ELEMS = 4 * PS_THREADS;  // elements per workgroup: one group of four per thread
+// The KV store's launches are small (one server's share of a tensor, a few
+// hundred thousand elements): one-wave workgroups fill the chip better there
+// (server 0's VGG19-22K applies at 5.5 vs 4.8 TB/s).
+constexpr int KV_THREADS = 64;
+constexpr int KV_BLOCK_ELEMS = 4 * KV_THREADS;
 constexpr int64_t PS_MAX_GRID = int64_t{1} << 30;
 
 // ---------------------------------------------------------------------------
@@ -155,7 +167,7 @@ void launch_batch_mom(const PsBatchArgs& a, int blocks, int grid, int32_t P, flo
 // passed in worker order, the same for every range of the launch).  Range r
 // covers elements [offset, offset + length) of the tensor (W, buf) and owns
 // the workgroups [first_block[r], first_block[r+1]); each workgroup updates
-// PS_BLOCK_ELEMS consecutive elements of its range, with 16-byte accesses
+// KV_BLOCK_ELEMS consecutive elements of its range, with 16-byte accesses
 // that are aligned when the range's arrays allow it.
 // ---------------------------------------------------------------------------
 struct KvRange {
@@ -177,7 +189,7 @@ struct KvArgs {
 };
 
 template <int PT, bool MOM>
-__global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, int P, float lr, float mu)
+__global__ __launch_bounds__(KV_THREADS) void kv_apply_kernel(const KvArgs a, int P, float lr, float mu)
 {
     const int b = blockIdx.x;
     int r = 0;                                  // as in the batched kernel: independent loads
@@ -185,7 +197,7 @@ __global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, in
     for (int k = 1; k < KV_MAX_RANGES; ++k)
         r += (k < a.nranges && a.first_block[k] <= b) ? 1 : 0;
     const KvRange& q = a.r[r];
-    const int64_t j = static_cast<int64_t>(b - q.first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
+    const int64_t j = static_cast<int64_t>(b - q.first_block) * KV_BLOCK_ELEMS + 4 * threadIdx.x;
     if (j >= q.length)
         return;
     const PerWorker src{a.g, a.msg_mask, q.delta};
@@ -198,12 +210,12 @@ __global__ __launch_bounds__(PS_THREADS) void kv_apply_kernel(const KvArgs a, in
 // ---------------------------------------------------------------------------
 // KV-store message: the slices [src_k, src_k + length_k) of one worker's
 // updates copied one after another into its message (range k starts at
-// element dst_k).  Each one-wave workgroup copies PACK_BLOCK_ELEMS elements of
+// element dst_k).  Each workgroup copies PACK_BLOCK_ELEMS elements of
 // one range: four 16-byte groups per thread, all loads issued before the
 // stores (a copy moves few bytes per thread otherwise).
 // ---------------------------------------------------------------------------
 constexpr int PACK_UNROLL = 4;
-constexpr int PACK_BLOCK_ELEMS = PACK_UNROLL * PS_BLOCK_ELEMS;
+constexpr int PACK_BLOCK_ELEMS = PACK_UNROLL * KV_BLOCK_ELEMS;
 
 struct PackArgs {
     const float* src[KV_PACK_MAX];
@@ -213,7 +225,7 @@ struct PackArgs {
     int32_t count;
 };
 
-__global__ __launch_bounds__(PS_THREADS) void kv_pack_kernel(const PackArgs a, float* __restrict__ message)
+__global__ __launch_bounds__(KV_THREADS) void kv_pack_kernel(const PackArgs a, float* __restrict__ message)
 {
     const int b = blockIdx.x;
     int k = 0;
@@ -227,13 +239,13 @@ __global__ __launch_bounds__(PS_THREADS) void kv_pack_kernel(const PackArgs a, f
     f4 v[PACK_UNROLL];
 #pragma unroll
     for (int u = 0; u < PACK_UNROLL; ++u) {
-        const int64_t j = j0 + u * PS_BLOCK_ELEMS;
+        const int64_t j = j0 + u * KV_BLOCK_ELEMS;
         if (j + 3 < len)
             v[u] = ld4<false>(src + j);
     }
 #pragma unroll
     for (int u = 0; u < PACK_UNROLL; ++u) {
-        const int64_t j = j0 + u * PS_BLOCK_ELEMS;
+        const int64_t j = j0 + u * KV_BLOCK_ELEMS;
         if (j + 3 < len) {
             st4<false>(dst + j, v[u]);
         } else {
@@ -247,11 +259,11 @@ template <bool MOM>
 void launch_kv_mom(const KvArgs& a, int grid, int32_t P, float lr, float mu, hipStream_t stream)
 {
     switch (P) {
-    case 4:  kv_apply_kernel<4, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
-    case 8:  kv_apply_kernel<8, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
-    case 16: kv_apply_kernel<16, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
-    case 32: kv_apply_kernel<32, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
-    default: kv_apply_kernel<0, MOM><<<grid, PS_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    case 4:  kv_apply_kernel<4, MOM><<<grid, KV_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    case 8:  kv_apply_kernel<8, MOM><<<grid, KV_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    case 16: kv_apply_kernel<16, MOM><<<grid, KV_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    case 32: kv_apply_kernel<32, MOM><<<grid, KV_THREADS, 0, stream>>>(a, P, lr, mu); break;
+    default: kv_apply_kernel<0, MOM><<<grid, KV_THREADS, 0, stream>>>(a, P, lr, mu); break;
     }
 }
 
@@ -344,7 +356,7 @@ hipError_t launch_kv_apply(const KvApplyRange* ranges, int32_t nranges, const fl
             const KvApplyRange& x = ranges[i];
             if (x.length == 0 || (x.buf != nullptr) != (mom == 1))
                 continue;
-            const int64_t nb = (x.length + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
+            const int64_t nb = (x.length + KV_BLOCK_ELEMS - 1) / KV_BLOCK_ELEMS;
             if (a.nranges == KV_MAX_RANGES || blocks + nb > INT32_MAX) {
                 const hipError_t e = flush();
                 if (e != hipSuccess)
@@ -387,7 +399,7 @@ hipError_t launch_kv_pack(const float* const* src, const int64_t* dst, const int
         }
         if (blocks == 0)
             continue;
-        kv_pack_kernel<<<static_cast<int>(blocks), PS_THREADS, 0, stream>>>(a, message);
+        kv_pack_kernel<<<static_cast<int>(blocks), KV_THREADS, 0, stream>>>(a, message);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
