@@ -535,7 +535,7 @@ int poseidon_pool_launch_times(poseidon_stream_pool* pool, poseidon_launch_recor
                                int32_t capacity, int32_t* count);
 
 /* Library version, for the binding's load check: returns POSEIDON_ABI_VERSION. */
-#define POSEIDON_ABI_VERSION 1
+#define POSEIDON_ABI_VERSION 2
 int poseidon_abi_version(void);
 
 #ifdef __cplusplus

@@ -155,6 +155,10 @@ int main(void)
         memset(B2, 0, n * 4);
         float *dW1 = dev_copy(W1, M * N), *dU = dev_copy(U, K * M), *dV = dev_copy(V, K * N);
         float *dW2 = dev_copy(W2, n), *dG = dev_copy(G, P * n), *dB2 = dev_copy(B2, n);
+        /* the same start for the wait-free iterations below, one copy per schedule */
+        float *eW1[2], *eW2[2], *eB2[2];
+        for (int c = 0; c < 2; ++c)
+            eW1[c] = dev_copy(W1, M * N), eW2[c] = dev_copy(W2, n), eB2[c] = dev_copy(B2, n);
         poseidon_stream_pool *pool = NULL;
         int rc = poseidon_pool_create(2, &pool);
         poseidon_tensor t[2];
@@ -169,6 +173,40 @@ int main(void)
         HIP_OK(hipDeviceSynchronize());
         to_host(g1, dW1, M * N);
         to_host(g2, dW2, n);
+        /* The wait-free iteration under Alg. 2's schedule and under the
+         * default (every update after every event): the same results. */
+        {
+            hipEvent_t ev;
+            HIP_OK(hipEventCreate(&ev));
+            HIP_OK(hipEventRecord(ev, 0));
+            const hipEvent_t ready[2] = {ev, ev};
+            const int32_t pol[2] = {POSEIDON_WFBP_EACH, POSEIDON_WFBP_ALL_LAST};
+            int same = 1, wrc = POSEIDON_OK;
+            float *h1 = malloc(M * N * 4), *h2 = malloc(n * 4);
+            for (int c = 0; c < 2 && wrc == POSEIDON_OK; ++c) {
+                poseidon_tensor u[2];
+                memcpy(u, t, sizeof u);
+                u[0].W = eW1[c], u[1].W = eW2[c], u[1].buf = eB2[c];
+                wrc = poseidon_pool_set_wfbp_policy(pool, pol[c]);
+                if (wrc == POSEIDON_OK)
+                    wrc = poseidon_sync_iteration_wfbp(pool, u, 2, Bsz, P, 0.01f, 0.9f, ready, 0, NULL);
+                HIP_OK(hipDeviceSynchronize());
+                to_host(h1, eW1[c], M * N);
+                to_host(h2, eW2[c], n);
+                same &= memcmp(h1, g1, M * N * 4) == 0 && memcmp(h2, g2, n * 4) == 0;
+            }
+            const int bad_policy = poseidon_pool_set_wfbp_policy(pool, 17) == POSEIDON_ERR_INVALID_ARG;
+            printf("%-44s rc %d %s\n", "poseidon_sync_iteration_wfbp (2 schedules)", wrc,
+                   wrc == POSEIDON_OK && same && bad_policy ? "ok" : "FAIL");
+            failures += !(wrc == POSEIDON_OK && same && bad_policy);
+            free(h1), free(h2);
+            HIP_OK(hipEventDestroy(ev));
+            for (int c = 0; c < 2; ++c) {
+                HIP_OK(hipFree(eW1[c]));
+                HIP_OK(hipFree(eW2[c]));
+                HIP_OK(hipFree(eB2[c]));
+            }
+        }
         poseidon_pool_destroy(pool);
         const int want0 = oracle_hybcomm_choose(M, N, Bsz, P);
         if (want0 == 1)
