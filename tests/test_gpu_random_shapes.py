@@ -78,12 +78,13 @@ def test_ps_random_shapes(seed):
                 assert_close(to_np(b), b_ref, BUF_TOL, f"buf ({how})")
 
 
-@pytest.mark.parametrize("seed", range(10))
+@pytest.mark.parametrize("seed", range(16))
 def test_sync_iteration_random_networks(seed):
     """Random layer lists (FC layers with factors and shards, with or without
     a momentum buffer; PS tensors on both sides of the batching thresholds),
-    random P, B and pool size, with or without ready events: schemes exactly,
-    and every update, as the oracle's iteration."""
+    random P, B and pool size, with or without ready events and under each
+    wait-free schedule: schemes exactly, and every update, as the oracle's
+    iteration."""
     d = dev()
     rng = np.random.default_rng(700 + seed)
     P, B = int(rng.integers(2, 21)), int(rng.integers(1, 17))
@@ -101,17 +102,26 @@ def test_sync_iteration_random_networks(seed):
             host.append({"fc": False, "W": I.randn(base, (n,), 0.01), "shards": I.randn(base + 3, (P, n), 1e-3),
                          "buf": I.randn(base + 4, (n,), 1e-3) if rng.random() < 0.7 else None})
     streams = int(rng.choice([1, 2, 4]))
-    wfbp = bool(rng.random() < 0.3)
+    wfbp = bool(rng.random() < 0.5)
+    policy = int(rng.choice([api.WFBP_ALL_LAST, api.WFBP_SFB_LAST, api.WFBP_EACH]))
     devt = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items() if v is not None}
             for h in host]
-    log(f"sync random seed={seed} P={P} B={B} layers={len(host)} streams={streams} wfbp={wfbp}")
+    log(f"sync random seed={seed} P={P} B={B} layers={len(host)} streams={streams} wfbp={wfbp} policy={policy}")
     pool = api.StreamPool(streams)
+    pool.set_wfbp_policy(policy)
     it = api.SyncIteration(pool, devt, B, P, 0.01, 0.9)
     cs = torch.cuda.current_stream(d)
     if wfbp:
-        ev = torch.cuda.Event()
-        ev.record(cs)
-        schemes = it(cs, ready=[ev] * len(devt))
+        # One event per layer, recorded in backprop order (last layer first),
+        # some layers sharing an event.
+        ready = [None] * len(devt)
+        ev = None
+        for t in reversed(range(len(devt))):
+            if ev is None or rng.random() < 0.6:
+                ev = torch.cuda.Event()
+                ev.record(cs)
+            ready[t] = ev
+        schemes = it(cs, ready=ready)
     else:
         schemes = it(cs)
     torch.cuda.synchronize()
