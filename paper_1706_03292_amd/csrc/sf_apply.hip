@@ -387,6 +387,11 @@ struct Direct {
         wait_loads();
         __syncthreads();
         issue<S ^ 1>(ur, vr, ldu, ldv, kt + 1, tid);
+        // Keep the loads ahead of the multiply: left to itself the scheduler
+        // sinks them (they have no register results) to the end of the slice,
+        // just before the next step waits for them, and their latency is then
+        // hidden only by the other workgroups on the CU.
+        __builtin_amdgcn_sched_barrier(0);
         mma<S>(acc, wm, wn, lane);
     }
 };
