@@ -414,9 +414,11 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * and issued from the last to the first (backpropagation order).  For each
  * tensor the scheme is Alg. 1's (FC: poseidon_hybcomm_choose(M, N, B, P);
  * other kinds: PS).  Every tensor with work is one launch, in
- * backpropagation order: the SFB updates (bound by the matrix cores) on the
- * pool's first stream, the PS updates (bound by memory bandwidth) on its
- * second, so that the two kinds overlap; a one-stream pool, an iteration
+ * backpropagation order: the SFB updates (bound by the matrix cores) and the
+ * PS updates (bound by memory bandwidth) on two streams, so that the two
+ * kinds overlap -- the kind with the longer estimated time (at the rates
+ * below) on the caller's `stream` itself, the other on the pool's first
+ * stream, forked from and joined back to `stream`; a one-stream pool, an iteration
  * whose work would take under 30 us at the kernels' rates (130 TFLOP/s for
  * SFB, 5 TB/s for PS), or one whose two kinds would take comparable times at
  * those rates (the smaller above 0.35 of the larger: neither leaves gaps the
@@ -437,8 +439,8 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
  * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
  * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,
- * momentum, buf) (momentum is used only when buf != NULL).  Every pool
- * stream first waits for the work already
+ * momentum, buf) (momentum is used only when buf != NULL).  The pool
+ * stream used first waits for the work already
  * enqueued on `stream`, and `stream` then waits for every tensor's update, so
  * the call behaves like one asynchronous operation on `stream` (the
  * bulk-synchronous barrier of Sec. 4.1 "Managing Consistency").
@@ -465,9 +467,11 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
  * hipEventRecord, on any stream of the current device, BEFORE this call --
  * an event never recorded counts as complete) after the last kernel that
  * reads W_t or writes t's payload (U/V rows or shards) in this iteration;
- * tensors of one layer may share an event.  Issue order, streams, schemes,
- * payload rules and results are those of poseidon_sync_iteration (bitwise:
- * the same kernels), except that only PS tensors of fewer than 2^17 values
+ * tensors of one layer may share an event.  Issue order, schemes, payload
+ * rules and results are those of poseidon_sync_iteration (bitwise: the same
+ * kernels), except that every update runs on the pool's streams (the SFB
+ * updates on its first, the PS updates on its second, or all on the first in
+ * a one-stream iteration), none on `stream`, that only PS tensors of fewer than 2^17 values
  * share the batched pass, so that each other PS update starts after its own
  * event, and that the pool's schedule (poseidon_pool_set_wfbp_policy) can
  * hold updates back: by default every update waits for every ready event and
@@ -520,7 +524,9 @@ typedef struct poseidon_launch_record {
     int32_t tensor;   /* index into that call's tensors[], or -1 for a shared launch (scheme
                          POSEIDON_PS: the batched pass of the small PS tensors; POSEIDON_SFB:
                          the grouped launch of the SFB tensors without a buffer) */
-    int32_t stream;   /* pool stream index */
+    int32_t stream;   /* 0: the SFB updates' stream, 1: the PS updates' (one-stream
+                         iterations: 0); see poseidon_sync_iteration for which
+                         stream each is */
     float   ms;       /* time between the events around the launch */
 } poseidon_launch_record;
 

@@ -298,7 +298,7 @@ def test_sync_iteration_runs_comparable_kinds_on_one_stream():
     """The 4096 x 4096 layer rebuilt from its factors beside the same layer's
     805 MB of dense shards: the two kinds are of comparable size, so co-running
     them only delays both, and the iteration issues them one after the other
-    on the pool's first stream; results as the oracle's."""
+    on one stream (the caller's); results as the oracle's."""
     d = dev()
     wl = I.workload(2)
     host = I.make_tensors(wl)
@@ -316,11 +316,15 @@ def test_sync_iteration_runs_comparable_kinds_on_one_stream():
     pool.close()
 
 
-@pytest.mark.parametrize("cfg,only", [(1, None), (5, ["fc7.W", "fc7.b", "conv5_4.W"])])
+@pytest.mark.parametrize("cfg,only", [(1, None), (5, ["fc7.W", "fc7.b", "conv5_4.W"]),
+                                      (4, ["conv45", "conv46", "fc.W"])])
 def test_sync_iteration_is_ordered_on_the_callers_stream(cfg, only):
     """The iteration behaves as one operation on the caller's stream, whether
     it runs there directly (the one-stream, latency-bound workload 1) or
-    forks to the pool's two streams (an FC layer beside a conv kernel): work
+    on two streams, the longer kind on the caller's stream and the other
+    forked to the pool (an FC layer beside a conv kernel, the rebuild the
+    longer; the Inception-shaped classifier beside two large conv kernels,
+    the applies the longer): work
     enqueued on that stream before it is seen by the updates (a payload
     scaled by 64 first), and work enqueued after it sees the updated weights
     (a copy taken right after the call, with no synchronisation between)."""
