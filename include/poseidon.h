@@ -435,7 +435,11 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * n*(4P+16) bytes, or 4P+8 without a buffer), so do PS tensors of fewer than
  * 2^21 values; and the SFB tensors without a momentum buffer, when there are
  * several, are rebuilt by one grouped launch (poseidon_sf_apply_batch) at the
- * place of the first of them, so that the layers' tiles share one work list.
+ * place of the first of them, so that the layers' tiles share one work list
+ * -- except in a two-stream iteration whose PS applies are the longer kind:
+ * there every SFB launch runs on few workgroups that each walk several of
+ * its tiles, sized to take about 90% of the applies' estimated time, so that
+ * the rebuilds run thin beside the applies.
  * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
  * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
  * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,

@@ -60,13 +60,16 @@ inline bool writes_collide(std::vector<Span> writes, const std::vector<Span>& re
 // Number of compute units of the current device (cached per device).
 int device_cu_count();
 
-// Internal launchers (arguments already validated; nonzero sizes).
+// Internal launchers (arguments already validated; nonzero sizes).  Given
+// spread_s > 0, an SF launch runs on as few workgroups as would walk its
+// tiles in about spread_s seconds, instead of one workgroup per tile.
 hipError_t launch_sf_apply(float* W, const float* U, const float* V,
-                           int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream);
+                           int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream, double spread_s = 0.0);
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
                            float lr, float momentum, float* buf, hipStream_t stream);
 hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M,
-                                    int64_t N, int64_t K, float lr, float mu, hipStream_t stream);
+                                    int64_t N, int64_t K, float lr, float mu, hipStream_t stream,
+                                    double spread_s = 0.0);
 
 // One FC layer of a grouped SF launch (same layout as poseidon_sf_tensor).
 struct SfTensor {

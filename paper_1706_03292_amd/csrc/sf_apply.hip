@@ -612,6 +612,29 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_kernel(
     sf_tile_direct<BM, BN, BK, WM, WN, MOM>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
 }
 
+// The spread launch: fewer workgroups than tiles (a multiple of 8, so that
+// tile t stays on the XCD of workgroup t % 8), each walking the tiles
+// grid-stride.  A kernel of its own: the loop makes the compiler keep more
+// values live (the 128 x 128 tile spilled 61 VGPRs at the one-tile kernel's
+// 128), and a spread launch has few workgroups resident, so it is compiled
+// for 2 waves per SIMD.  The barrier keeps a wave's first loads of the next
+// tile out of the LDS stage the others may still read.
+template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(1, 2))) void sf_apply_walk_kernel(
+    float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
+    float lr, int tiles_m, int tiles_n, float* __restrict__ buf, float mu)
+{
+    const int tiles = tiles_m * tiles_n;
+    for (int t = blockIdx.x; t < tiles; t += gridDim.x) {
+        if (t != static_cast<int>(blockIdx.x))
+            __syncthreads();
+        int tm, tn;
+        tile_coords<8>(t, tiles, tiles_m, tiles_n, tm, tn);
+        sf_tile_direct<BM, BN, BK, WM, WN, MOM>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
+    }
+}
+
 template <int BM, int BN, int BK, int WM, int WN, bool WIDE, bool MOM>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_staged_kernel(
@@ -691,9 +714,14 @@ bool direct_fits(int64_t M, int64_t N, int64_t K, int BM, int BN, int BK)
     return (K + BK) * M * 4 < LIM && (K + BK) * N * 4 < LIM && (static_cast<int64_t>(BM) * N + BN) * 4 < LIM;
 }
 
+// A workgroup's rate when few of them walk a layer's tiles beside the PS
+// applies (the 1000 x 2048 classifier at K = 1024: 8 tiles of 64 x 64 each
+// on 64 workgroups in 0.52 ms, 1.29e11 flop/s), a little under.
+constexpr double SPREAD_WG_FLOPS_PER_S = 1.2e11;
+
 template <int BM, int BN, int BK, int WM, int WN, bool MOM>
 hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
-                        float lr, float mu, hipStream_t stream)
+                        float lr, float mu, double spread_s, hipStream_t stream)
 {
     constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
     const int64_t tiles_m = (M + BM - 1) / BM;
@@ -702,8 +730,25 @@ hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, in
         return hipErrorInvalidValue;
     const int t = static_cast<int>(tiles_m * tiles_n), tmi = static_cast<int>(tiles_m),
               tni = static_cast<int>(tiles_n);
-    if (direct_fits(M, N, K, BM, BN, BK))
-        sf_apply_kernel<BM, BN, BK, WM, WN, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni, buf, mu);
+    if (direct_fits(M, N, K, BM, BN, BK)) {
+        // Spread: as few workgroups (a multiple of 8) as walk the tiles
+        // within spread_s at SPREAD_WG_FLOPS_PER_S each.
+        int grid = t;
+        if (spread_s > 0.0) {
+            const double per = spread_s * SPREAD_WG_FLOPS_PER_S / (2.0 * BM * BN * static_cast<double>(K));
+            if (per >= 2.0) {
+                const int64_t p = per < t ? static_cast<int64_t>(per) : t;
+                const int64_t g = ((t + p - 1) / p + NUM_XCD - 1) / NUM_XCD * NUM_XCD;
+                if (g < t)
+                    grid = static_cast<int>(g);
+            }
+        }
+        if (grid < t)
+            sf_apply_walk_kernel<BM, BN, BK, WM, WN, MOM><<<grid, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
+                                                                                  buf, mu);
+        else
+            sf_apply_kernel<BM, BN, BK, WM, WN, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni, buf, mu);
+    }
     else if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
         sf_apply_staged_kernel<BM, BN, BK, WM, WN, false, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
                                                                                      buf, mu);
@@ -718,26 +763,26 @@ hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, in
 // (32 x 32 per wave, K-slices of 32) so that small layers still fill the chip.
 template <bool MOM>
 hipError_t launch_sf(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
-                     float mu, hipStream_t stream)
+                     float mu, double spread_s, hipStream_t stream)
 {
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
     if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_tiles<128, 128, 16, 64, 64, MOM>(W, buf, U, V, M, N, K, lr, mu, stream);
-    return launch_tiles<64, 64, 32, 32, 32, MOM>(W, buf, U, V, M, N, K, lr, mu, stream);
+        return launch_tiles<128, 128, 16, 64, 64, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, stream);
+    return launch_tiles<64, 64, 32, 32, 32, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, stream);
 }
 
 }  // namespace
 
 hipError_t launch_sf_apply(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
-                           hipStream_t stream)
+                           hipStream_t stream, double spread_s)
 {
-    return launch_sf<false>(W, nullptr, U, V, M, N, K, lr, 0.f, stream);
+    return launch_sf<false>(W, nullptr, U, V, M, N, K, lr, 0.f, spread_s, stream);
 }
 
 hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N,
-                                    int64_t K, float lr, float mu, hipStream_t stream)
+                                    int64_t K, float lr, float mu, hipStream_t stream, double spread_s)
 {
-    return launch_sf<true>(W, buf, U, V, M, N, K, lr, mu, stream);
+    return launch_sf<true>(W, buf, U, V, M, N, K, lr, mu, spread_s, stream);
 }
 
 // Grouped launch: every layer the LDS-direct 128 x 128 tile covers joins one

@@ -158,6 +158,15 @@ constexpr double ONE_STREAM_BELOW_S = 30e-6;
 // two streams (VGG19-22K: 0.19; the Inception-shaped workload: 0.05;
 // that 4096 x 4096 layer through both schemes: 0.41).
 constexpr double CORUN_MAX_RATIO = 0.35;
+// When the PS applies are the longer kind on two streams, every SF launch is
+// spread over few workgroups that walk its tiles, given this fraction of the
+// applies' estimated time (each layer its share by flops): thin beside the
+// HBM-bound applies the rebuilds take less from them than a short full-chip
+// launch does (Inception-shaped iteration 0.651 -> 0.637 ms, its 1000 x 2048
+// classifier on 64 workgroups for 0.52 ms instead of 512 for 0.08 ms; 48 or
+// 56 workgroups, whose rebuild outlasts the applies, 0.67-0.69 ms; 72-96,
+// 0.647 ms).
+constexpr double SF_SPREAD_OF_PS = 0.9;
 
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
 // for the work enqueued on `stream` before the call) and of
@@ -279,7 +288,14 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // SFB layer keeps its own launch, so that each starts as soon as its own
     // backward pass has run.
     const bool sfb_last = per && pool->wfbp_policy == POSEIDON_WFBP_SFB_LAST;
-    const bool group_sf = (!per || sfb_last) && plain_sf > 1;
+    const int32_t S = static_cast<int32_t>(pool->streams.size());
+    const bool tiny = t_sf + t_ps < ONE_STREAM_BELOW_S;
+    // With ready events the second stream also lets the updates start while
+    // the caller's backward pass still runs, so it is kept.
+    const bool balanced = !per && std::min(t_sf, t_ps) > CORUN_MAX_RATIO * std::max(t_sf, t_ps);
+    // Spread SF launches (below) replace the grouped one.
+    const bool spread = !ready && S > 1 && !tiny && !balanced && t_ps > t_sf && sf_flops > 0.0;
+    const bool group_sf = (!per || sfb_last) && plain_sf > 1 && !spread;
     std::vector<SfTensor> grouped;   // in backpropagation order
     if (group_sf)
         for (int32_t t = count - 1; t >= 0; --t) {
@@ -296,16 +312,12 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (launches == 0)
         return POSEIDON_OK;
 
-    // Stream assignment: the compute-bound SF reconstructions go to the pool's
-    // first stream, the bandwidth-bound PS applies to the second, in
-    // backpropagation order, so that the two kinds overlap on the GPU instead
-    // of queueing behind each other.  A one-stream pool, or an iteration too
-    // small to gain from the overlap, serialises everything on the first.
-    const int32_t S = static_cast<int32_t>(pool->streams.size());
-    const bool tiny = t_sf + t_ps < ONE_STREAM_BELOW_S;
-    // With ready events the second stream also lets the updates start while
-    // the caller's backward pass still runs, so it is kept.
-    const bool balanced = !per && std::min(t_sf, t_ps) > CORUN_MAX_RATIO * std::max(t_sf, t_ps);
+    // Stream assignment: the compute-bound SF reconstructions and the
+    // bandwidth-bound PS applies go to two streams (below: which), each kind
+    // in backpropagation order, so that the two kinds overlap on the GPU
+    // instead of queueing behind each other.  A one-stream pool, or an
+    // iteration too small or too balanced to gain from the overlap,
+    // serialises everything on one.
     const int32_t used = (S > 1 && launches > 1 && !tiny && !balanced) ? 2 : 1;
     hipEvent_t waited[2] = {nullptr, nullptr};   // last ready event each used stream waits on
     // An iteration issued on one stream that waits for nothing but the
@@ -324,8 +336,11 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (direct)
         st[0] = stream;
     int32_t forked = -1;   // split: the lane (0 SFB, 1 PS) on the pool stream
+    double sf_spread = 0.0;   // seconds per flop given to the SF launches
     if (split) {
         const int32_t crit = t_sf >= t_ps ? 0 : 1;
+        if (spread && crit == 1)
+            sf_spread = SF_SPREAD_OF_PS * t_ps / sf_flops;
         forked = 1 - crit;
         st[crit] = stream;
         st[forked] = pool->streams[0];
@@ -421,8 +436,10 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
                 continue;
             }
             if (!timed(s, POSEIDON_SFB, t, 0, [&] {
-                    return x.buf ? launch_sf_apply_momentum(x.W, x.buf, x.U, x.V, x.M, x.N, K, lr, momentum, s)
-                                 : launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s);
+                    const double spread_s = sf_spread * 2.0 * static_cast<double>(n) * static_cast<double>(K);
+                    return x.buf ? launch_sf_apply_momentum(x.W, x.buf, x.U, x.V, x.M, x.N, K, lr, momentum, s,
+                                                            spread_s)
+                                 : launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s, spread_s);
                 }))
                 return POSEIDON_ERR_HIP;
         } else {

@@ -376,3 +376,60 @@ def test_sync_iteration_is_ordered_on_the_callers_stream(cfg, only):
                                       wl.momentum if b0 is not None else 0.0, b0)
             assert_close(to_np(c).reshape(-1), want, W_TOL, name)
     pool.close()
+
+
+@pytest.mark.parametrize("case", ["64-tiles", "64-tiles-momentum", "128-tiles", "128-tiles-momentum"])
+def test_sync_iteration_spreads_the_rebuilds_beside_longer_applies(case):
+    """When the PS applies are the longer kind on two streams, each SFB
+    rebuild runs on few workgroups that walk its tiles (the 1000 x 2048
+    classifier at K = 1024 with two Inception-sized conv kernels at P = 32;
+    a 4096 x 4096 layer at K = 32 with a 4M-value tensor at P = 8, whose
+    tiles are 128 x 128).  The walk runs the one-tile kernel's code, so W
+    (and buf) are bitwise those of poseidon_sf_apply(_momentum); and they,
+    and the applies, match the oracle."""
+    d = dev()
+    small = case.startswith("64")
+    if small:
+        (M, N), B, P, sizes = (1000, 2048), 32, 32, [2460843, 2786166]
+    else:
+        (M, N), B, P, sizes = (4096, 4096), 4, 8, [4 << 20]
+    assert oracle.best_scheme(True, M, N, B, P) == oracle.SFB
+    K, lr, mu = B * P, 0.01, 0.9
+    base = 31000 + 100 * len(case)
+    fc = {"fc": True, "W": I.randn(base, (M, N), 0.01), "U": I.randn(base + 1, (K, M), 0.1),
+          "V": I.randn(base + 2, (K, N), 0.1)}
+    if case.endswith("momentum"):
+        fc["buf"] = I.randn(base + 4, (M, N), 1e-3)
+    host = [{"fc": False, "W": I.randn(base + 10 + i, (n,), 0.01), "shards": I.randn(base + 11 + i, (P, n), 1e-3),
+             "buf": I.randn(base + 12 + i, (n,), 1e-3)} for i, n in enumerate(sizes)] + [fc]
+    devt = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in host]
+    Wc, Uc, Vc = host[-1]["W"].to(d), host[-1]["U"].to(d), host[-1]["V"].to(d)
+    log(f"sync_iteration spread rebuild: {case}, FC {M}x{N} K={K}, PS {sizes} at P={P}")
+    pool = api.StreamPool(2)
+    schemes = api.SyncIteration(pool, devt, B, P, lr, mu)()
+    if "buf" in fc:
+        bc = host[-1]["buf"].to(d)
+        api.sf_apply_momentum(Wc, bc, Uc, Vc, lr, mu)
+    else:
+        api.sf_apply(Wc, Uc, Vc, lr)
+    torch.cuda.synchronize()
+    assert schemes == [api.PS] * len(sizes) + [api.SFB]
+    assert torch.equal(devt[-1]["W"], Wc)
+    if "buf" in fc:
+        assert torch.equal(devt[-1]["buf"], bc)
+    r, c = sample_points(M, N, 2000, seed=M)
+    if "buf" in fc:
+        w_ref, b_ref = oracle.sf_apply_momentum_points(fc["W"].numpy(), fc["buf"].numpy(), fc["U"].numpy(),
+                                                       fc["V"].numpy(), lr, mu, r, c)
+        assert_close(to_np(Wc)[r, c], w_ref, W_TOL, "W")
+        assert_close(to_np(bc)[r, c], b_ref, BUF_TOL, "buf")
+    else:
+        assert_close(to_np(Wc)[r, c], oracle.sf_apply_points(fc["W"].numpy(), fc["U"].numpy(), fc["V"].numpy(),
+                                                             lr, r, c), W_TOL, "W")
+    for h, g in zip(host[:-1], devt[:-1]):
+        n = h["W"].numel()
+        idx = np.concatenate([np.random.default_rng(n).integers(0, n, 3000), np.arange(n - 64, n)])
+        w_ref, b_ref = oracle.ps_apply_points(h["W"].numpy(), h["shards"].numpy(), lr, mu, h["buf"].numpy(), idx)
+        assert_close(to_np(g["W"])[idx], w_ref, W_TOL, f"PS {n} W")
+        assert_close(to_np(g["buf"])[idx], b_ref, BUF_TOL, f"PS {n} buf")
+    pool.close()
