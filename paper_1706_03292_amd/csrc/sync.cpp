@@ -2,9 +2,9 @@
 // (Sec. 3 "wait-free backpropagation"; Sec. 4.1 "Client Library", "Managing
 // Consistency"; Alg. 2).  The host walks the tensors in backpropagation
 // order, asks Alg. 1 for each one's scheme, and enqueues the matching update
-// on the next stream of the pool; a fork event and one join event per stream
-// make the whole iteration a single asynchronous operation on the caller's
-// stream (the bulk-synchronous barrier).
+// on the caller's stream or a stream of the pool; a fork event and a join
+// event per pool stream used make the whole iteration a single asynchronous
+// operation on the caller's stream (the bulk-synchronous barrier).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
