@@ -378,7 +378,8 @@ def test_sync_iteration_is_ordered_on_the_callers_stream(cfg, only):
     pool.close()
 
 
-@pytest.mark.parametrize("case", ["64-tiles", "64-tiles-momentum", "128-tiles", "128-tiles-momentum"])
+@pytest.mark.parametrize("case", ["64-tiles", "64-tiles-momentum", "128-tiles", "128-tiles-momentum",
+                                  "64-tiles-ragged", "128-tiles-ragged"])
 def test_sync_iteration_spreads_the_rebuilds_beside_longer_applies(case):
     """When the PS applies are the longer kind on two streams, each SFB
     rebuild runs on few workgroups that walk its tiles (the 1000 x 2048
@@ -386,10 +387,13 @@ def test_sync_iteration_spreads_the_rebuilds_beside_longer_applies(case):
     a 4096 x 4096 layer at K = 32 with a 4M-value tensor at P = 8, whose
     tiles are 128 x 128).  The walk runs the one-tile kernel's code, so W
     (and buf) are bitwise those of poseidon_sf_apply(_momentum); and they,
-    and the applies, match the oracle."""
+    and the applies, match the oracle.  The ragged cases take K = 21 and 40
+    (one and three K-slices) and tiles cut by the matrix edges."""
     d = dev()
     small = case.startswith("64")
-    if small:
+    if case.endswith("ragged"):      # K not a multiple of the K-slice (an odd slice count), ragged tile edges
+        (M, N), B, P, sizes = ((1000, 2048), 7, 3, [5_400_001]) if small else ((4100, 4000), 5, 8, [4_194_303])
+    elif small:
         (M, N), B, P, sizes = (1000, 2048), 32, 32, [2460843, 2786166]
     else:
         (M, N), B, P, sizes = (4096, 4096), 4, 8, [4 << 20]
