@@ -508,8 +508,8 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
  * events but holds the SFB rebuilds until every tensor's event has completed
  * and runs them as one grouped launch.  POSEIDON_WFBP_ALL_LAST (the default)
  * holds every update until every tensor's event has completed and then
- * issues exactly poseidon_sync_iteration's launches: the serial order, as a
- * fallback for a GPU that has no idle time to fill.  On one GPU the updates
+ * issues poseidon_sync_iteration's launches (on the pool's streams): the
+ * serial order, as a fallback for a GPU that has no idle time to fill.  On one GPU the updates
  * are local computation that competes with the caller's backward pass: the
  * rebuilds for the matrix cores its GEMMs use, the applies for the memory
  * bandwidth and CU slots of its elementwise steps.  Measured on a 34.6 ms

@@ -293,8 +293,9 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // With ready events the second stream also lets the updates start while
     // the caller's backward pass still runs, so it is kept.
     const bool balanced = !per && std::min(t_sf, t_ps) > CORUN_MAX_RATIO * std::max(t_sf, t_ps);
-    // Spread SF launches (below) replace the grouped one.
-    const bool spread = !ready && S > 1 && !tiny && !balanced && t_ps > t_sf && sf_flops > 0.0;
+    // Spread SF launches (below) replace the grouped one; under the held
+    // schedule the launches are the plain iteration's, spread included.
+    const bool spread = (!ready || all_last) && S > 1 && !tiny && !balanced && t_ps > t_sf && sf_flops > 0.0;
     const bool group_sf = (!per || sfb_last) && plain_sf > 1 && !spread;
     std::vector<SfTensor> grouped;   // in backpropagation order
     if (group_sf)
@@ -336,11 +337,10 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (direct)
         st[0] = stream;
     int32_t forked = -1;   // split: the lane (0 SFB, 1 PS) on the pool stream
-    double sf_spread = 0.0;   // seconds per flop given to the SF launches
+    // Seconds per flop given to the SF launches when they are spread.
+    const double sf_spread = (spread && used == 2) ? SF_SPREAD_OF_PS * t_ps / sf_flops : 0.0;
     if (split) {
         const int32_t crit = t_sf >= t_ps ? 0 : 1;
-        if (spread && crit == 1)
-            sf_spread = SF_SPREAD_OF_PS * t_ps / sf_flops;
         forked = 1 - crit;
         st[crit] = stream;
         st[forked] = pool->streams[0];

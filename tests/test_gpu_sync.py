@@ -386,8 +386,9 @@ def test_sync_iteration_spreads_the_rebuilds_beside_longer_applies(case):
     classifier at K = 1024 with two Inception-sized conv kernels at P = 32;
     a 4096 x 4096 layer at K = 32 with a 4M-value tensor at P = 8, whose
     tiles are 128 x 128).  The walk runs the one-tile kernel's code, so W
-    (and buf) are bitwise those of poseidon_sf_apply(_momentum); and they,
-    and the applies, match the oracle.  The ragged cases take K = 21 and 40
+    (and buf) are bitwise those of poseidon_sf_apply(_momentum), and of the
+    held wait-free schedule's iteration; and they, and the applies, match
+    the oracle.  The ragged cases take K = 21 and 40
     (one and three K-slices) and tiles cut by the matrix edges."""
     d = dev()
     small = case.startswith("64")
@@ -421,6 +422,18 @@ def test_sync_iteration_spreads_the_rebuilds_beside_longer_applies(case):
     assert torch.equal(devt[-1]["W"], Wc)
     if "buf" in fc:
         assert torch.equal(devt[-1]["buf"], bc)
+    # The held wait-free schedule issues the same (spread) launches on the
+    # pool's streams: bitwise the same updates.
+    held = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in host]
+    cs = torch.cuda.current_stream(d)
+    ev = torch.cuda.Event()
+    ev.record(cs)
+    api.SyncIteration(pool, held, B, P, lr, mu)(cs, ready=[ev] * len(held))
+    torch.cuda.synchronize()
+    for g, h in zip(devt, held):
+        assert torch.equal(g["W"], h["W"])
+        if "buf" in g:
+            assert torch.equal(g["buf"], h["buf"])
     r, c = sample_points(M, N, 2000, seed=M)
     if "buf" in fc:
         w_ref, b_ref = oracle.sf_apply_momentum_points(fc["W"].numpy(), fc["buf"].numpy(), fc["U"].numpy(),
