@@ -36,6 +36,7 @@
 // Operands whose byte offsets do not fit the 32-bit buffer offsets (K*M or
 // K*N of 2^29 elements and more, or rows over 4,194,303 elements) take a
 // register-staged variant of the same tile with 64-bit addressing.
+#include <atomic>
 #include <vector>
 
 #include "common.h"
@@ -625,11 +626,11 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_kernel(
 // grid-stride.  A kernel of its own: the loop makes the compiler keep more
 // values live (the 128 x 128 tile spilled 61 VGPRs at the one-tile kernel's
 // 128), and a spread launch has few workgroups resident, so it is compiled
-// for 2 waves per SIMD.  The barrier keeps a wave's first loads of the next
+// for 2 waves per SIMD (two workgroups per CU).  The barrier keeps a wave's first loads of the next
 // tile out of the LDS stage the others may still read.
 template <int BM, int BN, int BK, int WM, int WN, bool MOM>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(1, 2))) void sf_apply_walk_kernel(
+__attribute__((amdgpu_waves_per_eu(2, 2))) void sf_apply_walk_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
     float lr, int tiles_m, int tiles_n, float* __restrict__ buf, float mu)
 {
@@ -722,6 +723,23 @@ bool direct_fits(int64_t M, int64_t N, int64_t K, int BM, int BN, int BK)
     return (K + BK) * M * 4 < LIM && (K + BK) * N * 4 < LIM && (static_cast<int64_t>(BM) * N + BN) * 4 < LIM;
 }
 
+// Workgroups of the spread kernel that one CU holds at once (its register
+// and LDS needs; cached per instantiation).
+template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+int64_t walk_groups_per_cu()
+{
+    static std::atomic<int> cached{0};
+    int n = cached.load(std::memory_order_relaxed);
+    if (n > 0)
+        return n;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, sf_apply_walk_kernel<BM, BN, BK, WM, WN, MOM>,
+                                                     SfTile<BM, BN, BK, WM, WN>::THREADS, 0) != hipSuccess ||
+        n < 1)
+        n = 1;
+    cached.store(n, std::memory_order_relaxed);
+    return n;
+}
+
 // A workgroup's rate when few of them walk a layer's tiles beside the PS
 // applies (the 1000 x 2048 classifier at K = 1024: 8 tiles of 64 x 64 each
 // on 64 workgroups in 0.52 ms, 1.29e11 flop/s), a little under.
@@ -740,14 +758,17 @@ hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, in
               tni = static_cast<int>(tiles_n);
     if (direct_fits(M, N, K, BM, BN, BK)) {
         // Spread: as few workgroups (a multiple of 8) as walk the tiles
-        // within spread_s at SPREAD_WG_FLOPS_PER_S each.
+        // within spread_s at SPREAD_WG_FLOPS_PER_S each -- provided the chip
+        // holds them all at once (otherwise the later ones would wait for
+        // the first to finish all their tiles).
         int grid = t;
         if (spread_s > 0.0) {
             const double per = spread_s * SPREAD_WG_FLOPS_PER_S / (2.0 * BM * BN * static_cast<double>(K));
             if (per >= 2.0) {
                 const int64_t p = per < t ? static_cast<int64_t>(per) : t;
                 const int64_t g = ((t + p - 1) / p + NUM_XCD - 1) / NUM_XCD * NUM_XCD;
-                if (g < t)
+                const int64_t resident = walk_groups_per_cu<BM, BN, BK, WM, WN, MOM>() * device_cu_count();
+                if (g < t && g <= resident)
                     grid = static_cast<int>(g);
             }
         }
