@@ -227,6 +227,73 @@ int main(void)
         free(W1), free(U), free(V), free(g1), free(W2), free(G), free(B2), free(g2);
     }
 
+    /* Two-stream iterations on a caller's stream of its own, each followed on
+     * that stream by a copy of the weights taken with no synchronisation in
+     * between (the iteration is one operation on the caller's stream):
+     * (a) the PS apply the longer kind (8M values at P = 4 beside a
+     *     1000 x 2048 layer at K = 32: the rebuild spread thin beside it);
+     * (b) the SF rebuild the longer kind (4096 x 4096 at K = 128 beside a
+     *     1M-value tensor at P = 4: the rebuild on the caller's stream). */
+    for (int c = 0; c < 2; ++c) {
+        const int64_t M = c == 0 ? 1000 : 4096, N = c == 0 ? 2048 : 4096;
+        const int64_t n = c == 0 ? (int64_t)8 << 20 : (int64_t)1 << 20;
+        const int64_t Bsz = c == 0 ? 8 : 32;
+        const int32_t P = 4;
+        const int64_t K = P * Bsz;
+        float *W1 = malloc(M * N * 4), *U = malloc(K * M * 4), *V = malloc(K * N * 4), *g1 = malloc(M * N * 4);
+        float *W2 = malloc(n * 4), *G = malloc(P * n * 4), *B2 = malloc(n * 4), *g2 = malloc(n * 4);
+        fill(W1, M * N, 20 + c, 0.01f);
+        fill(U, K * M, 22 + c, 0.1f);
+        fill(V, K * N, 24 + c, 0.1f);
+        fill(W2, n, 26 + c, 0.01f);
+        fill(G, P * n, 28 + c, 1e-3f);
+        fill(B2, n, 30 + c, 1e-3f);
+        float *dW1 = dev_copy(W1, M * N), *dU = dev_copy(U, K * M), *dV = dev_copy(V, K * N);
+        float *dW2 = dev_copy(W2, n), *dG = dev_copy(G, P * n), *dB2 = dev_copy(B2, n);
+        float *cW1 = NULL, *cW2 = NULL;
+        HIP_OK(hipMalloc((void **)&cW1, (size_t)(M * N) * 4));
+        HIP_OK(hipMalloc((void **)&cW2, (size_t)n * 4));
+        hipStream_t cs;
+        HIP_OK(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
+        poseidon_stream_pool *pool = NULL;
+        int rc = poseidon_pool_create(2, &pool);
+        poseidon_tensor t[2];
+        memset(t, 0, sizeof t);
+        t[0].kind = POSEIDON_KIND_FC;
+        t[0].W = dW1, t[0].M = M, t[0].N = N, t[0].U = dU, t[0].V = dV;
+        t[1].kind = POSEIDON_KIND_OTHER;
+        t[1].W = dW2, t[1].M = n, t[1].N = 1, t[1].shards = dG, t[1].buf = dB2;
+        int32_t schemes[2] = {-9, -9};
+        if (rc == POSEIDON_OK)
+            rc = poseidon_sync_iteration(pool, t, 2, Bsz, P, 0.01f, 0.9f, cs, schemes);
+        HIP_OK(hipMemcpyAsync(cW1, dW1, (size_t)(M * N) * 4, hipMemcpyDeviceToDevice, cs));
+        HIP_OK(hipMemcpyAsync(cW2, dW2, (size_t)n * 4, hipMemcpyDeviceToDevice, cs));
+        HIP_OK(hipStreamSynchronize(cs));
+        to_host(g1, cW1, M * N);
+        to_host(g2, cW2, n);
+        poseidon_pool_destroy(pool);
+        HIP_OK(hipStreamDestroy(cs));
+        oracle_sf_apply(W1, U, V, M, N, K, 0.01f);
+        oracle_ps_apply(W2, G, P, n, 0.01f, 0.9f, B2);
+        const int ok = rc == POSEIDON_OK && schemes[0] == POSEIDON_SFB && schemes[1] == POSEIDON_PS;
+        printf("%-44s rc %d, schemes %d %d %s\n", c == 0 ? "two streams, PS longer: rc" : "two streams, SF longer: rc",
+               rc, schemes[0], schemes[1], ok ? "ok" : "FAIL");
+        failures += !ok;
+        check(c == 0 ? "two streams, PS longer (FC layer, spread)" : "two streams, SF longer (FC layer)", g1, W1, M * N,
+              1e-4);
+        check(c == 0 ? "two streams, PS longer (dense tensor)" : "two streams, SF longer (dense tensor)", g2, W2, n,
+              1e-4);
+        HIP_OK(hipFree(dW1));
+        HIP_OK(hipFree(dU));
+        HIP_OK(hipFree(dV));
+        HIP_OK(hipFree(dW2));
+        HIP_OK(hipFree(dG));
+        HIP_OK(hipFree(dB2));
+        HIP_OK(hipFree(cW1));
+        HIP_OK(hipFree(cW2));
+        free(W1), free(U), free(V), free(g1), free(W2), free(G), free(B2), free(g2);
+    }
+
     /* The KV store: every server of P = 3 applies its pairs from the workers'
      * messages; together they equal the plain PS apply of the whole tensor. */
     {
