@@ -23,9 +23,10 @@
 // an MFMA operand read (rows k and k+1) hit disjoint LDS banks.
 //
 // The SGD update is the epilogue: W is read once and written once, straight
-// from the accumulators, so the gradient is never materialised.  On tiles that
-// lie wholly inside W the first block of W is loaded before the last K step
-// (its latency hides behind that step's MFMAs) and no access carries a
+// from the accumulators, so the gradient is never materialised, with
+// non-temporal accesses that leave the L2 to the operand panels.  On tiles
+// that lie wholly inside W the first block of W is loaded before the last K
+// step (its latency hides behind that step's MFMAs) and no access carries a
 // per-element branch.
 //
 // Tile order: the hardware hands consecutive workgroups to the 8 XCDs in turn,
@@ -36,6 +37,10 @@
 // Operands whose byte offsets do not fit the 32-bit buffer offsets (K*M or
 // K*N of 2^29 elements and more, or rows over 4,194,303 elements) take a
 // register-staged variant of the same tile with 64-bit addressing.
+//
+// Launch forms: one workgroup per tile (a layer, or several layers of one K
+// as one grouped tile list), or a spread launch whose few workgroups each
+// walk several tiles, for running the rebuild thin beside longer PS work.
 #include <atomic>
 #include <vector>
 
