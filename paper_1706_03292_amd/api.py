@@ -60,6 +60,28 @@ def _uses(stream, *tensors) -> None:
                 t.record_stream(stream)
 
 
+def _stream_id(stream):
+    """The raw handle of a torch stream, else None (``stream`` None or a raw
+    handle, for which _uses records nothing)."""
+    return stream.cuda_stream if isinstance(stream, torch.cuda.Stream) else None
+
+
+class _KeptUses:
+    """_uses for tensors an object keeps for its whole life: the caching
+    allocator, when such a tensor is freed, waits for the work enqueued up to
+    then on every stream it was recorded on, so one record per stream is
+    enough -- later calls on a stream already recorded cost nothing."""
+
+    def __init__(self, tensors):
+        self._tensors = [t for t in tensors if t is not None]
+        self._streams = set()
+
+    def __call__(self, stream) -> None:
+        if isinstance(stream, torch.cuda.Stream) and stream.cuda_stream not in self._streams:
+            _uses(stream, *self._tensors)
+            self._streams.add(stream.cuda_stream)
+
+
 def _same_device(*ts):
     devs = {t.device for t in ts if t is not None}
     if len(devs) > 1:
@@ -314,6 +336,7 @@ class SyncIteration:
         self._arr = arr
         self._schemes = (ctypes.c_int32 * max(1, len(tensors)))()
         self.count = len(tensors)
+        self._kept_uses = _KeptUses([x for keep in self._keep for x in keep])
 
     def __call__(self, stream=None, ready=None) -> list[int]:
         """Enqueue the iteration on ``stream`` (default: the current stream).
@@ -326,7 +349,7 @@ class SyncIteration:
         # Every update joins back into `stream`; work on another torch stream
         # than the current one must be known to the caching allocator.
         if isinstance(stream, torch.cuda.Stream) and stream != torch.cuda.current_stream(self.pool.device):
-            _uses(stream, *[x for keep in self._keep for x in keep])
+            self._kept_uses(stream)
         with torch.cuda.device(self.pool.device):
             if ready is None:
                 _check("poseidon_sync_iteration", L.lib().poseidon_sync_iteration(
@@ -428,6 +451,7 @@ class KVStore:
                                                                     ctypes.byref(self._h)))
         self.pairs = kv_layout(self.sizes, pair_elems, P)
         self._msg_len = self.message_size()
+        self._kept_uses = _KeptUses([x for pair in self._keep for x in pair])
 
     def begin(self) -> None:
         _check("poseidon_kv_begin", L.lib().poseidon_kv_begin(self._h))
@@ -443,10 +467,12 @@ class KVStore:
         with torch.cuda.device(self.device):
             done = _check("poseidon_kv_receive", L.lib().poseidon_kv_receive(
                 self._h, int(worker), int(tensor), grad.data_ptr(), _stream_handle(stream, self.device)))
-        self._grads[(worker, tensor)] = grad
+        sid = _stream_id(stream)
+        self._grads[(worker, tensor)] = (grad, sid)
         if done:       # an apply was enqueued: it reads the tensor's updates and writes its W and buf
-            _uses(stream, *self._keep[tensor],
-                  *[g for (_, k), g in self._grads.items() if k == tensor or k == "message"])
+            self._kept_uses(stream)
+            _uses(stream, *[g for (_, k), (g, s_) in self._grads.items()
+                            if (k == tensor or k == "message") and s_ != sid])
         return done
 
     def receive_message(self, worker: int, message: torch.Tensor, stream=None) -> int:
@@ -462,9 +488,11 @@ class KVStore:
             done = _check("poseidon_kv_receive_message", L.lib().poseidon_kv_receive_message(
                 self._h, int(worker), message.data_ptr() if message.numel() else None,
                 _stream_handle(stream, self.device)))
-        self._grads[(worker, "message")] = message
+        sid = _stream_id(stream)
+        self._grads[(worker, "message")] = (message, sid)
         if done:       # applies were enqueued: they read the updates and write W and buf
-            _uses(stream, *[x for pair in self._keep for x in pair], *self._grads.values())
+            self._kept_uses(stream)
+            _uses(stream, *[g for g, s_ in self._grads.values() if s_ != sid])
         return done
 
     def message_size(self) -> int:
