@@ -1,7 +1,6 @@
 // The per-group update of the parameter-server apply (Sec. 2.1 "Parameter
 // Server"; Sec. 4.1 "KV Store"), shared by every kernel that applies dense
-// updates: the single-tensor, batched and KV-store launches and the grouped
-// launch that co-schedules the applies with the SF reconstruction.
+// updates: the single-tensor, batched and KV-store launches.
 //
 //   s_i = sum_{p<P} G_p[i]   (p increasing, fp32)
 //   buf_i = fma(mu, buf_i, s_i);  W_i = fma(-lr, buf_i, W_i)
