@@ -439,7 +439,12 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * -- except in a two-stream iteration whose PS applies are the longer kind:
  * there every SFB launch runs on few workgroups that each walk several of
  * its tiles, sized to take about 90% of the applies' estimated time, so that
- * the rebuilds run thin beside the applies.
+ * the rebuilds run thin beside the applies.  Conversely, when the SFB
+ * rebuilds are the longer kind (and the applies would still end first at
+ * 1.3 TB/s), the rebuilds leave each SIMD the registers of one more wave and
+ * the PS applies of aligned tensors use a low-register kernel that runs in
+ * them, on the CUs the rebuilds keep busy.  Every variant computes the same
+ * results, bitwise.
  * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
  * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
  * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,

@@ -62,11 +62,15 @@ int device_cu_count();
 
 // Internal launchers (arguments already validated; nonzero sizes).  Given
 // spread_s > 0, an SF launch runs on as few workgroups as would walk its
-// tiles in about spread_s seconds, instead of one workgroup per tile.
+// tiles in about spread_s seconds, instead of one workgroup per tile.  Given
+// `room`, the SF tiles leave each SIMD the registers of one wave of the lean
+// PS kernel beside four of theirs, and a PS launch given `beside_sf` uses
+// that kernel (aligned tensors), so that the two run on the same CUs.
 hipError_t launch_sf_apply(float* W, const float* U, const float* V,
-                           int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream, double spread_s = 0.0);
+                           int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream, double spread_s = 0.0,
+                           bool room = false);
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
-                           float lr, float momentum, float* buf, hipStream_t stream);
+                           float lr, float momentum, float* buf, hipStream_t stream, bool beside_sf = false);
 hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M,
                                     int64_t N, int64_t K, float lr, float mu, hipStream_t stream,
                                     double spread_s = 0.0);
@@ -83,7 +87,7 @@ constexpr int SF_BATCH_MAX = 16;   // layers per grouped launch (kernel-argument
 
 // Every layer with work, grouped into as few launches as possible (validated).
 hipError_t launch_sf_apply_batch(const SfTensor* layers, int32_t count, int64_t K, float lr,
-                                 hipStream_t stream);
+                                 hipStream_t stream, bool room = false);
 
 // One dense tensor of a batched PS apply (same layout as poseidon_ps_tensor).
 struct PsTensor {

@@ -64,10 +64,84 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_kernel(float* __restrict_
         apply_group<PT, MOM, AL>(W, buf, src, P, 4 * i, n, lr, mu);
 }
 
+// ---------------------------------------------------------------------------
+// One tensor beside the SF rebuild.  The rebuild's tiles, launched with room
+// for it, take 118 VGPRs, so a SIMD's four SF waves leave it 32; a wave of
+// this kernel takes 22: one VGPR offset shared by all of a thread's accesses
+// (buffer loads, the shard stride in the scalar offset), the shard loads
+// LEAN_CHUNK at a time.  It therefore runs on the CUs the rebuild keeps busy,
+// streaming memory while the matrix cores work, instead of waiting for a
+// rebuild workgroup's slot to free up (VGG19-22K iteration 1.702-1.710 ->
+// 1.659-1.675 ms).  One workgroup per CU walks the tensor grid-stride.  The
+// arithmetic and its order are apply_group's: the same results, bitwise.
+// Aligned tensors whose P*n*4 bytes fit 31-bit buffer offsets.
+// ---------------------------------------------------------------------------
+constexpr int LEAN_CHUNK = 4;
+constexpr int BUF_DWORD = 0x00020000;   // buffer resource word 3: raw dword accesses
+constexpr int NT_AUX = 2;               // non-temporal
+
+typedef unsigned u4v __attribute__((ext_vector_type(4)));
+
+__device__ inline f4 lean_ld(__amdgpu_buffer_rsrc_t r, int voff, int soff)
+{
+    return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, NT_AUX));
+}
+
+__device__ inline void lean_st(__amdgpu_buffer_rsrc_t r, int voff, f4 v)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u4v, v), r, voff, 0, NT_AUX);
+}
+
+template <int PT, bool MOM>
+__global__ __launch_bounds__(PS_THREADS) void ps_apply_lean_kernel(float* __restrict__ W, const float* __restrict__ G,
+                                                                   int P, int n, float lr, float mu,
+                                                                   float* __restrict__ buf)
+{
+    const __amdgpu_buffer_rsrc_t gr =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(G), static_cast<short>(0), P * n * 4, BUF_DWORD);
+    const __amdgpu_buffer_rsrc_t wr = __builtin_amdgcn_make_buffer_rsrc(W, static_cast<short>(0), n * 4, BUF_DWORD);
+    const __amdgpu_buffer_rsrc_t br = __builtin_amdgcn_make_buffer_rsrc(buf, static_cast<short>(0), n * 4, BUF_DWORD);
+    const int np = PT > 0 ? PT : P;
+    const int groups = n / 4;
+    for (int i = blockIdx.x * PS_THREADS + threadIdx.x; i < groups; i += gridDim.x * PS_THREADS) {
+        const int vo = i * 16;
+        f4 s = lean_ld(gr, vo, 0);
+        for (int p = 1; p < np; p += LEAN_CHUNK) {
+            f4 g[LEAN_CHUNK];
+#pragma unroll
+            for (int c = 0; c < LEAN_CHUNK; ++c)
+                if (p + c < np)
+                    g[c] = lean_ld(gr, vo, (p + c) * n * 4);
+#pragma unroll
+            for (int c = 0; c < LEAN_CHUNK; ++c)
+                if (p + c < np)
+                    s += g[c];
+            // one chunk in registers at a time
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        f4 w = lean_ld(wr, vo, 0);
+        if constexpr (MOM) {
+            const f4 b = fma4(mu, lean_ld(br, vo, 0), s);
+            lean_st(br, vo, b);
+            w = fma4(-lr, b, w);
+        } else {
+            w = fma4(-lr, s, w);
+        }
+        lean_st(wr, vo, w);
+    }
+}
+
 template <int PT, bool MOM>
 hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, float mu, float* buf, bool al,
-                     hipStream_t stream)
+                     bool beside_sf, hipStream_t stream)
 {
+    if (beside_sf && al && static_cast<int64_t>(P) * n * 4 <= 0x7fffffffLL) {
+        const int64_t want = (n / 4 + PS_THREADS - 1) / PS_THREADS;
+        const int64_t cus = device_cu_count();
+        ps_apply_lean_kernel<PT, MOM><<<static_cast<int>(want < cus ? want : cus), PS_THREADS, 0, stream>>>(
+            W, G, P, static_cast<int>(n), lr, mu, buf);
+        return hipGetLastError();
+    }
     // One group per thread; the grid-stride loop only matters beyond 2^30 workgroups.
     const int64_t want = ((n + 3) / 4 + PS_THREADS - 1) / PS_THREADS;
     const int grid = static_cast<int>(want < PS_MAX_GRID ? want : PS_MAX_GRID);
@@ -80,16 +154,16 @@ hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, f
 
 template <bool MOM>
 hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, float mu, float* buf, bool al,
-                      hipStream_t stream)
+                      bool beside_sf, hipStream_t stream)
 {
     switch (P) {
-    case 1:  return launch_pt<1, MOM>(W, G, P, n, lr, mu, buf, al, stream);
-    case 2:  return launch_pt<2, MOM>(W, G, P, n, lr, mu, buf, al, stream);
-    case 4:  return launch_pt<4, MOM>(W, G, P, n, lr, mu, buf, al, stream);
-    case 8:  return launch_pt<8, MOM>(W, G, P, n, lr, mu, buf, al, stream);
-    case 16: return launch_pt<16, MOM>(W, G, P, n, lr, mu, buf, al, stream);
-    case 32: return launch_pt<32, MOM>(W, G, P, n, lr, mu, buf, al, stream);
-    default: return launch_pt<0, MOM>(W, G, P, n, lr, mu, buf, al, stream);
+    case 1:  return launch_pt<1, MOM>(W, G, P, n, lr, mu, buf, al, beside_sf, stream);
+    case 2:  return launch_pt<2, MOM>(W, G, P, n, lr, mu, buf, al, beside_sf, stream);
+    case 4:  return launch_pt<4, MOM>(W, G, P, n, lr, mu, buf, al, beside_sf, stream);
+    case 8:  return launch_pt<8, MOM>(W, G, P, n, lr, mu, buf, al, beside_sf, stream);
+    case 16: return launch_pt<16, MOM>(W, G, P, n, lr, mu, buf, al, beside_sf, stream);
+    case 32: return launch_pt<32, MOM>(W, G, P, n, lr, mu, buf, al, beside_sf, stream);
+    default: return launch_pt<0, MOM>(W, G, P, n, lr, mu, buf, al, beside_sf, stream);
     }
 }
 
@@ -270,12 +344,12 @@ void launch_kv_mom(const KvArgs& a, int grid, int32_t P, float lr, float mu, hip
 }  // namespace
 
 hipError_t launch_ps_apply(float* W, const float* shards, int32_t P, int64_t n,
-                           float lr, float momentum, float* buf, hipStream_t stream)
+                           float lr, float momentum, float* buf, hipStream_t stream, bool beside_sf)
 {
     const bool al = (n % 4 == 0) && aligned16(W) && aligned16(shards) && (!buf || aligned16(buf));
     if (buf)
-        return launch_mom<true>(W, shards, P, n, lr, momentum, buf, al, stream);
-    return launch_mom<false>(W, shards, P, n, lr, 0.0f, nullptr, al, stream);
+        return launch_mom<true>(W, shards, P, n, lr, momentum, buf, al, beside_sf, stream);
+    return launch_mom<false>(W, shards, P, n, lr, 0.0f, nullptr, al, beside_sf, stream);
 }
 
 hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, float lr, float momentum,

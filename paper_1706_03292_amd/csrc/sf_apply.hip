@@ -110,7 +110,9 @@ __device__ __forceinline__ void zero_acc(f16v (&acc)[TM][TN])
 __device__ __forceinline__ constexpr int acc_row(int i, int r) { return 32 * i + 8 * (r >> 2) + (r & 3); }
 
 // Values of W's first MFMA block that an interior tile loads ahead of the last
-// K step (as many as the register budget holds without spilling).
+// K step (as many as the register budget holds without spilling).  Launches
+// that leave room for PS waves beside the rebuild load none ahead: 118
+// instead of 127 VGPRs, so that a SIMD's four SF waves leave it 32.
 constexpr int W_PRE = 10;
 
 // Cache policy of the epilogue's W and buf accesses: non-temporal (the
@@ -615,7 +617,7 @@ __device__ __forceinline__ void sf_tile_staged(float* As, float* Bs, float* __re
 // ---------------------------------------------------------------------------
 // Kernels, compiled for at least 4 waves per SIMD (at most 128 VGPRs a wave).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+template <int BM, int BN, int BK, int WM, int WN, bool MOM, int PRE = W_PRE>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
@@ -623,7 +625,7 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_kernel(
 {
     int tm, tn;
     tile_coords<8>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
-    sf_tile_direct<BM, BN, BK, WM, WN, MOM>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
+    sf_tile_direct<BM, BN, BK, WM, WN, MOM, PRE>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
 }
 
 // The spread launch: fewer workgroups than tiles (a multiple of 8, so that
@@ -709,14 +711,14 @@ __device__ __forceinline__ void batch_tile(const SfBatchArgs& args, int t, int64
                                                    in / rows, nullptr, 0.f);
 }
 
-template <int BM, int BN, int BK, int WM, int WN>
+template <int BM, int BN, int BK, int WM, int WN, int PRE = W_PRE>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K, float lr)
 {
     const int tiles = args.total_tiles;
     const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
     const int x = blockIdx.x % NUM_XCD, j = blockIdx.x / NUM_XCD;
-    batch_tile<BM, BN, BK, WM, WN>(args, x * q + (x < r ? x : r) + j, K, lr);
+    batch_tile<BM, BN, BK, WM, WN, PRE>(args, x * q + (x < r ? x : r) + j, K, lr);
 }
 
 // True when the LDS-direct tile's 32-bit buffer offsets cover the layer: the
@@ -752,7 +754,7 @@ constexpr double SPREAD_WG_FLOPS_PER_S = 1.2e11;
 
 template <int BM, int BN, int BK, int WM, int WN, bool MOM>
 hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
-                        float lr, float mu, double spread_s, hipStream_t stream)
+                        float lr, float mu, double spread_s, bool room, hipStream_t stream)
 {
     constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
     const int64_t tiles_m = (M + BM - 1) / BM;
@@ -777,9 +779,14 @@ hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, in
                     grid = static_cast<int>(g);
             }
         }
+        // (The momentum epilogue loads no W ahead anyway: 114 VGPRs.)
+        constexpr bool can_drop_pre = !MOM;
         if (grid < t)
             sf_apply_walk_kernel<BM, BN, BK, WM, WN, MOM><<<grid, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
                                                                                   buf, mu);
+        else if (room && can_drop_pre)
+            sf_apply_kernel<BM, BN, BK, WM, WN, MOM, can_drop_pre ? 0 : W_PRE><<<t, NT, 0, stream>>>(
+                W, U, V, M, N, K, lr, tmi, tni, buf, mu);
         else
             sf_apply_kernel<BM, BN, BK, WM, WN, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni, buf, mu);
     }
@@ -797,32 +804,32 @@ hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, in
 // (32 x 32 per wave, K-slices of 32) so that small layers still fill the chip.
 template <bool MOM>
 hipError_t launch_sf(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
-                     float mu, double spread_s, hipStream_t stream)
+                     float mu, double spread_s, bool room, hipStream_t stream)
 {
     const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
     if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_tiles<128, 128, 16, 64, 64, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, stream);
-    return launch_tiles<64, 64, 32, 32, 32, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, stream);
+        return launch_tiles<128, 128, 16, 64, 64, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
+    return launch_tiles<64, 64, 32, 32, 32, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
 }
 
 }  // namespace
 
 hipError_t launch_sf_apply(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
-                           hipStream_t stream, double spread_s)
+                           hipStream_t stream, double spread_s, bool room)
 {
-    return launch_sf<false>(W, nullptr, U, V, M, N, K, lr, 0.f, spread_s, stream);
+    return launch_sf<false>(W, nullptr, U, V, M, N, K, lr, 0.f, spread_s, room, stream);
 }
 
 hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N,
                                     int64_t K, float lr, float mu, hipStream_t stream, double spread_s)
 {
-    return launch_sf<true>(W, buf, U, V, M, N, K, lr, mu, spread_s, stream);
+    return launch_sf<true>(W, buf, U, V, M, N, K, lr, mu, spread_s, false, stream);
 }
 
 // Grouped launch: every layer the LDS-direct 128 x 128 tile covers joins one
 // tile list when the group has at least two tiles per CU; the others, and
 // groups too small to fill the chip, take per-layer launches.
-hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, float lr, hipStream_t stream)
+hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, float lr, hipStream_t stream, bool room)
 {
     constexpr int BM = 128, BN = 128, BK = 16;
     std::vector<int32_t> grouped;
@@ -835,14 +842,14 @@ hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, fl
             grouped.push_back(i);
             tiles += tl;
         } else {
-            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream);
+            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream, 0.0, room);
             if (e != hipSuccess)
                 return e;
         }
     }
     if (tiles < 2 * static_cast<int64_t>(device_cu_count())) {
         for (int32_t i : grouped) {
-            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream);
+            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream, 0.0, room);
             if (e != hipSuccess)
                 return e;
         }
@@ -865,7 +872,10 @@ hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, fl
             first += it.tiles_m * it.tiles_n;
         }
         a.total_tiles = first;
-        sf_apply_batch_kernel<BM, BN, BK, 64, 64><<<first, 256, 0, stream>>>(a, K, lr);
+        if (room)
+            sf_apply_batch_kernel<BM, BN, BK, 64, 64, 0><<<first, 256, 0, stream>>>(a, K, lr);
+        else
+            sf_apply_batch_kernel<BM, BN, BK, 64, 64><<<first, 256, 0, stream>>>(a, K, lr);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;

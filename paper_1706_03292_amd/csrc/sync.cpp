@@ -167,6 +167,15 @@ constexpr double CORUN_MAX_RATIO = 0.35;
 // 56 workgroups, whose rebuild outlasts the applies, 0.67-0.69 ms; 72-96,
 // 0.647 ms).
 constexpr double SF_SPREAD_OF_PS = 0.9;
+// When the SF rebuilds are the longer kind on two streams, the rebuilds
+// leave each SIMD room for one wave of the lean PS kernel and the large PS
+// applies use it, so that they stream memory on the CUs the rebuilds keep
+// busy -- provided the applies still end before the rebuilds: at the lean
+// kernel's rate beside them (1.3 TB/s, one workgroup per CU; VGG19-22K's
+// largest PS tensor, 189 MB in 0.141 ms) they must take at most this
+// fraction of the rebuilds' estimated time.
+constexpr double LEAN_PS_BYTES_PER_S = 1.3e12;
+constexpr double LEAN_OF_SF = 0.85;
 
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
 // for the work enqueued on `stream` before the call) and of
@@ -339,6 +348,9 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     int32_t forked = -1;   // split: the lane (0 SFB, 1 PS) on the pool stream
     // Seconds per flop given to the SF launches when they are spread.
     const double sf_spread = (spread && used == 2) ? SF_SPREAD_OF_PS * t_ps / sf_flops : 0.0;
+    // The PS applies beside the rebuilds on the same CUs (see LEAN_OF_SF).
+    const bool room = (!ready || all_last) && used == 2 && t_sf >= t_ps &&
+                      ps_bytes / LEAN_PS_BYTES_PER_S <= LEAN_OF_SF * t_sf;
     if (split) {
         const int32_t crit = t_sf >= t_ps ? 0 : 1;
         forked = 1 - crit;
@@ -429,7 +441,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
                     grouped_issued = true;
                     if (!timed(s, POSEIDON_SFB, -1, 0, [&] {
                             return launch_sf_apply_batch(grouped.data(), static_cast<int32_t>(grouped.size()), K,
-                                                         lr, s);
+                                                         lr, s, room);
                         }))
                         return POSEIDON_ERR_HIP;
                 }
@@ -439,14 +451,14 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
                     const double spread_s = sf_spread * 2.0 * static_cast<double>(n) * static_cast<double>(K);
                     return x.buf ? launch_sf_apply_momentum(x.W, x.buf, x.U, x.V, x.M, x.N, K, lr, momentum, s,
                                                             spread_s)
-                                 : launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s, spread_s);
+                                 : launch_sf_apply(x.W, x.U, x.V, x.M, x.N, K, lr, s, spread_s, room);
                 }))
                 return POSEIDON_ERR_HIP;
         } else {
             const int32_t si = used == 1 ? 0 : 1;
             hipStream_t s = st[si];
             if (!timed(s, POSEIDON_PS, t, si, [&] {
-                    return launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s);
+                    return launch_ps_apply(x.W, x.shards, P, n, lr, x.buf ? momentum : 0.0f, x.buf, s, room);
                 }))
                 return POSEIDON_ERR_HIP;
         }

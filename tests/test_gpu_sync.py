@@ -450,3 +450,54 @@ def test_sync_iteration_spreads_the_rebuilds_beside_longer_applies(case):
         assert_close(to_np(g["W"])[idx], w_ref, W_TOL, f"PS {n} W")
         assert_close(to_np(g["buf"])[idx], b_ref, BUF_TOL, f"PS {n} buf")
     pool.close()
+
+
+@pytest.mark.parametrize("P", [2, 8, 16, 32])
+def test_sync_iteration_runs_the_applies_beside_longer_rebuilds(P):
+    """When the SF rebuild is the longer kind on two streams, the rebuild
+    leaves room on each SIMD and the aligned PS applies run there with the
+    lean kernel (unaligned and small tensors keep theirs): every update is
+    bitwise that of the single calls (poseidon_sf_apply, poseidon_ps_apply)
+    and matches the oracle.  A 4096 x 4096 layer at K = 1024 beside tensors
+    of 1M (momentum), 500K (plain SGD), 300,001 (unaligned) and 50K values
+    (the batched pass)."""
+    d = dev()
+    M = N = 4096
+    B = 1024 // P
+    K, lr, mu = P * B, 0.01, 0.9
+    assert oracle.best_scheme(True, M, N, B, P) == oracle.SFB
+    base = 41000 + 100 * P
+    fc = {"fc": True, "W": I.randn(base, (M, N), 0.01), "U": I.randn(base + 1, (K, M), 0.1),
+          "V": I.randn(base + 2, (K, N), 0.1)}
+    dense = []
+    for i, (n, with_buf) in enumerate([(1 << 20, True), (500_000, False), (300_001, True), (50_000, True)]):
+        h = {"fc": False, "W": I.randn(base + 10 + 3 * i, (n,), 0.01),
+             "shards": I.randn(base + 11 + 3 * i, (P, n), 1e-3)}
+        if with_buf:
+            h["buf"] = I.randn(base + 12 + 3 * i, (n,), 1e-3)
+        dense.append(h)
+    host = dense + [fc]
+    devt = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in host]
+    single = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in host]
+    log(f"sync_iteration applies beside the rebuild: P={P}, K={K}")
+    pool = api.StreamPool(2)
+    schemes = api.SyncIteration(pool, devt, B, P, lr, mu)()
+    for h in single[:-1]:
+        api.ps_apply(h["W"], h["shards"], lr, mu if "buf" in h else 0.0, h.get("buf"))
+    api.sf_apply(single[-1]["W"], single[-1]["U"], single[-1]["V"], lr)
+    torch.cuda.synchronize()
+    assert schemes == [api.PS] * len(dense) + [api.SFB]
+    for g, h in zip(devt, single):
+        assert torch.equal(g["W"], h["W"])
+        if "buf" in g:
+            assert torch.equal(g["buf"], h["buf"])
+    r, c = sample_points(M, N, 2000, seed=M + P)
+    assert_close(to_np(devt[-1]["W"])[r, c], oracle.sf_apply_points(fc["W"].numpy(), fc["U"].numpy(), fc["V"].numpy(),
+                                                                    lr, r, c), W_TOL, "W")
+    for h, g in zip(dense, devt):
+        b0 = h["buf"].numpy() if "buf" in h else None
+        w_ref, b_ref = oracle.ps_apply(h["W"].numpy(), h["shards"].numpy(), lr, mu if b0 is not None else 0.0, b0)
+        assert_close(to_np(g["W"]), w_ref, W_TOL, f"PS {h['W'].numel()} W")
+        if b0 is not None:
+            assert_close(to_np(g["buf"]), b_ref, BUF_TOL, f"PS {h['W'].numel()} buf")
+    pool.close()
