@@ -28,6 +28,8 @@ if ROOT not in sys.path:
 
 METRIC = "per-iteration sync ms; SFB TFLOP/s + PS apply GB/s vs roofline at P=16"
 PEAK_FP32_MFMA_TFLOPS = 157.3     # MI355X dense fp32 matrix peak
+PEAK_BF16_MFMA_TFLOPS = 2500.0    # MI355X dense bf16 matrix peak
+SPLIT_PRODUCTS = 6                # bf16 products per fp32 multiply-add with the split arithmetic
 PEAK_HBM_GBS = 8000.0             # MI355X HBM3E
 
 
@@ -52,6 +54,8 @@ def _parse():
                     help="fraction of each tensor the CPU oracle runs on")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the CPU oracle's pass until it has run this long (at least once)")
+    ap.add_argument("--fp32-products", choices=["on", "off"], default="on",
+                    help="also time the iteration and the SF launches with the fp32 matrix-core products")
     ap.add_argument("--calibration-copy-mib", type=int, default=512,
                     help="size of one plain device copy run before the timed region, whose "
                          "FETCH_SIZE/WRITE_SIZE counters calibrate the kernels' HBM traffic")
@@ -255,6 +259,19 @@ def _cpu_baseline(wl, host, fraction, min_seconds):
     }
 
 
+def _sf_peak(arith):
+    """The SF kernel's matrix-core ceiling in contraction flops (2MNK): the
+    fp32 peak, or the bf16 peak over the six products the split arithmetic
+    forms per fp32 multiply-add."""
+    from paper_1706_03292_amd import api
+    if arith == api.SF_FP32:
+        return PEAK_FP32_MFMA_TFLOPS, "fp32 MFMA (v_mfma_f32_32x32x2_f32)"
+    return (PEAK_BF16_MFMA_TFLOPS / SPLIT_PRODUCTS,
+            "split-bf16 MFMA (v_mfma_f32_32x32x16_bf16): each fp32 operand split exactly into three bf16 parts, "
+            f"six part products per fp32 multiply-add, fp32 accumulation; peak = {PEAK_BF16_MFMA_TFLOPS:.0f} "
+            f"bf16 TFLOP/s / {SPLIT_PRODUCTS}")
+
+
 def _sf_phase(wl, host, devt, schemes, launch_ms, time_fn, stream):
     """The SF-reconstruction kernel: its launch time inside the iteration (the
     grouped launch of the FC layers, or per-layer launches; launch records)
@@ -290,16 +307,18 @@ def _sf_phase(wl, host, devt, schemes, launch_ms, time_fn, stream):
     tflops = flops / in_ms / 1e9 if in_ms else None
     how = (f"the grouped launch of the {len(idx)} SFB layers inside the iteration ({grouped_ms:.4f} ms)"
            if grouped_ms else f"the summed average durations of their launches inside the iteration ({in_ms:.4f} ms)")
+    peak, arith_name = _sf_peak(api.sf_arithmetic())
     return {
         "in_iteration_ms": in_ms,
         "layers": layers,
         "layers_momentum": layers_mom,
         "roofline": {"bound": "mfma",
-                     "kernel": "sf_apply (fp32 MFMA; " + ("one grouped launch for the FC layers)" if grouped_ms
-                                                          else "one launch per FC layer)"),
+                     "kernel": f"sf_apply ({arith_name}; " + ("one grouped launch for the FC layers)" if grouped_ms
+                                                              else "one launch per FC layer)"),
                      "achieved": round(tflops, 2) if tflops else None,
-                     "peak": PEAK_FP32_MFMA_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tflops / PEAK_FP32_MFMA_TFLOPS, 4) if tflops else None,
+                     "peak": round(peak, 1), "unit": "TFLOP/s",
+                     "frac": round(tflops / peak, 4) if tflops else None,
+                     "fp32_peak_frac": round(tflops / PEAK_FP32_MFMA_TFLOPS, 4) if tflops else None,
                      "traffic": _stored_traffic("sf_apply", "sf_apply.hip") if wl.config == 5 else None,
                      "work": f"2*M*N*K flops of the {len(idx)} SFB layers of one step ({flops / 1e9:.1f} GFLOP) / "
                              + how},
@@ -449,6 +468,43 @@ def _kv_phase(wl, devt, time_fn, stream, ksteps):
                 "in one pass (each of its PS update values read and written once), queued the same way"}
 
 
+def _fp32_products_phase(wl, host, devt, schemes, it, stream, time_fn, args):
+    """The same iteration and grouped SF launch with the fp32 matrix-core
+    products (poseidon_sf_set_arithmetic(POSEIDON_SF_FP32)), for comparison;
+    the default split arithmetic is restored afterwards."""
+    from paper_1706_03292_amd import api
+    import torch
+    idx = [i for i, s_ in enumerate(schemes) if s_ == api.SFB]
+    api.sf_set_arithmetic(api.SF_FP32)
+    try:
+        t_w = time.perf_counter()
+        n = 0
+        while n < args.warmup or time.perf_counter() - t_w < args.min_warmup_s:
+            it(stream)
+            n += 1
+            if n % 16 == 0:
+                torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            it(stream)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3 / args.steps
+        layers = [(devt[i]["W"].clone(), devt[i]["U"], devt[i]["V"]) for i in idx]
+        flops = sum(_sf_flops(host[i]["spec"], wl.K) for i in idx)
+        g_ms = time_fn(lambda: api.sf_apply_batch(layers, wl.lr, stream=stream), queued=True) if layers else None
+        del layers
+    finally:
+        api.sf_set_arithmetic(api.SF_BF16X6)
+    out = {"what": "the same iteration with poseidon_sf_set_arithmetic(POSEIDON_SF_FP32): fp32 matrix-core "
+                   "products instead of the split-bf16 ones",
+           "ms_per_step": round(ms, 4), "steps": args.steps}
+    if g_ms:
+        out.update({"sf_grouped_alone_ms": round(g_ms, 4), "sf_grouped_alone_tflops": round(flops / g_ms / 1e9, 2),
+                    "frac_of_fp32_peak": round(flops / g_ms / 1e9 / PEAK_FP32_MFMA_TFLOPS, 4)})
+    return out
+
+
 def main():
     args = _parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -589,13 +645,13 @@ def main():
         "warmup_steps_run": warm_steps,
         "warmup_note": f"untimed steps run before the timed region: at least --warmup {args.warmup}, continued "
                        f"until {args.min_warmup_s} s had passed ({warm_steps} steps); the steps of a fresh process "
-                       "take 25-50 iterations to reach their steady duration (2.9 ms falling to ~1.8 ms), "
-                       "a ramp that a longer pre-warm of other kernels does not remove",
+                       "take 25-50 iterations to reach their steady duration (the first ones up to ~1.7 times "
+                       "longer), a ramp that a longer pre-warm of other kernels does not remove",
         "ms_per_step": round(wall_ms, 4),
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "f32" if api.sf_arithmetic() == api.SF_FP32 else "f32 (SF products: bf16x6 split)",
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: {sum(s.numel for s in wl.specs)} params, "
                                f"{len(wl.specs)} tensors, K={wl.K}, lr={wl.lr}, momentum={wl.momentum}",
@@ -623,6 +679,9 @@ def main():
         print("[bench] WFBP phase (synthetic backward)", file=sys.stderr, flush=True)
         result["wfbp"] = _wfbp_phase(wl, devt, it, pool, d, args.wfbp_steps)
         print(f"[bench] WFBP: {result['wfbp']}", file=sys.stderr, flush=True)
+    if args.fp32_products == "on" and sf:
+        result["sf_fp32_products"] = _fp32_products_phase(wl, host, devt, schemes, it, stream, _time, args)
+        print(f"[bench] fp32 products: {result['sf_fp32_products']}", file=sys.stderr, flush=True)
     if args.cpu_baseline == "on":
         print("[bench] timing the CPU oracle on a sample", file=sys.stderr, flush=True)
         result["cpu_baseline"] = _cpu_baseline(wl, host, args.cpu_fraction, args.cpu_seconds)

@@ -64,6 +64,10 @@ extern "C" {
 #define POSEIDON_WFBP_SFB_LAST 1   /* PS applies on their own events, SFB rebuilds after every event */
 #define POSEIDON_WFBP_EACH     2   /* every update on its own ready event (Alg. 2) */
 
+/* Arithmetic of the SF reconstruction's contraction (poseidon_sf_set_arithmetic). */
+#define POSEIDON_SF_BF16X6 0   /* split-bf16 products, fp32 accumulation (default) */
+#define POSEIDON_SF_FP32   1   /* fp32 matrix-core products, fp32 accumulation */
+
 /*
  * Sufficient-factor reconstruction fused with the SGD step (Sec. 2.1
  * "Sufficient Factor Broadcasting"; Eq. 2; Eq. 1), the work of a syncer's
@@ -78,7 +82,12 @@ extern "C" {
  *     workers of per-worker batch B, this node's own included; the rows of
  *     worker p are contiguous.
  * The sum is accumulated in fp32 on the matrix cores and W is read and written
- * exactly once.  lr is applied as given (no 1/(P*B) scaling).
+ * exactly once.  lr is applied as given (no 1/(P*B) scaling).  The products
+ * are formed as poseidon_sf_set_arithmetic last chose: by default each fp32
+ * operand is split exactly into three bf16 parts and six of their nine
+ * products are accumulated (fp32-grade: the three left out are below 2^-23
+ * of the product); POSEIDON_SF_FP32 uses the fp32 matrix-core product.
+ * Operands whose byte offsets exceed 32 bits always take the fp32 product.
  * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (negative size, NULL pointer
  * with nonzero size, W overlapping U or V) or POSEIDON_ERR_HIP.
  */
@@ -104,6 +113,23 @@ int poseidon_sf_apply(float* W, const float* U, const float* V,
 int poseidon_sf_apply_momentum(float* W, float* buf, const float* U, const float* V,
                                int64_t M, int64_t N, int64_t K, float lr, float momentum,
                                hipStream_t stream);
+
+/*
+ * Chooses how every SF reconstruction enqueued after the call, from any
+ * thread, forms its products (the sums, the update and the layouts are the
+ * same): POSEIDON_SF_BF16X6 (the default) splits each fp32 operand x exactly
+ * into bf16 parts h + m + l (h and m rounded to nearest, l the remainder,
+ * which has at most 8 significant bits) and accumulates the six products
+ * h*h, h*m, m*h, h*l, l*h and m*m in fp32 on the bf16 matrix cores (the six-
+ * product split of Henry, Tang and Heinecke, ARITH 2019); POSEIDON_SF_FP32
+ * accumulates the fp32 matrix-core products.  The choice is process-wide
+ * and does not change which scheme Alg. 1 picks.  Returns POSEIDON_OK or
+ * POSEIDON_ERR_INVALID_ARG (an unknown value; the setting is unchanged).
+ */
+int poseidon_sf_set_arithmetic(int32_t arithmetic);
+
+/* The current choice of poseidon_sf_set_arithmetic. */
+int32_t poseidon_sf_arithmetic(void);
 
 /* One fully-connected layer of a grouped SF reconstruction. */
 typedef struct poseidon_sf_tensor {
@@ -550,7 +576,7 @@ int poseidon_pool_launch_times(poseidon_stream_pool* pool, poseidon_launch_recor
                                int32_t capacity, int32_t* count);
 
 /* Library version, for the binding's load check: returns POSEIDON_ABI_VERSION. */
-#define POSEIDON_ABI_VERSION 2
+#define POSEIDON_ABI_VERSION 3
 int poseidon_abi_version(void);
 
 #ifdef __cplusplus

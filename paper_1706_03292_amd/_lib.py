@@ -9,7 +9,7 @@ import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libposeidon.so")
-ABI_VERSION = 2
+ABI_VERSION = 3
 
 OK = 0
 ERR_INVALID_ARG = -1
@@ -23,6 +23,8 @@ KIND_OTHER = 1
 WFBP_ALL_LAST = 0
 WFBP_SFB_LAST = 1
 WFBP_EACH = 2
+SF_BF16X6 = 0
+SF_FP32 = 1
 
 EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply_batch",
            "poseidon_ps_apply", "poseidon_ps_apply_batch",
@@ -33,7 +35,8 @@ EXPORTS = ("poseidon_sf_apply", "poseidon_sf_apply_momentum", "poseidon_sf_apply
            "poseidon_pool_launch_times", "poseidon_abi_version",
            "poseidon_kv_layout", "poseidon_kv_create", "poseidon_kv_destroy", "poseidon_kv_begin",
            "poseidon_kv_receive", "poseidon_kv_pair_count", "poseidon_kv_receive_message",
-           "poseidon_kv_message_size", "poseidon_kv_pack")
+           "poseidon_kv_message_size", "poseidon_kv_pack", "poseidon_sf_set_arithmetic",
+           "poseidon_sf_arithmetic")
 
 
 class PoseidonTensor(ctypes.Structure):
@@ -105,6 +108,8 @@ def lib() -> ctypes.CDLL:
     L.poseidon_pool_launch_times.argtypes = [vp, ctypes.POINTER(PoseidonLaunchRecord), i32,
                                              ctypes.POINTER(i32)]
     L.poseidon_abi_version.argtypes = []
+    L.poseidon_sf_set_arithmetic.argtypes = [i32]
+    L.poseidon_sf_arithmetic.argtypes = []
     L.poseidon_kv_layout.argtypes = [ctypes.POINTER(i64), i32, i64, i32, ctypes.POINTER(PoseidonKvPair), i32,
                                      ctypes.POINTER(i32)]
     L.poseidon_kv_create.argtypes = [ctypes.POINTER(PoseidonKvTensor), i32, i64, i32, i32, f32, f32,

@@ -14,7 +14,7 @@ import torch
 
 from . import _lib as L
 from ._lib import (ADAM, ERR_HIP, ERR_INVALID_ARG, ERR_PAYLOAD, KIND_FC, KIND_OTHER, PS, SFB,  # noqa: F401
-                   WFBP_ALL_LAST, WFBP_EACH, WFBP_SFB_LAST)
+                   SF_BF16X6, SF_FP32, WFBP_ALL_LAST, WFBP_EACH, WFBP_SFB_LAST)
 
 
 class PoseidonError(RuntimeError):
@@ -127,6 +127,18 @@ def sf_apply_momentum(W: torch.Tensor, buf: torch.Tensor, U: torch.Tensor, V: to
         _check("poseidon_sf_apply_momentum", L.lib().poseidon_sf_apply_momentum(
             W.data_ptr(), buf.data_ptr(), U.data_ptr(), V.data_ptr(), M, N, K, float(lr), float(momentum),
             _stream_handle(stream, W.device)))
+
+
+def sf_set_arithmetic(arithmetic: int) -> None:
+    """How later SF reconstructions form their products, process-wide
+    (poseidon_sf_set_arithmetic): SF_BF16X6 (the default: six products of
+    exact bf16 parts, fp32 accumulation) or SF_FP32 (fp32 products)."""
+    _check("poseidon_sf_set_arithmetic", L.lib().poseidon_sf_set_arithmetic(int(arithmetic)))
+
+
+def sf_arithmetic() -> int:
+    """The current choice of sf_set_arithmetic (poseidon_sf_arithmetic)."""
+    return int(L.lib().poseidon_sf_arithmetic())
 
 
 def sf_apply_batch(layers: list, lr: float, stream=None) -> None:

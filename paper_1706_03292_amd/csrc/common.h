@@ -60,12 +60,27 @@ inline bool writes_collide(std::vector<Span> writes, const std::vector<Span>& re
 // Number of compute units of the current device (cached per device).
 int device_cu_count();
 
+// The SF contraction's arithmetic (POSEIDON_SF_BF16X6 or POSEIDON_SF_FP32),
+// process-wide.
+int32_t sf_arithmetic();
+void set_sf_arithmetic(int32_t arithmetic);
+
+// The time the iteration's stream policy assumes for one layer's rebuild,
+// from the rates measured alone on one MI355X (fp32-equivalent contraction
+// flops): split-bf16 products on 256 x 128 tiles 186-194 TFLOP/s (the
+// grouped VGG19-22K FC launch), on smaller tiles about 140 (the 4096 x 4096
+// layer at K = 256: 142); fp32 products 124-138.
+constexpr double SF_SPLIT_BIG_FLOPS_PER_S = 1.85e14;
+constexpr double SF_SPLIT_FLOPS_PER_S = 1.4e14;
+constexpr double SF_FP32_FLOPS_PER_S = 1.3e14;
+double sf_seconds(int64_t M, int64_t N, int64_t K);
+
 // Internal launchers (arguments already validated; nonzero sizes).  Given
 // spread_s > 0, an SF launch runs on as few workgroups as would walk its
 // tiles in about spread_s seconds, instead of one workgroup per tile.  Given
-// `room`, the SF tiles leave each SIMD the registers of one wave of the lean
-// PS kernel beside four of theirs, and a PS launch given `beside_sf` uses
-// that kernel (aligned tensors), so that the two run on the same CUs.
+// `room`, the SF tiles leave each SIMD the registers of a wave of the lean PS
+// kernel beside theirs, and a PS launch given `beside_sf` uses that kernel
+// (aligned tensors), so that the two run on the same CUs.
 hipError_t launch_sf_apply(float* W, const float* U, const float* V,
                            int64_t M, int64_t N, int64_t K, float lr, hipStream_t stream, double spread_s = 0.0,
                            bool room = false);

@@ -106,6 +106,16 @@ extern "C" int poseidon_sf_apply(float* W, const float* U, const float* V,
                : POSEIDON_ERR_HIP;
 }
 
+extern "C" int poseidon_sf_set_arithmetic(int32_t arithmetic)
+{
+    if (arithmetic != POSEIDON_SF_BF16X6 && arithmetic != POSEIDON_SF_FP32)
+        return POSEIDON_ERR_INVALID_ARG;
+    poseidon::set_sf_arithmetic(arithmetic);
+    return POSEIDON_OK;
+}
+
+extern "C" int32_t poseidon_sf_arithmetic(void) { return poseidon::sf_arithmetic(); }
+
 extern "C" int poseidon_sf_apply_batch(const poseidon_sf_tensor* layers, int32_t count, int64_t K, float lr,
                                        hipStream_t stream)
 {

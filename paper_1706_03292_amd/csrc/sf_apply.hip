@@ -70,6 +70,30 @@ struct SfTile {
     static_assert(BK % 2 == 0, "MFMA depth is 2");
 };
 
+// Waves per SIMD a tile shape is compiled for: 4 (at most 128 VGPRs a wave)
+// for wave sub-blocks up to 64 x 64, else 2 (256 VGPRs: the accumulators of a
+// 128 x 64 sub-block alone take 128).
+template <int WM, int WN>
+struct SfOcc {
+    static constexpr int W = WM * WN > 64 * 64 ? 2 : 4;
+};
+
+// Tile shapes (workgroup BM x BN, K-slices of BK, wave sub-block WM x WN).
+// Split-bf16 layers with at least four 256 x 128 tiles per CU take that tile
+// (two waves per SIMD, each on a 128 x 64 sub-block: 48 MFMAs per 48 split
+// operand values instead of 24 per 32); otherwise, and for fp32 MFMA layers,
+// 128 x 128 tiles when there are at least two per CU, else 64 x 64.
+struct Big {
+    static constexpr int BM = 256, BN = 128, BK = 16, WM = 128, WN = 64;
+};
+struct Mid {
+    static constexpr int BM = 128, BN = 128, BK = 16, WM = 64, WN = 64;
+};
+struct Small {
+    static constexpr int BM = 64, BN = 64, BK = 32, WM = 32, WN = 32;
+};
+constexpr int64_t BIG_TILES_PER_CU = 4, MID_TILES_PER_CU = 2;
+
 // Workgroup id -> (tile row, tile column): contiguous runs per XCD, GM tile
 // rows at a time inside a run.
 template <int GM>
@@ -306,6 +330,86 @@ struct LdsStage {
     }
 };
 
+// ---------------------------------------------------------------------------
+// Split-bf16 products (the default arithmetic).  An fp32 value x is the exact
+// sum of three bf16 values: h = bf16(x) and m = bf16(x - h), each rounded to
+// nearest, and l = x - h - m, which has at most 8 significant bits (bf16
+// keeps 8 of fp32's 24 and the same exponent range).  A product x*y is the
+// sum of the nine products of the parts; the six kept here (h*h, h*m, m*h,
+// h*l, l*h, m*m) are each exact in fp32 and formed on the bf16 matrix cores
+// with fp32 accumulation.  The three dropped (m*l, l*m, l*l) are below 2^-23
+// of |x*y| together and of either sign.  This is the six-product split of
+// Henry, Tang and Heinecke, "Leveraging the bfloat16 Artificial Intelligence
+// Datatype For Higher-Precision Computations" (ARITH 2019).
+// ---------------------------------------------------------------------------
+typedef __bf16 bf8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf2 __attribute__((ext_vector_type(2)));
+typedef float fl2 __attribute__((ext_vector_type(2)));
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+struct Split3 {
+    bf8 h, m, l;
+};
+
+// Two values rounded to bf16 and packed (the first in the low half).
+__device__ __forceinline__ unsigned pack_bf16(float a, float b)
+{
+    return __builtin_bit_cast(unsigned, __builtin_convertvector((fl2){a, b}, bf2));
+}
+
+// The top halves of two fp32 values packed (a's in the low half): exact for
+// values of at most 8 significant bits.
+__device__ __forceinline__ unsigned pack_top(float a, float b)
+{
+    return __builtin_amdgcn_perm(__builtin_bit_cast(unsigned, b), __builtin_bit_cast(unsigned, a), 0x07060302u);
+}
+
+// x minus half HI of the packed pair p (a bf16's fp32 value is its bits in
+// the top half of the word).
+template <int HI>
+__device__ __forceinline__ float minus_half(float x, unsigned p)
+{
+    return x - __builtin_bit_cast(float, HI ? (p & 0xffff0000u) : (p << 16));
+}
+
+// The parts of x[0..7], two values per conversion.
+__device__ __forceinline__ Split3 split3(const float (&x)[8])
+{
+    u32x4 h, m, l;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const unsigned hp = pack_bf16(x[2 * q], x[2 * q + 1]);
+        const float r0 = minus_half<0>(x[2 * q], hp);
+        const float r1 = minus_half<1>(x[2 * q + 1], hp);
+        const unsigned mp = pack_bf16(r0, r1);
+        h[q] = hp;
+        m[q] = mp;
+        l[q] = pack_top(minus_half<0>(r0, mp), minus_half<1>(r1, mp));
+    }
+    return {__builtin_bit_cast(bf8, h), __builtin_bit_cast(bf8, m), __builtin_bit_cast(bf8, l)};
+}
+
+// acc[j] += A * B_j over 16 values of K: the six products, the small ones
+// first, each over every block of the row before the next.
+template <int TN>
+__device__ __forceinline__ void split_products(f16v (&acc)[TN], const Split3& a, const Split3 (&b)[TN])
+{
+    auto each = [&](auto pick_a, auto pick_b) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+            acc[j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pick_a(a), pick_b(b[j]), acc[j], 0, 0, 0);
+    };
+    auto H = [](const Split3& x) { return x.h; };
+    auto Mi = [](const Split3& x) { return x.m; };
+    auto L = [](const Split3& x) { return x.l; };
+    each(Mi, Mi);
+    each(H, L);
+    each(L, H);
+    each(H, Mi);
+    each(Mi, H);
+    each(H, H);
+}
+
 // Chunk (16 bytes) c of slice row k is stored at chunk position c ^ swz(k).
 __device__ __forceinline__ constexpr int swz(int k) { return (k & 1) << 3; }
 
@@ -314,7 +418,7 @@ __device__ __forceinline__ constexpr int swz(int k) { return (k & 1) << 3; }
 // loads of the slice visible.
 __device__ __forceinline__ void wait_loads() { __builtin_amdgcn_s_waitcnt(0x0F70); }   // vmcnt(0)
 
-template <int BM, int BN, int BK, int WM, int WN>
+template <int BM, int BN, int BK, int WM, int WN, bool SPLIT>
 struct Direct {
     using T = SfTile<BM, BN, BK, WM, WN>;
     static constexpr int NT = T::THREADS;
@@ -354,10 +458,57 @@ struct Direct {
         issue_panel<BN>(vr, B<S>(), ldv, kt * BK, tid);
     }
 
-    // One BK-deep step of the contraction out of LDS stage S: the MFMA
-    // operands of step kk+2 are read while the matrix cores work on step kk.
+    // One BK-deep step of the contraction out of LDS stage S.
     template <int S>
     static __device__ __forceinline__ void mma(f16v (&acc)[T::TM][T::TN], int wm, int wn, int lane)
+    {
+        if constexpr (SPLIT)
+            mma_split<S>(acc, wm, wn, lane);
+        else
+            mma_f32<S>(acc, wm, wn, lane);
+    }
+
+    // Split-bf16 step: 16 values of K per MFMA.  Lane l of an operand holds
+    // slot q = 0..7 of its row (column) as K index 2q + l/32, the LDS reads
+    // of the fp32 step below, eight at a time; A and B use the same slots.
+    template <int S>
+    static __device__ __forceinline__ void mma_split(f16v (&acc)[T::TM][T::TN], int wm, int wn, int lane)
+    {
+        static_assert(BK % 16 == 0, "bf16 MFMA depth is 16");
+        const float* a_s = A<S>();
+        const float* b_s = B<S>();
+        const int lrow = lane >> 5, lcol = lane & 31;
+        auto at = [&](const float* s, int ld, int kk, int x) {
+            const int k = kk + lrow;
+            return s[k * ld + ((((x >> 2) ^ swz(k)) << 2) | (x & 3))];
+        };
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 16) {
+            Split3 b[T::TN];
+#pragma unroll
+            for (int j = 0; j < T::TN; ++j) {
+                float x[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q)
+                    x[q] = at(b_s, BN, kk + 2 * q, wn + 32 * j + lcol);
+                b[j] = split3(x);
+            }
+            // One A block row at a time (its parts and B's stay in registers).
+#pragma unroll
+            for (int i = 0; i < T::TM; ++i) {
+                float x[8];
+#pragma unroll
+                for (int q = 0; q < 8; ++q)
+                    x[q] = at(a_s, BM, kk + 2 * q, wm + 32 * i + lcol);
+                split_products<T::TN>(acc[i], split3(x), b);
+            }
+        }
+    }
+
+    // fp32 step: the MFMA operands of step kk+2 are read while the matrix
+    // cores work on step kk.
+    template <int S>
+    static __device__ __forceinline__ void mma_f32(f16v (&acc)[T::TM][T::TN], int wm, int wn, int lane)
     {
         const float* a_s = A<S>();
         const float* b_s = B<S>();
@@ -416,12 +567,12 @@ struct Direct {
 // lives in stage (nkt-1-kt) & 1, so the last slice is always in stage 0 and
 // the loop body and the final step are each emitted once.  An interior tile
 // loads PRE values of W ahead of the last K step.
-template <int BM, int BN, int BK, int WM, int WN, bool MOM, int PRE = W_PRE>
+template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, bool MOM, int PRE = W_PRE>
 __device__ __forceinline__ void sf_tile_direct(float* __restrict__ W, const float* __restrict__ U,
                                                const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
                                                float lr, int tm, int tn, float* __restrict__ buf, float mu)
 {
-    using D = Direct<BM, BN, BK, WM, WN>;
+    using D = Direct<BM, BN, BK, WM, WN, SPLIT>;
     using T = SfTile<BM, BN, BK, WM, WN>;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -617,15 +768,15 @@ __device__ __forceinline__ void sf_tile_staged(float* As, float* Bs, float* __re
 // ---------------------------------------------------------------------------
 // Kernels, compiled for at least 4 waves per SIMD (at most 128 VGPRs a wave).
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int BK, int WM, int WN, bool MOM, int PRE = W_PRE>
+template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, bool MOM, int PRE = W_PRE>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_kernel(
+__attribute__((amdgpu_waves_per_eu(SfOcc<WM, WN>::W, SfOcc<WM, WN>::W))) void sf_apply_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
     float lr, int tiles_m, int tiles_n, float* __restrict__ buf, float mu)
 {
     int tm, tn;
     tile_coords<8>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
-    sf_tile_direct<BM, BN, BK, WM, WN, MOM, PRE>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
+    sf_tile_direct<BM, BN, BK, WM, WN, SPLIT, MOM, PRE>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
 }
 
 // The spread launch: fewer workgroups than tiles (a multiple of 8, so that
@@ -635,7 +786,7 @@ __attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_kernel(
 // 128), and a spread launch has few workgroups resident, so it is compiled
 // for 2 waves per SIMD (two workgroups per CU).  The barrier keeps a wave's first loads of the next
 // tile out of the LDS stage the others may still read.
-template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, bool MOM>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(2, 2))) void sf_apply_walk_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
@@ -647,13 +798,13 @@ __attribute__((amdgpu_waves_per_eu(2, 2))) void sf_apply_walk_kernel(
             __syncthreads();
         int tm, tn;
         tile_coords<8>(t, tiles, tiles_m, tiles_n, tm, tn);
-        sf_tile_direct<BM, BN, BK, WM, WN, MOM>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
+        sf_tile_direct<BM, BN, BK, WM, WN, SPLIT, MOM>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
     }
 }
 
 template <int BM, int BN, int BK, int WM, int WN, bool WIDE, bool MOM>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_staged_kernel(
+__attribute__((amdgpu_waves_per_eu(SfOcc<WM, WN>::W, SfOcc<WM, WN>::W))) void sf_apply_staged_kernel(
     float* __restrict__ W, const float* __restrict__ U, const float* __restrict__ V, int64_t M, int64_t N, int64_t K,
     float lr, int tiles_m, int tiles_n, float* __restrict__ buf, float mu)
 {
@@ -692,7 +843,7 @@ struct SfBatchArgs {
 
 // Tile t of the combined list (layer by layer; inside a layer tile rows
 // walked 8 at a time).
-template <int BM, int BN, int BK, int WM, int WN, int PRE = W_PRE>
+template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, int PRE = W_PRE>
 __device__ __forceinline__ void batch_tile(const SfBatchArgs& args, int t, int64_t K, float lr)
 {
     int l = 0;
@@ -707,18 +858,18 @@ __device__ __forceinline__ void batch_tile(const SfBatchArgs& args, int t, int64
     const int rows = (tiles_m - first_m) < G ? (tiles_m - first_m) : G;
     const int in = local - g * per_group;
     const SfBatchItem& it = args.item[l];
-    sf_tile_direct<BM, BN, BK, WM, WN, false, PRE>(it.W, it.U, it.V, it.M, it.N, K, lr, first_m + in % rows,
+    sf_tile_direct<BM, BN, BK, WM, WN, SPLIT, false, PRE>(it.W, it.U, it.V, it.M, it.N, K, lr, first_m + in % rows,
                                                    in / rows, nullptr, 0.f);
 }
 
-template <int BM, int BN, int BK, int WM, int WN, int PRE = W_PRE>
+template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, int PRE = W_PRE>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
-__attribute__((amdgpu_waves_per_eu(4, 4))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K, float lr)
+__attribute__((amdgpu_waves_per_eu(SfOcc<WM, WN>::W, SfOcc<WM, WN>::W))) void sf_apply_batch_kernel(const SfBatchArgs args, int64_t K, float lr)
 {
     const int tiles = args.total_tiles;
     const int q = tiles / NUM_XCD, r = tiles % NUM_XCD;
     const int x = blockIdx.x % NUM_XCD, j = blockIdx.x / NUM_XCD;
-    batch_tile<BM, BN, BK, WM, WN, PRE>(args, x * q + (x < r ? x : r) + j, K, lr);
+    batch_tile<BM, BN, BK, WM, WN, SPLIT, PRE>(args, x * q + (x < r ? x : r) + j, K, lr);
 }
 
 // True when the LDS-direct tile's 32-bit buffer offsets cover the layer: the
@@ -732,14 +883,14 @@ bool direct_fits(int64_t M, int64_t N, int64_t K, int BM, int BN, int BK)
 
 // Workgroups of the spread kernel that one CU holds at once (its register
 // and LDS needs; cached per instantiation).
-template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, bool MOM>
 int64_t walk_groups_per_cu()
 {
     static std::atomic<int> cached{0};
     int n = cached.load(std::memory_order_relaxed);
     if (n > 0)
         return n;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, sf_apply_walk_kernel<BM, BN, BK, WM, WN, MOM>,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, sf_apply_walk_kernel<BM, BN, BK, WM, WN, SPLIT, MOM>,
                                                      SfTile<BM, BN, BK, WM, WN>::THREADS, 0) != hipSuccess ||
         n < 1)
         n = 1;
@@ -752,10 +903,11 @@ int64_t walk_groups_per_cu()
 // on 64 workgroups in 0.52 ms, 1.29e11 flop/s), a little under.
 constexpr double SPREAD_WG_FLOPS_PER_S = 1.2e11;
 
-template <int BM, int BN, int BK, int WM, int WN, bool MOM>
+template <class TL, bool SPLIT, bool MOM>
 hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
                         float lr, float mu, double spread_s, bool room, hipStream_t stream)
 {
+    constexpr int BM = TL::BM, BN = TL::BN, BK = TL::BK, WM = TL::WM, WN = TL::WN;
     constexpr int NT = SfTile<BM, BN, BK, WM, WN>::THREADS;
     const int64_t tiles_m = (M + BM - 1) / BM;
     const int64_t tiles_n = (N + BN - 1) / BN;
@@ -763,98 +915,95 @@ hipError_t launch_tiles(float* W, float* buf, const float* U, const float* V, in
         return hipErrorInvalidValue;
     const int t = static_cast<int>(tiles_m * tiles_n), tmi = static_cast<int>(tiles_m),
               tni = static_cast<int>(tiles_n);
-    if (direct_fits(M, N, K, BM, BN, BK)) {
+    // The large tile is only chosen where it fits the LDS-direct path, and
+    // never spread: the staged and spread kernels come in the other shapes.
+    constexpr bool LARGE = WM * WN > 64 * 64;
+    if (LARGE || direct_fits(M, N, K, BM, BN, BK)) {
         // Spread: as few workgroups (a multiple of 8) as walk the tiles
         // within spread_s at SPREAD_WG_FLOPS_PER_S each -- provided the chip
         // holds them all at once (otherwise the later ones would wait for
         // the first to finish all their tiles).
         int grid = t;
-        if (spread_s > 0.0) {
-            const double per = spread_s * SPREAD_WG_FLOPS_PER_S / (2.0 * BM * BN * static_cast<double>(K));
-            if (per >= 2.0) {
-                const int64_t p = per < t ? static_cast<int64_t>(per) : t;
-                const int64_t g = ((t + p - 1) / p + NUM_XCD - 1) / NUM_XCD * NUM_XCD;
-                const int64_t resident = walk_groups_per_cu<BM, BN, BK, WM, WN, MOM>() * device_cu_count();
-                if (g < t && g <= resident)
-                    grid = static_cast<int>(g);
+        if constexpr (!LARGE) {
+            if (spread_s > 0.0) {
+                const double per = spread_s * SPREAD_WG_FLOPS_PER_S / (2.0 * BM * BN * static_cast<double>(K));
+                if (per >= 2.0) {
+                    const int64_t p = per < t ? static_cast<int64_t>(per) : t;
+                    const int64_t g = ((t + p - 1) / p + NUM_XCD - 1) / NUM_XCD * NUM_XCD;
+                    const int64_t resident =
+                        walk_groups_per_cu<BM, BN, BK, WM, WN, SPLIT, MOM>() * device_cu_count();
+                    if (g < t && g <= resident)
+                        grid = static_cast<int>(g);
+                }
             }
         }
-        // (The momentum epilogue loads no W ahead anyway: 114 VGPRs.)
+        // (The momentum epilogue loads no W ahead anyway.)
         constexpr bool can_drop_pre = !MOM;
-        if (grid < t)
-            sf_apply_walk_kernel<BM, BN, BK, WM, WN, MOM><<<grid, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
-                                                                                  buf, mu);
-        else if (room && can_drop_pre)
-            sf_apply_kernel<BM, BN, BK, WM, WN, MOM, can_drop_pre ? 0 : W_PRE><<<t, NT, 0, stream>>>(
+        if constexpr (!LARGE) {
+            if (grid < t) {
+                sf_apply_walk_kernel<BM, BN, BK, WM, WN, SPLIT, MOM><<<grid, NT, 0, stream>>>(W, U, V, M, N, K, lr,
+                                                                                             tmi, tni, buf, mu);
+                return hipGetLastError();
+            }
+        }
+        if (room && can_drop_pre)
+            sf_apply_kernel<BM, BN, BK, WM, WN, SPLIT, MOM, can_drop_pre ? 0 : W_PRE><<<t, NT, 0, stream>>>(
                 W, U, V, M, N, K, lr, tmi, tni, buf, mu);
         else
-            sf_apply_kernel<BM, BN, BK, WM, WN, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni, buf, mu);
+            sf_apply_kernel<BM, BN, BK, WM, WN, SPLIT, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
+                                                                                 buf, mu);
     }
-    else if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
-        sf_apply_staged_kernel<BM, BN, BK, WM, WN, false, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
-                                                                                     buf, mu);
-    else
-        sf_apply_staged_kernel<BM, BN, BK, WM, WN, true, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi, tni,
-                                                                                    buf, mu);
+    else if constexpr (!LARGE) {
+        if ((static_cast<int64_t>(BM) * N + BN) * 4 < 0x7fffffffLL)
+            sf_apply_staged_kernel<BM, BN, BK, WM, WN, false, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi,
+                                                                                         tni, buf, mu);
+        else
+            sf_apply_staged_kernel<BM, BN, BK, WM, WN, true, MOM><<<t, NT, 0, stream>>>(W, U, V, M, N, K, lr, tmi,
+                                                                                        tni, buf, mu);
+    }
     return hipGetLastError();
 }
 
-// Tile choice: 128 x 128 workgroup tiles (64 x 64 per wave, K-slices of 16)
-// when the layer has at least two such tiles per CU; otherwise 64 x 64 tiles
-// (32 x 32 per wave, K-slices of 32) so that small layers still fill the chip.
-template <bool MOM>
+template <class TL>
+int64_t tiles_of(int64_t M, int64_t N)
+{
+    return ((M + TL::BM - 1) / TL::BM) * ((N + TL::BN - 1) / TL::BN);
+}
+
+// Tile choice (see Big, Mid, Small).  A spread launch takes the 128 x 128 or
+// 64 x 64 tile: its few workgroups walk the tiles at two per CU.
+template <bool SPLIT, bool MOM>
 hipError_t launch_sf(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
                      float mu, double spread_s, bool room, hipStream_t stream)
 {
-    const int64_t big_tiles = ((M + 127) / 128) * ((N + 127) / 128);
-    if (big_tiles >= 2 * static_cast<int64_t>(device_cu_count()))
-        return launch_tiles<128, 128, 16, 64, 64, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
-    return launch_tiles<64, 64, 32, 32, 32, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
-}
-
-}  // namespace
-
-hipError_t launch_sf_apply(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
-                           hipStream_t stream, double spread_s, bool room)
-{
-    return launch_sf<false>(W, nullptr, U, V, M, N, K, lr, 0.f, spread_s, room, stream);
-}
-
-hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N,
-                                    int64_t K, float lr, float mu, hipStream_t stream, double spread_s)
-{
-    return launch_sf<true>(W, buf, U, V, M, N, K, lr, mu, spread_s, false, stream);
-}
-
-// Grouped launch: every layer the LDS-direct 128 x 128 tile covers joins one
-// tile list when the group has at least two tiles per CU; the others, and
-// groups too small to fill the chip, take per-layer launches.
-hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, float lr, hipStream_t stream, bool room)
-{
-    constexpr int BM = 128, BN = 128, BK = 16;
-    std::vector<int32_t> grouped;
-    int64_t tiles = 0;
-    for (int32_t i = 0; i < count; ++i) {
-        if (t[i].M == 0 || t[i].N == 0 || K == 0)
-            continue;
-        const int64_t tl = ((t[i].M + BM - 1) / BM) * ((t[i].N + BN - 1) / BN);
-        if (direct_fits(t[i].M, t[i].N, K, BM, BN, BK) && tiles + tl <= INT32_MAX) {
-            grouped.push_back(i);
-            tiles += tl;
-        } else {
-            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream, 0.0, room);
-            if (e != hipSuccess)
-                return e;
-        }
+    const int64_t cus = device_cu_count();
+    if constexpr (SPLIT) {
+        if (spread_s <= 0.0 && tiles_of<Big>(M, N) >= BIG_TILES_PER_CU * cus &&
+            direct_fits(M, N, K, Big::BM, Big::BN, Big::BK))
+            return launch_tiles<Big, SPLIT, MOM>(W, buf, U, V, M, N, K, lr, mu, 0.0, room, stream);
     }
-    if (tiles < 2 * static_cast<int64_t>(device_cu_count())) {
-        for (int32_t i : grouped) {
-            const hipError_t e = launch_sf_apply(t[i].W, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, stream, 0.0, room);
-            if (e != hipSuccess)
-                return e;
-        }
-        return hipSuccess;
-    }
+    if (tiles_of<Mid>(M, N) >= MID_TILES_PER_CU * cus)
+        return launch_tiles<Mid, SPLIT, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
+    return launch_tiles<Small, SPLIT, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
+}
+
+template <bool MOM>
+hipError_t launch_sf_arith(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N, int64_t K,
+                           float lr, float mu, double spread_s, bool room, hipStream_t stream)
+{
+    if (sf_arithmetic() == POSEIDON_SF_FP32)
+        return launch_sf<false, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
+    return launch_sf<true, MOM>(W, buf, U, V, M, N, K, lr, mu, spread_s, room, stream);
+}
+
+// One grouped launch per SF_BATCH_MAX layers of `grouped` (every one covered
+// by the LDS-direct tile TL).
+template <class TL, bool SPLIT>
+hipError_t launch_grouped(const SfTensor* t, const std::vector<int32_t>& grouped, int64_t K, float lr, bool room,
+                          hipStream_t stream)
+{
+    constexpr int BM = TL::BM, BN = TL::BN, BK = TL::BK;
+    constexpr int NT = SfTile<BM, BN, BK, TL::WM, TL::WN>::THREADS;
     for (size_t g0 = 0; g0 < grouped.size(); g0 += SF_BATCH_MAX) {
         SfBatchArgs a{};
         int32_t first = 0;
@@ -873,9 +1022,9 @@ hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, fl
         }
         a.total_tiles = first;
         if (room)
-            sf_apply_batch_kernel<BM, BN, BK, 64, 64, 0><<<first, 256, 0, stream>>>(a, K, lr);
+            sf_apply_batch_kernel<BM, BN, BK, TL::WM, TL::WN, SPLIT, 0><<<first, NT, 0, stream>>>(a, K, lr);
         else
-            sf_apply_batch_kernel<BM, BN, BK, 64, 64><<<first, 256, 0, stream>>>(a, K, lr);
+            sf_apply_batch_kernel<BM, BN, BK, TL::WM, TL::WN, SPLIT><<<first, NT, 0, stream>>>(a, K, lr);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
@@ -883,5 +1032,86 @@ hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, fl
     return hipSuccess;
 }
 
+// Grouped launch: every layer the LDS-direct tile covers joins one tile list
+// -- of 256 x 128 tiles (split-bf16) when the group has at least four per CU,
+// else of 128 x 128 tiles when it has at least two per CU; the others, and
+// groups too small to fill the chip, take per-layer launches.
+template <bool SPLIT>
+hipError_t launch_batch(const SfTensor* t, int32_t count, int64_t K, float lr, hipStream_t stream, bool room)
+{
+    std::vector<int32_t> grouped;
+    int64_t big = 0, mid = 0;
+    for (int32_t i = 0; i < count; ++i) {
+        if (t[i].M == 0 || t[i].N == 0 || K == 0)
+            continue;
+        // A layer joins the list when the 32-bit offsets of the 256-row
+        // tile cover it (then those of the 128-row tile do too), so that
+        // either shape can run the list; the 128 x 128 tiles are the more
+        // numerous, so their count bounds both.
+        const int64_t tm = tiles_of<Mid>(t[i].M, t[i].N);
+        if (direct_fits(t[i].M, t[i].N, K, Big::BM, Mid::BN, Mid::BK) && mid + tm <= INT32_MAX) {
+            grouped.push_back(i);
+            mid += tm;
+            big += tiles_of<Big>(t[i].M, t[i].N);
+        } else {
+            const hipError_t e =
+                launch_sf<SPLIT, false>(t[i].W, nullptr, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, 0.f, 0.0, room,
+                                        stream);
+            if (e != hipSuccess)
+                return e;
+        }
+    }
+    const int64_t cus = device_cu_count();
+    if constexpr (SPLIT) {
+        if (big >= BIG_TILES_PER_CU * cus)
+            return launch_grouped<Big, SPLIT>(t, grouped, K, lr, room, stream);
+    }
+    if (mid >= MID_TILES_PER_CU * cus)
+        return launch_grouped<Mid, SPLIT>(t, grouped, K, lr, room, stream);
+    for (int32_t i : grouped) {
+        const hipError_t e =
+            launch_sf<SPLIT, false>(t[i].W, nullptr, t[i].U, t[i].V, t[i].M, t[i].N, K, lr, 0.f, 0.0, room, stream);
+        if (e != hipSuccess)
+            return e;
+    }
+    return hipSuccess;
+}
+
+std::atomic<int32_t> g_arithmetic{POSEIDON_SF_BF16X6};
+
+}  // namespace
+
+int32_t sf_arithmetic() { return g_arithmetic.load(std::memory_order_relaxed); }
+
+void set_sf_arithmetic(int32_t a) { g_arithmetic.store(a, std::memory_order_relaxed); }
+
+double sf_seconds(int64_t M, int64_t N, int64_t K)
+{
+    const double flops = 2.0 * static_cast<double>(M) * static_cast<double>(N) * static_cast<double>(K);
+    if (sf_arithmetic() == POSEIDON_SF_FP32)
+        return flops / SF_FP32_FLOPS_PER_S;
+    const bool big = tiles_of<Big>(M, N) >= BIG_TILES_PER_CU * device_cu_count() &&
+                     direct_fits(M, N, K, Big::BM, Big::BN, Big::BK);
+    return flops / (big ? SF_SPLIT_BIG_FLOPS_PER_S : SF_SPLIT_FLOPS_PER_S);
+}
+
+hipError_t launch_sf_apply(float* W, const float* U, const float* V, int64_t M, int64_t N, int64_t K, float lr,
+                           hipStream_t stream, double spread_s, bool room)
+{
+    return launch_sf_arith<false>(W, nullptr, U, V, M, N, K, lr, 0.f, spread_s, room, stream);
+}
+
+hipError_t launch_sf_apply_momentum(float* W, float* buf, const float* U, const float* V, int64_t M, int64_t N,
+                                    int64_t K, float lr, float mu, hipStream_t stream, double spread_s)
+{
+    return launch_sf_arith<true>(W, buf, U, V, M, N, K, lr, mu, spread_s, false, stream);
+}
+
+hipError_t launch_sf_apply_batch(const SfTensor* t, int32_t count, int64_t K, float lr, hipStream_t stream, bool room)
+{
+    if (sf_arithmetic() == POSEIDON_SF_FP32)
+        return launch_batch<false>(t, count, K, lr, stream, room);
+    return launch_batch<true>(t, count, K, lr, stream, room);
+}
 
 }  // namespace poseidon

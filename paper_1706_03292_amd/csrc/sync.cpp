@@ -130,8 +130,8 @@ namespace {
 // launch costs a few microseconds; 2^17 elements at P = 32 move 19 MB, about
 // 4 us of HBM time): the iteration gathers them into a batched pass.  When
 // the PS applies are the iteration's critical path -- the SF rebuilds would
-// take less time than them, judged by the ratio of the two kernels' rates on
-// this GPU (about 130 TFLOP/s over 5 TB/s, 26 flops per PS byte) -- every
+// take less time than them, judged by the kernels' rates on this GPU
+// (sf_seconds; PS_BYTES_PER_S) -- every
 // launch saved shortens the iteration, and tensors below PS_CRITICAL_ELEMS
 // join the pass too (Inception-shaped workload, 95 tensors at P = 32:
 // 0.69 vs 0.77 ms per iteration); when the SF chain is the critical path,
@@ -139,9 +139,7 @@ namespace {
 // (VGG19-22K: neutral to 0.8% slower with the larger threshold).
 constexpr int64_t SMALL_PS_ELEMS = int64_t{1} << 17;
 constexpr int64_t PS_CRITICAL_ELEMS = int64_t{1} << 21;
-constexpr double SF_FLOPS_PER_S = 1.3e14;   // the two kernels' rates on this GPU
-constexpr double PS_BYTES_PER_S = 5.0e12;
-constexpr double SF_FLOPS_PER_PS_BYTE = SF_FLOPS_PER_S / PS_BYTES_PER_S;
+constexpr double PS_BYTES_PER_S = 5.0e12;   // the PS kernel's rate on this GPU (the SF one: sf_seconds)
 // An iteration whose work would take less than this on one stream is bound
 // by launch latency: the second stream's fork and join cost more than the
 // overlap gains (a 1024 x 512 FC layer and a 1M-value PS layer at P = 4:
@@ -152,11 +150,13 @@ constexpr double ONE_STREAM_BELOW_S = 30e-6;
 // ends, the last partial round), and take little from it.  When the two are
 // of comparable size neither has gaps to fill, and the co-running launches
 // only delay each other: the 4096 x 4096 layer rebuilt at K = 256 (one round
-// of tiles, 0.083 ms alone) beside 805 MB of PS applies (0.139 ms alone)
-// took 0.236 ms on two streams against 0.222 ms one after the other.  Below
-// this ratio of the smaller estimated time to the larger the iteration uses
-// two streams (VGG19-22K: 0.19; the Inception-shaped workload: 0.05;
-// that 4096 x 4096 layer through both schemes: 0.41).
+// of tiles, 0.083 ms alone with fp32 products, 0.060 split) beside 805 MB of
+// PS applies (0.139-0.152 ms alone) took 0.236 ms on two streams against
+// 0.222 ms one after the other (split: 0.216 against 0.206).  Below this
+// ratio of the smaller estimated time to the larger the iteration uses two
+// streams (VGG19-22K: 0.27 split, 0.19 fp32, two streams 1.24 ms against
+// 1.37 on one, split; the Inception-shaped workload: 0.05; that 4096 x 4096
+// layer through both schemes: 0.38 split, 0.41 fp32).
 constexpr double CORUN_MAX_RATIO = 0.35;
 // When the PS applies are the longer kind on two streams, every SF launch is
 // spread over few workgroups that walk its tiles, given this fraction of the
@@ -168,13 +168,17 @@ constexpr double CORUN_MAX_RATIO = 0.35;
 // 0.647 ms).
 constexpr double SF_SPREAD_OF_PS = 0.9;
 // When the SF rebuilds are the longer kind on two streams, the rebuilds
-// leave each SIMD room for one wave of the lean PS kernel and the large PS
+// leave each SIMD room for waves of the lean PS kernel and the large PS
 // applies use it, so that they stream memory on the CUs the rebuilds keep
 // busy -- provided the applies still end before the rebuilds: at the lean
-// kernel's rate beside them (1.3 TB/s, one workgroup per CU; VGG19-22K's
-// largest PS tensor, 189 MB in 0.141 ms) they must take at most this
-// fraction of the rebuilds' estimated time.
-constexpr double LEAN_PS_BYTES_PER_S = 1.3e12;
+// kernel's rate beside them they must take at most this fraction of the
+// rebuilds' estimated time.  That rate, one lean workgroup per CU, is set by
+// the waves that fit beside the rebuild's: two per SIMD beside the split-
+// bf16 256 x 128 tiles (two waves of 228 VGPRs; VGG19-22K's largest PS
+// tensors, 189 MB, in 0.06-0.07 ms), one beside the fp32 128 x 128 tiles
+// (four of 120; 0.141 ms).
+constexpr double LEAN_PS_BYTES_PER_S_SPLIT = 2.5e12;
+constexpr double LEAN_PS_BYTES_PER_S_FP32 = 1.3e12;
 constexpr double LEAN_OF_SF = 0.85;
 
 // The iteration of poseidon_sync_iteration (ready == NULL: every update waits
@@ -196,7 +200,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
 
     // Validate everything and fix every scheme before enqueueing anything.
     std::vector<int32_t> plan(static_cast<size_t>(count));
-    double sf_flops = 0.0, ps_bytes = 0.0;
+    double sf_flops = 0.0, t_sf = 0.0, ps_bytes = 0.0;
     for (int32_t t = 0; t < count; ++t) {
         const poseidon_tensor& x = tensors[t];
         if ((x.kind != POSEIDON_KIND_FC && x.kind != POSEIDON_KIND_OTHER) || x.reserved != 0 ||
@@ -216,6 +220,8 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
             rc = x.buf ? check_sf_momentum_args(x.W, x.buf, x.U, x.V, x.M, x.N, K)
                        : check_sf_args(x.W, x.U, x.V, x.M, x.N, K);
             sf_flops += 2.0 * static_cast<double>(n) * static_cast<double>(K);
+            if (rc == POSEIDON_OK && n > 0 && K > 0)
+                t_sf += sf_seconds(x.M, x.N, K);
         } else {
             if (n > 0 && !x.shards)
                 return POSEIDON_ERR_PAYLOAD;
@@ -262,9 +268,9 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
             schemes[t] = plan[static_cast<size_t>(t)];
     // With ready events each large tensor keeps its own launch, so that it
     // starts as soon as its own backward pass has run.
-    const double t_sf = sf_flops / SF_FLOPS_PER_S, t_ps = ps_bytes / PS_BYTES_PER_S;
+    const double t_ps = ps_bytes / PS_BYTES_PER_S;
     const int64_t small_elems =
-        (!per && sf_flops < SF_FLOPS_PER_PS_BYTE * ps_bytes) ? PS_CRITICAL_ELEMS : SMALL_PS_ELEMS;
+        (!per && t_sf < t_ps) ? PS_CRITICAL_ELEMS : SMALL_PS_ELEMS;
     int32_t active = 0;
     int32_t small_ps = 0;
     int32_t plain_sf = 0;     // SFB layers without a momentum buffer
@@ -349,8 +355,9 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // Seconds per flop given to the SF launches when they are spread.
     const double sf_spread = (spread && used == 2) ? SF_SPREAD_OF_PS * t_ps / sf_flops : 0.0;
     // The PS applies beside the rebuilds on the same CUs (see LEAN_OF_SF).
-    const bool room = (!ready || all_last) && used == 2 && t_sf >= t_ps &&
-                      ps_bytes / LEAN_PS_BYTES_PER_S <= LEAN_OF_SF * t_sf;
+    const double lean_rate =
+        sf_arithmetic() == POSEIDON_SF_FP32 ? LEAN_PS_BYTES_PER_S_FP32 : LEAN_PS_BYTES_PER_S_SPLIT;
+    const bool room = (!ready || all_last) && used == 2 && t_sf >= t_ps && ps_bytes / lean_rate <= LEAN_OF_SF * t_sf;
     if (split) {
         const int32_t crit = t_sf >= t_ps ? 0 : 1;
         forked = 1 - crit;

@@ -101,3 +101,19 @@ def test_hybcomm_argument_checks():
     # results that do not fit in int64 are refused, not wrapped
     big = 2 ** 31 - 1
     assert lib.poseidon_hybcomm_cost(big, big, big, big, big, ctypes.byref(a), ctypes.byref(b)) == L.ERR_INVALID_ARG
+
+
+def test_sf_arithmetic_setting():
+    """poseidon_sf_set_arithmetic is host state: the default is the split-bf16
+    products, an unknown value is refused and leaves the setting alone."""
+    lib = L.lib()
+    assert lib.poseidon_sf_arithmetic() == L.SF_BF16X6
+    try:
+        assert lib.poseidon_sf_set_arithmetic(L.SF_FP32) == L.OK
+        assert lib.poseidon_sf_arithmetic() == L.SF_FP32
+        assert lib.poseidon_sf_set_arithmetic(7) == L.ERR_INVALID_ARG
+        assert lib.poseidon_sf_set_arithmetic(-1) == L.ERR_INVALID_ARG
+        assert lib.poseidon_sf_arithmetic() == L.SF_FP32
+    finally:
+        assert lib.poseidon_sf_set_arithmetic(L.SF_BF16X6) == L.OK
+    assert lib.poseidon_sf_arithmetic() == L.SF_BF16X6

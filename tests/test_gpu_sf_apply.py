@@ -1,4 +1,6 @@
 """GPU parity of poseidon_sf_apply (SF reconstruction + SGD) with the oracle."""
+import contextlib
+
 import numpy as np
 import pytest
 import torch
@@ -10,6 +12,19 @@ from paper_1706_03292_amd import api
 from paper_1706_03292_amd import inputs as I
 
 pytestmark = pytest.mark.gpu
+
+# Both arithmetics of the contraction (poseidon_sf_set_arithmetic): the
+# default split-bf16 products and the fp32 matrix-core products.
+ARITHS = pytest.mark.parametrize("arith", [api.SF_BF16X6, api.SF_FP32], ids=["bf16x6", "fp32"])
+
+
+@contextlib.contextmanager
+def arithmetic(a):
+    api.sf_set_arithmetic(a)
+    try:
+        yield
+    finally:
+        api.sf_set_arithmetic(api.SF_BF16X6)
 
 
 def _draw(M, N, K, seed, w_std=0.01, sf_scale=1.0):
@@ -41,30 +56,79 @@ SHAPES = [
 ]
 
 
+@ARITHS
 @pytest.mark.parametrize("M,N,K", SHAPES)
-def test_sf_apply_matches_oracle(M, N, K):
+def test_sf_apply_matches_oracle(M, N, K, arith):
     d = dev()
     W, U, V = _draw(M, N, K, seed=10 * M + N + K)
     ref = oracle.sf_apply(W.numpy(), U.numpy(), V.numpy(), 0.01)
     Wd = W.to(d)
-    log(f"sf_apply M={M} N={N} K={K}")
-    api.sf_apply(Wd, U.to(d), V.to(d), 0.01)
-    torch.cuda.synchronize()
+    log(f"sf_apply M={M} N={N} K={K} arithmetic {arith}")
+    with arithmetic(arith):
+        api.sf_apply(Wd, U.to(d), V.to(d), 0.01)
+        torch.cuda.synchronize()
     assert_close(to_np(Wd), ref, W_TOL, f"W {M}x{N} K={K}")
 
 
+@ARITHS
 @pytest.mark.parametrize("M,N,K", SHAPES)
-def test_sf_raw_gradient_matches_oracle(M, N, K):
+def test_sf_raw_gradient_matches_oracle(M, N, K, arith):
     """W = 0 and lr = -1 make the kernel write the reconstructed gradient
     itself, so it can be held to a much tighter bar than the W update."""
     d = dev()
     _, U, V = _draw(M, N, K, seed=7 * M + N + 3 * K)
     ref = oracle.sf_delta(U.numpy(), V.numpy())
     Wd = torch.zeros(M, N, device=d)
-    log(f"sf_apply raw-delta M={M} N={N} K={K}")
-    api.sf_apply(Wd, U.to(d), V.to(d), -1.0)
-    torch.cuda.synchronize()
+    log(f"sf_apply raw-delta M={M} N={N} K={K} arithmetic {arith}")
+    with arithmetic(arith):
+        api.sf_apply(Wd, U.to(d), V.to(d), -1.0)
+        torch.cuda.synchronize()
     assert_close(to_np(Wd), ref, DELTA_TOL, f"dW {M}x{N} K={K}")
+
+
+def _factors(kind, seed, K, M, N):
+    if kind == "normal":
+        return I.randn(seed, (K, M), 1.0), I.randn(seed + 1, (K, N), 1.0)
+    g = torch.Generator("cpu").manual_seed(seed)
+    if kind == "positive":          # every product positive: no cancellation
+        return torch.rand(K, M, generator=g), torch.rand(K, N, generator=g)
+    # "wide": magnitudes spread over 2^-20 .. 2^20
+    def wide(r, c):
+        e = torch.randint(-20, 21, (r, c), generator=g).float()
+        return torch.randn(r, c, generator=g) * torch.exp2(e)
+    return wide(K, M), wide(K, N)
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 200, 37), (2085, 4125, 40), (8192, 4160, 64), (1000, 2048, 1024)])
+@pytest.mark.parametrize("kind", ["normal", "positive", "wide"])
+def test_sf_split_products_are_fp32_grade(M, N, K, kind):
+    """The split-bf16 products (each fp32 operand split exactly into three
+    bf16 parts, six of the nine part products accumulated in fp32) against
+    the oracle's fp64 gradient, per element in units of 2^-24 of the
+    absolute sum sum_k |U[k][m]| |V[k][n]| -- the scale of fp32 rounding in
+    any order of accumulation: within 2 sqrt(K) + 16 such units, and within
+    twice the fp32 matrix-core product's error plus 4 on the same inputs.
+    (A two-part split, bf16x3, errs by about 2^-16 of each product: hundreds
+    of units.)  Covers all three tile shapes (64 x 64, 128 x 128, 256 x 128),
+    ragged edges and K, and factors without cancellation or over a wide
+    exponent range."""
+    d = dev()
+    U, V = _factors(kind, 5100 + M + K, K, M, N)
+    ref = oracle.sf_delta(U.numpy(), V.numpy())
+    scale = oracle.sf_delta(np.abs(U.numpy()), np.abs(V.numpy()))
+    Ud, Vd = U.to(d), V.to(d)
+    units = {}
+    for a in (api.SF_BF16X6, api.SF_FP32):
+        Z = torch.zeros(M, N, device=d)
+        log(f"sf_apply split-product accuracy M={M} N={N} K={K} {kind} arithmetic {a}")
+        with arithmetic(a):
+            api.sf_apply(Z, Ud, Vd, -1.0)
+            torch.cuda.synchronize()
+        err = np.abs(to_np(Z).astype(np.float64) - ref)
+        assert np.all(np.isfinite(err))
+        units[a] = float(np.max(err / np.maximum(scale, 1e-300)) / 2.0 ** -24)
+    assert units[api.SF_BF16X6] <= 2 * np.sqrt(K) + 16, units
+    assert units[api.SF_BF16X6] <= 2 * units[api.SF_FP32] + 4, units
 
 
 @pytest.mark.parametrize("M,N,K", [(256, 384, 40), (203, 129, 17), (1024, 512, 64), (2052, 4100, 24)])
@@ -121,8 +185,9 @@ def test_sf_apply_rejects_cpu_and_bad_shapes():
         api.sf_apply(W.to(d).double(), U.to(d), V.to(d), 0.1)
 
 
+@ARITHS
 @pytest.mark.parametrize("cfg,name", [(5, "fc6.W"), (5, "fc7.W"), (5, "fc8.W"), (2, "fc7.W")])
-def test_sf_apply_full_size_sampled(cfg, name):
+def test_sf_apply_full_size_sampled(cfg, name, arith):
     """The VGG19-22K FC layers at full size (P=16, B=32, K=512), and the
     4096 x 4096 layer of Sec. 3.2's worked example at P=8, B=32 (K=256, factors
     ~N(0,1) unscaled), checked at sampled points, the corners and stretches of
@@ -135,15 +200,17 @@ def test_sf_apply_full_size_sampled(cfg, name):
     rows, cols = sample_points(M, N, 4000, seed=M + N)
     ref = oracle.sf_apply_points(W.numpy(), U.numpy(), V.numpy(), wl.lr, rows, cols)
     Wd = W.to(d)
-    log(f"sf_apply full config {cfg} {name} {M}x{N} K={wl.K}")
-    api.sf_apply(Wd, U.to(d), V.to(d), wl.lr)
-    torch.cuda.synchronize()
+    log(f"sf_apply full config {cfg} {name} {M}x{N} K={wl.K} arithmetic {arith}")
+    with arithmetic(arith):
+        api.sf_apply(Wd, U.to(d), V.to(d), wl.lr)
+        torch.cuda.synchronize()
     got = to_np(Wd)[rows, cols]
     assert_close(got, ref, W_TOL, name)
     # and the raw gradient at the same points, tightly
     Z = torch.zeros(M, N, device=d)
-    api.sf_apply(Z, U.to(d), V.to(d), -1.0)
-    torch.cuda.synchronize()
+    with arithmetic(arith):
+        api.sf_apply(Z, U.to(d), V.to(d), -1.0)
+        torch.cuda.synchronize()
     ref_d = oracle.sf_apply_points(np.zeros((M, N), np.float32), U.numpy(), V.numpy(), -1.0, rows, cols)
     assert_close(to_np(Z)[rows, cols], ref_d, DELTA_TOL, name + " raw")
 
@@ -198,22 +265,30 @@ def test_sf_operands_beyond_32bit_offsets(M, N, K):
     assert_close(to_np(Wm)[rows, cols], w_ref, W_TOL, "momentum W")
 
 
-def test_sf_apply_batch_matches_oracle_and_single_calls():
+@ARITHS
+@pytest.mark.parametrize("big", [False, True], ids=["128-tiles", "256x128-tiles"])
+def test_sf_apply_batch_matches_oracle_and_single_calls(big, arith):
     """Grouped launch over layers of different shapes (ragged, M % 4 != 0,
     unaligned V): every layer as the oracle computes it, and bit-identical to
-    poseidon_sf_apply on the same layer (same K order in every tile)."""
+    poseidon_sf_apply on the same layer (same K order in every tile, whatever
+    the tile shape: with the split-bf16 products a group of at least four
+    256 x 128 tiles per CU takes that tile, while most of its layers alone
+    take 128 x 128 or 64 x 64 tiles)."""
     d = dev()
     shapes = [(2085, 4125), (129, 257), (4100, 2052), (21841 // 8, 1024 + 3)]
+    if big:
+        shapes += [(8192, 4100), (6000, 3000)]
     K = 40
     host = [_draw(M, N, K, seed=900 + 17 * i) for i, (M, N) in enumerate(shapes)]
     a = [(W.to(d), U.to(d), V.to(d)) for W, U, V in host]
     a[1] = (a[1][0], a[1][1], misaligned(a[1][2]))
     b = [(W.clone(), U, V) for W, U, V in a]
-    log(f"sf_apply_batch layers={len(a)} K={K}")
-    api.sf_apply_batch(a, 0.01)
-    for W, U, V in b:
-        api.sf_apply(W, U, V, 0.01)
-    torch.cuda.synchronize()
+    log(f"sf_apply_batch layers={len(a)} K={K} arithmetic {arith}")
+    with arithmetic(arith):
+        api.sf_apply_batch(a, 0.01)
+        for W, U, V in b:
+            api.sf_apply(W, U, V, 0.01)
+        torch.cuda.synchronize()
     for (W0, U0, V0), (Wa, _, _), (Wb, _, _) in zip(host, a, b):
         ref = oracle.sf_apply(W0.numpy(), U0.numpy(), V0.numpy(), 0.01)
         assert_close(to_np(Wa), ref, W_TOL, f"batch {tuple(W0.shape)}")

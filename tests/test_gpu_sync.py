@@ -136,10 +136,12 @@ def test_sync_iteration_missing_payload_is_an_error():
 
 def test_sync_iteration_launch_records():
     """Timing mode: one record per launch in backprop order, SF layers on
-    stream 0 and PS tensors on stream 1 (small ones in one batched pass)."""
+    stream 0 and PS tensors on stream 1 (small ones in one batched pass).
+    fc6's rebuild is long next to the applies, so the iteration takes two
+    streams."""
     d = dev()
     wl = I.workload(5)
-    host = I.make_tensors(wl, only=["fc7.W", "fc7.b", "conv5_4.W"])
+    host = I.make_tensors(wl, only=["fc6.W", "fc7.b", "conv5_4.W"])
     devt = _to_dev(host, d)
     pool = api.StreamPool(4)
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
@@ -316,7 +318,7 @@ def test_sync_iteration_runs_comparable_kinds_on_one_stream():
     pool.close()
 
 
-@pytest.mark.parametrize("cfg,only", [(1, None), (5, ["fc7.W", "fc7.b", "conv5_4.W"]),
+@pytest.mark.parametrize("cfg,only", [(1, None), (5, ["fc6.W", "fc7.b", "conv5_4.W"]),
                                       (4, ["conv45", "conv46", "fc.W"])])
 def test_sync_iteration_is_ordered_on_the_callers_stream(cfg, only):
     """The iteration behaves as one operation on the caller's stream, whether

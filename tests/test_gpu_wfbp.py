@@ -213,9 +213,10 @@ def test_wfbp_updates_overlap_later_backward_work(policy):
 
 
 def test_wfbp_launch_records_and_errors():
+    # fc6's rebuild is long next to the applies: the iteration takes two streams
     d = dev()
     wl = I.workload(5)
-    host = I.make_tensors(wl, only=["fc7.W", "fc7.b", "conv5_4.W"])
+    host = I.make_tensors(wl, only=["fc6.W", "fc7.b", "conv5_4.W"])
     devt = _to_dev(host, d)
     pool = api.StreamPool(2)
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
