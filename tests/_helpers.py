@@ -1,6 +1,7 @@
 """Shared helpers for the GPU parity tests (no test functions here)."""
 from __future__ import annotations
 
+import contextlib
 import sys
 
 import numpy as np
@@ -65,3 +66,15 @@ def sample_points(M: int, N: int, count: int, seed: int):
     rows += [M - 1] * min(N, 64) + list(range(max(0, M - 64), M))
     cols += list(range(max(0, N - 64), N)) + [N - 1] * min(M, 64)
     return np.array(rows, dtype=np.int64), np.array(cols, dtype=np.int64)
+
+
+@contextlib.contextmanager
+def sf_arithmetic(a: int):
+    """Run the block with the SF products formed as `a` (poseidon_sf_set_arithmetic),
+    then restore the default split-bf16 products."""
+    from paper_1706_03292_amd import api
+    api.sf_set_arithmetic(a)
+    try:
+        yield
+    finally:
+        api.sf_set_arithmetic(api.SF_BF16X6)

@@ -7,7 +7,7 @@ import pytest
 import torch
 
 import oracle
-from _helpers import BUF_TOL, W_TOL, assert_close, dev, log, misaligned, to_np
+from _helpers import BUF_TOL, W_TOL, assert_close, dev, log, misaligned, sf_arithmetic, to_np
 from paper_1706_03292_amd import api
 from paper_1706_03292_amd import inputs as I
 
@@ -32,19 +32,22 @@ def test_sf_random_shapes(seed):
     U = I.randn(9001 + 5 * seed, (K, M))
     V = I.randn(9002 + 5 * seed, (K, N))
     buf = I.randn(9003 + 5 * seed, (M, N), 1e-3)
-    log(f"sf random seed={seed} M={M} N={N} K={K} momentum={mom} misaligned={mis}")
+    arith = api.SF_FP32 if seed % 3 == 2 else api.SF_BF16X6
+    log(f"sf random seed={seed} M={M} N={N} K={K} momentum={mom} misaligned={mis} arithmetic {arith}")
     place = (lambda t: misaligned(t.to(d))) if mis else (lambda t: t.to(d))
     Wd, Ud, Vd = place(W), place(U), place(V)
     if mom:
         bd = place(buf)
-        api.sf_apply_momentum(Wd, bd, Ud, Vd, 0.01, 0.9)
+        with sf_arithmetic(arith):
+            api.sf_apply_momentum(Wd, bd, Ud, Vd, 0.01, 0.9)
+            torch.cuda.synchronize()
         w_ref, b_ref = oracle.sf_apply_momentum(W.numpy(), buf.numpy(), U.numpy(), V.numpy(), 0.01, 0.9)
-        torch.cuda.synchronize()
         assert_close(to_np(bd), b_ref, BUF_TOL, "buf")
     else:
-        api.sf_apply(Wd, Ud, Vd, 0.01)
+        with sf_arithmetic(arith):
+            api.sf_apply(Wd, Ud, Vd, 0.01)
+            torch.cuda.synchronize()
         w_ref = oracle.sf_apply(W.numpy(), U.numpy(), V.numpy(), 0.01)
-        torch.cuda.synchronize()
     assert_close(to_np(Wd), w_ref, W_TOL, "W")
 
 

@@ -1,13 +1,11 @@
 """GPU parity of poseidon_sf_apply (SF reconstruction + SGD) with the oracle."""
-import contextlib
-
 import numpy as np
 import pytest
 import torch
 
 import oracle
 from _helpers import (DELTA_TOL, W_TOL, assert_close, dev, log, misaligned, sample_points,
-                      to_np)
+                      sf_arithmetic, to_np)
 from paper_1706_03292_amd import api
 from paper_1706_03292_amd import inputs as I
 
@@ -18,13 +16,7 @@ pytestmark = pytest.mark.gpu
 ARITHS = pytest.mark.parametrize("arith", [api.SF_BF16X6, api.SF_FP32], ids=["bf16x6", "fp32"])
 
 
-@contextlib.contextmanager
-def arithmetic(a):
-    api.sf_set_arithmetic(a)
-    try:
-        yield
-    finally:
-        api.sf_set_arithmetic(api.SF_BF16X6)
+arithmetic = sf_arithmetic
 
 
 def _draw(M, N, K, seed, w_std=0.01, sf_scale=1.0):

@@ -6,7 +6,8 @@ import pytest
 import torch
 
 import oracle
-from _helpers import DELTA_TOL, W_TOL, assert_close, dev, log, misaligned, sample_points, to_np
+from _helpers import (DELTA_TOL, W_TOL, assert_close, dev, log, misaligned, sample_points, sf_arithmetic,
+                      to_np)
 from paper_1706_03292_amd import api
 from paper_1706_03292_amd import inputs as I
 
@@ -27,18 +28,21 @@ SHAPES = [
     (1, 1, 1), (33, 65, 1), (300, 200, 37), (261, 387, 18), (1024, 512, 64),
     (1000, 2048, 1024),                       # 64 x 64 tiles
     (2085, 4125, 40), (4100, 2052, 100),      # 128 x 128 tiles, ragged, M and N % 4 != 0
+    (8192, 4130, 24),                         # 256 x 128 tiles (split products), ragged N
 ]
 
 
+@pytest.mark.parametrize("arith", [api.SF_BF16X6, api.SF_FP32], ids=["bf16x6", "fp32"])
 @pytest.mark.parametrize("M,N,K", SHAPES)
-def test_sf_momentum_matches_oracle(M, N, K):
+def test_sf_momentum_matches_oracle(M, N, K, arith):
     d = dev()
     W, U, V, buf = _draw(M, N, K, seed=7 * M + N + K)
     w_ref, b_ref = oracle.sf_apply_momentum(W.numpy(), buf.numpy(), U.numpy(), V.numpy(), 0.01, MU)
     Wd, bd = W.to(d), buf.to(d)
-    log(f"sf_apply_momentum M={M} N={N} K={K}")
-    api.sf_apply_momentum(Wd, bd, U.to(d), V.to(d), 0.01, MU)
-    torch.cuda.synchronize()
+    log(f"sf_apply_momentum M={M} N={N} K={K} arithmetic {arith}")
+    with sf_arithmetic(arith):
+        api.sf_apply_momentum(Wd, bd, U.to(d), V.to(d), 0.01, MU)
+        torch.cuda.synchronize()
     assert_close(to_np(bd), b_ref, DELTA_TOL, f"buf {M}x{N} K={K}")
     assert_close(to_np(Wd), w_ref, W_TOL, f"W {M}x{N} K={K}")
 
