@@ -76,23 +76,32 @@ int main(void)
     HIP_OK(hipSetDevice(0));
     printf("poseidon ABI version %d\n", poseidon_abi_version());
 
-    /* SF reconstruction + SGD, ragged shape. */
-    {
+    /* SF reconstruction + SGD, ragged shape, with each arithmetic of the
+     * products (the default split-bf16 and the fp32 matrix-core products). */
+    if (poseidon_sf_arithmetic() != POSEIDON_SF_BF16X6 || poseidon_sf_set_arithmetic(5) != POSEIDON_ERR_INVALID_ARG) {
+        printf("poseidon_sf_arithmetic default / bad value FAIL\n");
+        ++failures;
+    }
+    for (int a = 0; a < 2; ++a) {
+        const int32_t arith = a == 0 ? POSEIDON_SF_BF16X6 : POSEIDON_SF_FP32;
         const int64_t M = 300, N = 200, K = 37;
         float *W = malloc(M * N * 4), *U = malloc(K * M * 4), *V = malloc(K * N * 4), *got = malloc(M * N * 4);
         fill(W, M * N, 1, 0.01f);
         fill(U, K * M, 2, 1.0f);
         fill(V, K * N, 3, 1.0f);
         float *dW = dev_copy(W, M * N), *dU = dev_copy(U, K * M), *dV = dev_copy(V, K * N);
+        const int rs = poseidon_sf_set_arithmetic(arith);
         const int rc = poseidon_sf_apply(dW, dU, dV, M, N, K, 0.01f, 0);
         HIP_OK(hipDeviceSynchronize());
+        poseidon_sf_set_arithmetic(POSEIDON_SF_BF16X6);
         to_host(got, dW, M * N);
         oracle_sf_apply(W, U, V, M, N, K, 0.01f);
-        if (rc != POSEIDON_OK) {
-            printf("poseidon_sf_apply returned %d FAIL\n", rc);
+        if (rc != POSEIDON_OK || rs != POSEIDON_OK) {
+            printf("poseidon_sf_apply returned %d (arithmetic %d: %d) FAIL\n", rc, (int)arith, rs);
             ++failures;
         }
-        check("poseidon_sf_apply 300x200 K=37", got, W, M * N, 1e-4);
+        check(a == 0 ? "poseidon_sf_apply 300x200 K=37 (split-bf16 products)"
+                     : "poseidon_sf_apply 300x200 K=37 (fp32 products)", got, W, M * N, 1e-4);
         HIP_OK(hipFree(dW));
         HIP_OK(hipFree(dU));
         HIP_OK(hipFree(dV));
