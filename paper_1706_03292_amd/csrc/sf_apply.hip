@@ -94,6 +94,16 @@ struct Small {
 };
 constexpr int64_t BIG_TILES_PER_CU = 4, MID_TILES_PER_CU = 2;
 
+// Tile rows an XCD's run walks at a time: 8 of 128 rows (the 128 workgroups
+// an XCD runs together then read 8 U and 16 V panels, the fewest for 128 such
+// tiles), 4 of 256 rows (its 64 workgroups of 256 x 128 read 4 U and 16 V
+// panels: the VGG19-22K grouped launch fetched 1.50 GB from memory against
+// 1.81 GB with 8 rows, 1.85 with 2 and 2.57 with 16, in equal time).
+template <int BM>
+struct TileRows {
+    static constexpr int G = BM >= 256 ? 4 : 8;
+};
+
 // Workgroup id -> (tile row, tile column): contiguous runs per XCD, GM tile
 // rows at a time inside a run.
 template <int GM>
@@ -775,7 +785,7 @@ __attribute__((amdgpu_waves_per_eu(SfOcc<WM, WN>::W, SfOcc<WM, WN>::W))) void sf
     float lr, int tiles_m, int tiles_n, float* __restrict__ buf, float mu)
 {
     int tm, tn;
-    tile_coords<8>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
+    tile_coords<TileRows<BM>::G>(blockIdx.x, tiles_m * tiles_n, tiles_m, tiles_n, tm, tn);
     sf_tile_direct<BM, BN, BK, WM, WN, SPLIT, MOM, PRE>(W, U, V, M, N, K, lr, tm, tn, buf, mu);
 }
 
@@ -821,7 +831,7 @@ __attribute__((amdgpu_waves_per_eu(SfOcc<WM, WN>::W, SfOcc<WM, WN>::W))) void sf
 // instead of every layer ending in a partly idle round.  Layer descriptors
 // travel by value in the kernel arguments; the XCD-aware order runs over the
 // combined list (layer by layer, in the order given), and inside a layer tile
-// rows are walked 8 at a time.
+// rows are walked a group (TileRows) at a time.
 // ---------------------------------------------------------------------------
 struct SfBatchItem {
     float* W;
@@ -842,7 +852,7 @@ struct SfBatchArgs {
 };
 
 // Tile t of the combined list (layer by layer; inside a layer tile rows
-// walked 8 at a time).
+// walked a group (TileRows) at a time).
 template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, int PRE = W_PRE>
 __device__ __forceinline__ void batch_tile(const SfBatchArgs& args, int t, int64_t K, float lr)
 {
@@ -851,7 +861,7 @@ __device__ __forceinline__ void batch_tile(const SfBatchArgs& args, int t, int64
         ++l;
     const int local = t - args.item[l].first_tile;
     const int tiles_m = args.item[l].tiles_m, tiles_n = args.item[l].tiles_n;
-    constexpr int G = 8;
+    constexpr int G = TileRows<BM>::G;
     const int per_group = G * tiles_n;
     const int g = local / per_group;
     const int first_m = g * G;
