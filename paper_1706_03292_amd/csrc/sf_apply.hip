@@ -4,12 +4,18 @@
 //   W[m][n] <- W[m][n] - lr * sum_{k<K} U[k][m] * V[k][n]
 //
 // A dense contraction of depth K = P*B with both operands stored K-major
-// (row k of U is u_k, row k of V is v_k).  It runs on the fp32 matrix cores
-// (v_mfma_f32_32x32x2_f32: a 32x32 output block from a 32x2 and a 2x32
-// operand, 64 lanes, 16 accumulator registers per lane).
+// (row k of U is u_k, row k of V is v_k), on the matrix cores in 32x32 output
+// blocks (64 lanes, 16 fp32 accumulator registers per lane).  By default the
+// fp32 products are formed on the bf16 matrix cores (v_mfma_f32_32x32x16_bf16)
+// from an exact three-part bf16 split of each operand, six part products per
+// fp32 product (see "Split-bf16 products" below); the fp32 matrix cores
+// (v_mfma_f32_32x32x2_f32) are the alternative the caller can choose, and the
+// register-staged variant for very large operands always uses them.
 //
 // Tiling: a workgroup owns a BM x BN block of W and loops over K in steps of
-// BK; each wave owns a WM x WN sub-block (WM/32 x WN/32 MFMA blocks).  The
+// BK; each wave owns a WM x WN sub-block (WM/32 x WN/32 MFMA blocks): 256 x
+// 128 tiles of 128 x 64 sub-blocks for large layers with the split products,
+// else 128 x 128 tiles of 64 x 64, or 64 x 64 tiles of 32 x 32 for small ones.  The
 // K-slices U[k0:k0+BK, m0:m0+BM] and V[k0:k0+BK, n0:n0+BN] go straight from
 // global memory into LDS with the gfx950 LDS-direct buffer loads (each lane
 // moves 16 bytes, a wave instruction fills 1 KB of LDS), two slices in
@@ -776,7 +782,8 @@ __device__ __forceinline__ void sf_tile_staged(float* As, float* Bs, float* __re
 }
 
 // ---------------------------------------------------------------------------
-// Kernels, compiled for at least 4 waves per SIMD (at most 128 VGPRs a wave).
+// Kernels, compiled for the waves per SIMD of their tile shape (SfOcc: 4, at
+// most 128 VGPRs a wave, or 2 for the 128 x 64 sub-blocks).
 // ---------------------------------------------------------------------------
 template <int BM, int BN, int BK, int WM, int WN, bool SPLIT, bool MOM, int PRE = W_PRE>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
