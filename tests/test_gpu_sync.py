@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from _helpers import BUF_TOL, W_TOL, assert_close, dev, log, sample_points, to_np
+from _helpers import BUF_TOL, W_TOL, assert_close, dev, log, sample_points, sf_arithmetic, to_np
 from paper_1706_03292_amd import api
 from paper_1706_03292_amd import inputs as I
 
@@ -60,18 +60,24 @@ def _to_dev(host, d):
     return out
 
 
-@pytest.mark.parametrize("cfg,streams", [(1, 1), (1, 4), (2, 2), (2, 1), (3, 4), (4, 4), (5, 2), (5, 4), (5, 1),
-                                         (5, 8)])
-def test_sync_iteration_matches_oracle(cfg, streams):
+@pytest.mark.parametrize("cfg,streams,arith", [(1, 1, 0), (1, 4, 0), (2, 2, 0), (2, 1, 0), (3, 4, 0), (4, 4, 0),
+                                               (5, 2, 0), (5, 4, 0), (5, 1, 0), (5, 8, 0),
+                                               (2, 2, 1), (4, 2, 1), (5, 2, 1)])
+def test_sync_iteration_matches_oracle(cfg, streams, arith):
+    """Whole iterations against the oracle, with the split-bf16 SF products
+    (arith 0) and with the fp32 products (arith 1: the stream policy then
+    assumes the fp32 rates, so the same workload may be issued differently)."""
     d = dev()
     wl = I.workload(cfg)
     host = I.make_tensors(wl)
     devt = _to_dev(host, d)
     pool = api.StreamPool(streams)
     it = api.SyncIteration(pool, devt, wl.B, wl.P, wl.lr, wl.momentum)
-    log(f"sync_iteration config {cfg} streams={streams} tensors={len(devt)}")
-    schemes = it()
-    torch.cuda.synchronize()
+    a = api.SF_FP32 if arith else api.SF_BF16X6
+    log(f"sync_iteration config {cfg} streams={streams} tensors={len(devt)} arithmetic {a}")
+    with sf_arithmetic(a):
+        schemes = it()
+        torch.cuda.synchronize()
     _oracle_check(host, devt, wl, schemes)
     pool.close()
 
