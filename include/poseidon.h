@@ -122,7 +122,10 @@ int poseidon_sf_apply_momentum(float* W, float* buf, const float* U, const float
  * which has at most 8 significant bits) and accumulates the six products
  * h*h, h*m, m*h, h*l, l*h and m*m in fp32 on the bf16 matrix cores (the six-
  * product split of Henry, Tang and Heinecke, ARITH 2019); POSEIDON_SF_FP32
- * accumulates the fp32 matrix-core products.  The choice is process-wide
+ * accumulates the fp32 matrix-core products.  The two agree to fp32
+ * rounding on finite operands below 3.39e38 in magnitude (the largest bf16);
+ * an infinite or larger operand makes the outputs it reaches NaN with the
+ * split products (inf or NaN with the fp32 ones).  The choice is process-wide
  * and does not change which scheme Alg. 1 picks.  Returns POSEIDON_OK or
  * POSEIDON_ERR_INVALID_ARG (an unknown value; the setting is unchanged).
  */
