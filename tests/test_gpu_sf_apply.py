@@ -300,3 +300,29 @@ def test_sf_apply_batch_small_group_and_errors():
         api.sf_apply_batch([a[0], (a[1][0], a[1][1][:5].contiguous(), a[1][2][:5].contiguous())], 0.01)
     with pytest.raises(api.PoseidonError):
         api.sf_apply_batch([a[0], a[0]], 0.01)          # the same W twice
+
+
+def test_sf_non_finite_operands_as_documented():
+    """An infinite factor value reaches its row of the gradient: NaN with the
+    split-bf16 products (h rounds to infinity and inf - inf leaves the parts),
+    +-inf with the fp32 products; every other row is finite and as the oracle's."""
+    d = dev()
+    M, N, K = 64, 96, 8
+    _, U, V = _draw(M, N, K, seed=321)
+    U[3, 5] = float("inf")
+    ref = oracle.sf_delta(np.where(np.isfinite(U.numpy()), U.numpy(), 0.0).astype(np.float32), V.numpy())
+    for a in (api.SF_BF16X6, api.SF_FP32):
+        Z = torch.zeros(M, N, device=d)
+        log(f"sf_apply non-finite operand arithmetic {a}")
+        with arithmetic(a):
+            api.sf_apply(Z, U.to(d), V.to(d), -1.0)
+            torch.cuda.synchronize()
+        z = to_np(Z)
+        row = z[5]
+        if a == api.SF_BF16X6:
+            assert np.all(np.isnan(row[V[3].numpy() != 0]))
+        else:
+            assert np.all(np.isinf(row[V[3].numpy() != 0]))
+        others = np.delete(z, 5, axis=0)
+        assert np.all(np.isfinite(others))
+        assert_close(others, np.delete(ref, 5, axis=0), DELTA_TOL, "finite rows")
