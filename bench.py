@@ -49,7 +49,7 @@ def _parse():
     ap.add_argument("--cpu-baseline", choices=["on", "off"], default="on")
     ap.add_argument("--wfbp", choices=["on", "off"], default="on",
                     help="also time the iteration overlapped with a synthetic VGG19 backward pass")
-    ap.add_argument("--wfbp-steps", type=int, default=10)
+    ap.add_argument("--wfbp-steps", type=int, default=16)
     ap.add_argument("--cpu-fraction", type=float, default=1.0,
                     help="fraction of each tensor the CPU oracle runs on")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -138,17 +138,20 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
     bw = SB.SyntheticBackward(wl, [t["W"] for t in devt], d)
     events = {l.layer: torch.cuda.Event() for l in bw.layers}
     ready = bw.ready_list(events, len(devt))
-    def timed(fn):
-        out = []
+    def timed_interleaved(fns):
+        # every variant once per round, rounds repeated: slow drifts of the
+        # clock affect all alike; the median of each variant's passes
+        out = [[] for _ in fns]
         for rep in range(steps + 2):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(cs)
-            fn()
-            b.record(cs)
-            torch.cuda.synchronize()
-            if rep >= 2:
-                out.append(a.elapsed_time(b))
-        return sum(out) / len(out)
+            for i, fn in enumerate(fns):
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(cs)
+                fn()
+                b.record(cs)
+                torch.cuda.synchronize()
+                if rep >= 2:
+                    out[i].append(a.elapsed_time(b))
+        return [sorted(o)[len(o) // 2] for o in out]
 
     def serial():
         bw.run(cs)
@@ -163,26 +166,21 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
             pool.set_wfbp_policy(policy)
             bw.run(cs, events)
             it(cs, ready=ready)
-            pool.set_wfbp_policy(api.WFBP_ALL_LAST)
+            pool.set_wfbp_policy(api.WFBP_SFB_LAST)
         return run
 
     # Alg. 2's own schedule (every update, the SFB rebuilds included, on its
-    # own layer's event), and the PS applies alone on their events
+    # own layer's event), and every update held until the last event
     wfbp_each = with_policy(api.WFBP_EACH)
-    wfbp_sfb_last = with_policy(api.WFBP_SFB_LAST)
+    wfbp_all_last = with_policy(api.WFBP_ALL_LAST)
 
-    t_bw = timed(lambda: bw.run(cs))
-    t_bw_ev = timed(lambda: bw.run(cs, events))
-    t_sync = timed(lambda: it(cs))
-    t_serial = timed(serial)
-    t_wfbp = timed(wfbp)
-    t_each = timed(wfbp_each)
-    t_sfb_last = timed(wfbp_sfb_last)
+    t_bw, t_bw_ev, t_sync, t_serial, t_wfbp, t_each, t_all_last = timed_interleaved(
+        [lambda: bw.run(cs), lambda: bw.run(cs, events), lambda: it(cs), serial, wfbp, wfbp_each, wfbp_all_last])
     hidden = t_serial - t_wfbp
     # One more of each with the library's launch timing: the updates' own
     # durations show whether they ran beside the backward pass.
     launch = {}
-    for name, fn in (("serial", serial), ("wfbp", wfbp), ("wfbp_each", wfbp_each), ("wfbp_sfb_last", wfbp_sfb_last)):
+    for name, fn in (("serial", serial), ("wfbp", wfbp), ("wfbp_each", wfbp_each), ("wfbp_all_last", wfbp_all_last)):
         pool.set_timing(True)
         fn()
         recs = pool.launch_times()
@@ -203,13 +201,14 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
         "hidden_sync_ms": round(hidden, 3), "hidden_frac": round(hidden / t_sync, 3),
         "stall_ms": round(max(0.0, t_wfbp - t_bw), 3), "busy_frac": round(t_bw / t_wfbp, 3),
         "wfbp_each_ms": round(t_each, 3), "hidden_each_ms": round(t_serial - t_each, 3),
-        "wfbp_sfb_last_ms": round(t_sfb_last, 3), "hidden_sfb_last_ms": round(t_serial - t_sfb_last, 3),
-        "schedule_note": "wfbp: the library's default schedule on one GPU (POSEIDON_WFBP_ALL_LAST: every update "
-                         "waits for every layer's event, then the plain iteration's launches); wfbp_each: every "
-                         "update on its own layer's event (Alg. 2); wfbp_sfb_last: the PS applies on their own "
-                         "events, the SFB rebuilds after the backward pass as one grouped launch",
+        "wfbp_all_last_ms": round(t_all_last, 3), "hidden_all_last_ms": round(t_serial - t_all_last, 3),
+        "schedule_note": "wfbp: the library's default schedule on one GPU (POSEIDON_WFBP_SFB_LAST: the PS applies "
+                         "on their own layers' events, the SFB rebuilds after every event as one grouped launch); "
+                         "wfbp_each: every update on its own layer's event (Alg. 2); wfbp_all_last: every update "
+                         "waits for every layer's event, then the plain iteration's launches",
         "update_launch_ms": launch,
         "steps": steps,
+        "timing_note": "each figure the median of `steps` passes, the seven variants run in turn in every round",
     }
 
 

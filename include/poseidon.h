@@ -60,8 +60,8 @@ extern "C" {
 #define POSEIDON_KIND_OTHER  1
 
 /* Schedules of poseidon_sync_iteration_wfbp (poseidon_pool_set_wfbp_policy). */
-#define POSEIDON_WFBP_ALL_LAST 0   /* every update after every ready event (default on one GPU) */
-#define POSEIDON_WFBP_SFB_LAST 1   /* PS applies on their own events, SFB rebuilds after every event */
+#define POSEIDON_WFBP_ALL_LAST 0   /* every update after every ready event (the serial order) */
+#define POSEIDON_WFBP_SFB_LAST 1   /* PS applies on their own events, SFB rebuilds after every event (default) */
 #define POSEIDON_WFBP_EACH     2   /* every update on its own ready event (Alg. 2) */
 
 /* Arithmetic of the SF reconstruction's contraction (poseidon_sf_set_arithmetic). */
@@ -512,11 +512,11 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
  * a one-stream iteration), none on `stream`, that only PS tensors of fewer than 2^17 values
  * share the batched pass, so that each other PS update starts after its own
  * event, and that the pool's schedule (poseidon_pool_set_wfbp_policy) can
- * hold updates back: by default every update waits for every ready event and
- * the launches are poseidon_sync_iteration's; under POSEIDON_WFBP_SFB_LAST
- * the SFB tensors wait for every ready event and share one grouped launch;
- * under POSEIDON_WFBP_EACH every SFB tensor keeps a launch of its own that
- * starts after its own event.  `stream` waits for every update at the end.
+ * hold updates back: by default (POSEIDON_WFBP_SFB_LAST) the SFB tensors wait
+ * for every ready event and share one grouped launch; under
+ * POSEIDON_WFBP_ALL_LAST every update waits for every ready event and the
+ * launches are poseidon_sync_iteration's; under POSEIDON_WFBP_EACH every SFB
+ * tensor keeps a launch of its own that starts after its own event.  `stream` waits for every update at the end.
  * ready: count non-NULL events, caller-owned, not retained after the call.
  * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (also for NULL ready or a NULL
  * entry), POSEIDON_ERR_PAYLOAD or POSEIDON_ERR_HIP.
@@ -538,20 +538,22 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 /*
  * The schedule poseidon_sync_iteration_wfbp uses on this pool.
  * POSEIDON_WFBP_EACH is Alg. 2's: every tensor's update starts on its own
- * ready event.  POSEIDON_WFBP_SFB_LAST starts the PS applies on their own
- * events but holds the SFB rebuilds until every tensor's event has completed
- * and runs them as one grouped launch.  POSEIDON_WFBP_ALL_LAST (the default)
+ * ready event.  POSEIDON_WFBP_SFB_LAST (the default) starts the PS applies on
+ * their own events but holds the SFB rebuilds until every tensor's event has
+ * completed and runs them as one grouped launch.  POSEIDON_WFBP_ALL_LAST
  * holds every update until every tensor's event has completed and then
  * issues poseidon_sync_iteration's launches (on the pool's streams): the
- * serial order, as a fallback for a GPU that has no idle time to fill.  On one GPU the updates
- * are local computation that competes with the caller's backward pass: the
- * rebuilds for the matrix cores its GEMMs use, the applies for the memory
- * bandwidth and CU slots of its elementwise steps.  Measured on a 34.6 ms
- * synthetic VGG19-22K backward pass with a 1.9 ms iteration: EACH ends
- * 0.39 ms and SFB_LAST 0.10 ms later than the backward pass followed by the
- * iteration.  What Alg. 2 hides is time the GPU would otherwise spend
- * waiting for the network; EACH and SFB_LAST are for callers that have such
- * time.  Results are the same under every schedule (bit-identical kernels).
+ * serial order.  On one GPU the updates are local computation that competes
+ * with the caller's backward pass: the rebuilds for the matrix cores its
+ * GEMMs use, the applies for the memory bandwidth and CU slots of its
+ * elementwise steps.  Measured on a 34.5 ms synthetic VGG19-22K backward
+ * pass with a 1.2 ms iteration (medians of 16 interleaved passes; the median
+ * of five such runs on five machines), against the backward pass followed
+ * by the iteration: SFB_LAST 0.06 ms later (the applies beside the backward
+ * pass's last layers make up for the events the backward pass records),
+ * ALL_LAST 0.14 ms, EACH 0.41 ms; single runs move by +-0.15 ms.  What
+ * Alg. 2 hides is time the GPU would otherwise spend waiting for the
+ * network; EACH is for callers that have such time.  Results are the same under every schedule (bit-identical kernels).
  * Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG (NULL pool, unknown policy).
  */
 int poseidon_pool_set_wfbp_policy(poseidon_stream_pool* pool, int32_t policy);

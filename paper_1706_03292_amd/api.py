@@ -268,7 +268,7 @@ class StreamPool:
         return self._h
 
     def set_wfbp_policy(self, policy: int) -> None:
-        """WFBP_ALL_LAST (default), WFBP_SFB_LAST or WFBP_EACH (poseidon_pool_set_wfbp_policy)."""
+        """WFBP_SFB_LAST (default), WFBP_ALL_LAST or WFBP_EACH (poseidon_pool_set_wfbp_policy)."""
         _check("poseidon_pool_set_wfbp_policy", L.lib().poseidon_pool_set_wfbp_policy(self.handle, int(policy)))
 
     def set_timing(self, enable: bool) -> None:

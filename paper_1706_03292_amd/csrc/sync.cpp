@@ -19,7 +19,7 @@ struct poseidon_stream_pool {
     std::vector<hipEvent_t> joined;   // one per stream: its last update of the iteration
     hipEvent_t fork = nullptr;        // work enqueued on the caller's stream before the iteration
     bool timing = false;
-    int32_t wfbp_policy = POSEIDON_WFBP_ALL_LAST;
+    int32_t wfbp_policy = POSEIDON_WFBP_SFB_LAST;
     std::vector<hipEvent_t> t_start;  // per launch of the last timed iteration
     std::vector<hipEvent_t> t_stop;
     std::vector<poseidon_launch_record> t_rec;

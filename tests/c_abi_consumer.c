@@ -182,8 +182,9 @@ int main(void)
         HIP_OK(hipDeviceSynchronize());
         to_host(g1, dW1, M * N);
         to_host(g2, dW2, n);
-        /* The wait-free iteration under Alg. 2's schedule and under the
-         * default (every update after every event): the same results. */
+        /* The wait-free iteration under Alg. 2's schedule and under
+         * POSEIDON_WFBP_ALL_LAST (every update after every event): the same
+         * results. */
         {
             hipEvent_t ev;
             HIP_OK(hipEventCreate(&ev));

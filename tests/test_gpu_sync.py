@@ -172,8 +172,9 @@ def test_sync_iteration_launch_records():
 
 def test_sync_iteration_groups_the_fc_layers_unless_wfbp_each():
     """Several SFB layers without a buffer share one grouped launch (record
-    tensor -1) in the plain iteration and under the default wait-free
-    schedule and POSEIDON_WFBP_SFB_LAST (the rebuilds wait for every event);
+    tensor -1) in the plain iteration and under the held wait-free schedules,
+    POSEIDON_WFBP_ALL_LAST and POSEIDON_WFBP_SFB_LAST (the default; the
+    rebuilds wait for every event);
     under POSEIDON_WFBP_EACH each keeps its own launch, in backprop order;
     the results are bit-identical."""
     d = dev()
@@ -194,6 +195,7 @@ def test_sync_iteration_groups_the_fc_layers_unless_wfbp_each():
     log("sync_iteration grouped FC launch")
     it_a(cs)
     assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == [(api.SFB, -1, 0)]
+    pool.set_wfbp_policy(api.WFBP_ALL_LAST)
     it_b(cs, ready=[ev] * len(b))
     assert [(r["scheme"], r["tensor"], r["stream"]) for r in pool.launch_times()] == [(api.SFB, -1, 0)]
     pool.set_wfbp_policy(api.WFBP_SFB_LAST)
@@ -430,12 +432,13 @@ def test_sync_iteration_spreads_the_rebuilds_beside_longer_applies(case):
     assert torch.equal(devt[-1]["W"], Wc)
     if "buf" in fc:
         assert torch.equal(devt[-1]["buf"], bc)
-    # The held wait-free schedule issues the same (spread) launches on the
-    # pool's streams: bitwise the same updates.
+    # The held wait-free schedule POSEIDON_WFBP_ALL_LAST issues the same
+    # (spread) launches on the pool's streams: bitwise the same updates.
     held = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items()} for h in host]
     cs = torch.cuda.current_stream(d)
     ev = torch.cuda.Event()
     ev.record(cs)
+    pool.set_wfbp_policy(api.WFBP_ALL_LAST)
     api.SyncIteration(pool, held, B, P, lr, mu)(cs, ready=[ev] * len(held))
     torch.cuda.synchronize()
     for g, h in zip(devt, held):

@@ -174,7 +174,10 @@ def test_wfbp_backward_reads_weights_before_their_update(policy):
 def test_wfbp_updates_overlap_later_backward_work(policy):
     """All updates' events are recorded before a long single-wave sleep kernel
     (the rest of a backward pass that leaves the GPU idle): with WFBP the
-    iteration ends with the sleep, not after it."""
+    iteration ends with the sleep, not after it.  The sleep counts shader
+    clock cycles, and the updates beside it can lower the clock, so what is
+    checked is the time from the sleep's end to the iteration's, not the
+    total against a sleep measured alone."""
     d = dev()
     wl = I.workload(3)
     devt = _to_dev(I.make_tensors(wl), d)
@@ -199,16 +202,25 @@ def test_wfbp_updates_overlap_later_backward_work(policy):
     ev = torch.cuda.Event()
 
     def wfbp():
+        # (sleep beside the updates, iteration after the sleep's end)
+        a, b, c = (torch.cuda.Event(enable_timing=True) for _ in range(3))
         ev.record(cs)
+        a.record(cs)
         with torch.cuda.stream(cs):
             torch.cuda._sleep(cycles)
+        b.record(cs)
         it(cs, ready=[ev] * len(devt))
+        c.record(cs)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b), b.elapsed_time(c)
 
     log(f"wfbp overlap: sleep {t_sleep:.2f} ms, sync {t_sync:.2f} ms")
-    t_wfbp = min(timed(wfbp) for _ in range(3))
-    log(f"wfbp overlap: wfbp {t_wfbp:.2f} ms")
+    runs = [wfbp() for _ in range(3)]
+    t_beside = min(r[0] for r in runs)
+    t_tail = sorted(r[1] for r in runs)[1]          # median of three
+    log(f"wfbp overlap: sleep beside the updates {t_beside:.2f} ms, then {t_tail:.3f} ms")
     assert t_sleep > 4 * t_sync
-    assert t_wfbp < t_sleep + 0.5 * t_sync
+    assert t_tail < 0.5 * t_sync
     pool.close()
 
 
@@ -248,7 +260,7 @@ def test_wfbp_launch_records_and_errors():
 
 @pytest.mark.parametrize("policy", ["ALL_LAST", "SFB_LAST"])
 def test_wfbp_held_schedules_start_the_rebuilds_after_every_event(policy):
-    """Under POSEIDON_WFBP_ALL_LAST (the default) and POSEIDON_WFBP_SFB_LAST
+    """Under POSEIDON_WFBP_ALL_LAST and POSEIDON_WFBP_SFB_LAST (the default)
     an SFB rebuild waits for every tensor's ready event, not only its own: the FC layer's
     event is recorded first, then the stream is kept busy and the layer's own
     factor rows are scaled by 64 (exact in fp32) before the last tensor's
