@@ -548,10 +548,10 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
  * GEMMs use, the applies for the memory bandwidth and CU slots of its
  * elementwise steps.  Measured on a 34.5 ms synthetic VGG19-22K backward
  * pass with a 1.2 ms iteration (medians of 16 interleaved passes; the median
- * of five such runs on five machines), against the backward pass followed
+ * of six such runs on six machines), against the backward pass followed
  * by the iteration: SFB_LAST 0.06 ms later (the applies beside the backward
  * pass's last layers make up for the events the backward pass records),
- * ALL_LAST 0.14 ms, EACH 0.41 ms; single runs move by +-0.15 ms.  What
+ * ALL_LAST 0.12 ms, EACH 0.40 ms; single runs move by +-0.15 ms.  What
  * Alg. 2 hides is time the GPU would otherwise spend waiting for the
  * network; EACH is for callers that have such time.  Results are the same under every schedule (bit-identical kernels).
  * Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG (NULL pool, unknown policy).

@@ -72,9 +72,13 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_kernel(float* __restrict_
 // LEAN_CHUNK at a time.  It therefore runs on the CUs the rebuild keeps busy,
 // streaming memory while the matrix cores work, instead of waiting for a
 // rebuild workgroup's slot to free up (VGG19-22K iteration 1.702-1.710 ->
-// 1.659-1.675 ms).  One workgroup per CU walks the tensor grid-stride.  The
-// arithmetic and its order are apply_group's: the same results, bitwise.
-// Aligned tensors whose P*n*4 bytes fit 31-bit buffer offsets.
+// 1.659-1.675 ms).  Its workgroups walk the tensor grid-stride: one per CU
+// beside the fp32 rebuild, one per two CUs beside the split-bf16 one, whose
+// matrix-core work the applies then slow less (VGG19-22K iteration
+// 1.231-1.237 ms against 1.237-1.245 with one per CU and 1.242-1.250 with
+// two; 3/8 and 5/8 of the CUs measured as one half).  The arithmetic and its
+// order are apply_group's: the same results, bitwise.  Aligned tensors whose
+// P*n*4 bytes fit 31-bit buffer offsets.
 // ---------------------------------------------------------------------------
 constexpr int LEAN_CHUNK = 4;
 constexpr int BUF_DWORD = 0x00020000;   // buffer resource word 3: raw dword accesses
@@ -138,7 +142,8 @@ hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, f
     if (beside_sf && al && static_cast<int64_t>(P) * n * 4 <= 0x7fffffffLL) {
         const int64_t want = (n / 4 + PS_THREADS - 1) / PS_THREADS;
         const int64_t cus = device_cu_count();
-        ps_apply_lean_kernel<PT, MOM><<<static_cast<int>(want < cus ? want : cus), PS_THREADS, 0, stream>>>(
+        const int64_t grid = sf_arithmetic() == POSEIDON_SF_FP32 ? cus : (cus + 1) / 2;
+        ps_apply_lean_kernel<PT, MOM><<<static_cast<int>(want < grid ? want : grid), PS_THREADS, 0, stream>>>(
             W, G, P, static_cast<int>(n), lr, mu, buf);
         return hipGetLastError();
     }

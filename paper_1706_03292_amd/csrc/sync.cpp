@@ -172,12 +172,13 @@ constexpr double SF_SPREAD_OF_PS = 0.9;
 // applies use it, so that they stream memory on the CUs the rebuilds keep
 // busy -- provided the applies still end before the rebuilds: at the lean
 // kernel's rate beside them they must take at most this fraction of the
-// rebuilds' estimated time.  That rate, one lean workgroup per CU, is set by
-// the waves that fit beside the rebuild's: two per SIMD beside the split-
-// bf16 256 x 128 tiles (two waves of 228 VGPRs; VGG19-22K's largest PS
-// tensors, 189 MB, in 0.06-0.07 ms), one beside the fp32 128 x 128 tiles
-// (four of 120; 0.141 ms).
-constexpr double LEAN_PS_BYTES_PER_S_SPLIT = 2.5e12;
+// rebuilds' estimated time.  That rate is set by the lean kernel's grid
+// (one workgroup on every second CU beside the split-bf16 rebuild: its
+// 256 x 128 tiles' two waves of 228 VGPRs per SIMD; VGG19-22K's largest PS
+// tensors, 189 MB, in 0.10 ms) and by the waves that fit beside the rebuild's
+// (one workgroup per CU, one wave per SIMD beside the fp32 128 x 128 tiles'
+// four of 120; 0.141 ms).
+constexpr double LEAN_PS_BYTES_PER_S_SPLIT = 1.9e12;
 constexpr double LEAN_PS_BYTES_PER_S_FP32 = 1.3e12;
 constexpr double LEAN_OF_SF = 0.85;
 
