@@ -157,6 +157,10 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
         bw.run(cs)
         it(cs)
 
+    def serial_events():
+        bw.run(cs, events)
+        it(cs)
+
     def wfbp():
         bw.run(cs, events)
         it(cs, ready=ready)
@@ -166,21 +170,25 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
             pool.set_wfbp_policy(policy)
             bw.run(cs, events)
             it(cs, ready=ready)
-            pool.set_wfbp_policy(api.WFBP_SFB_LAST)
+            pool.set_wfbp_policy(api.WFBP_SERIAL)
         return run
 
     # Alg. 2's own schedule (every update, the SFB rebuilds included, on its
-    # own layer's event), and every update held until the last event
+    # own layer's event), the PS applies alone on their events, and every
+    # update held until the last event on the pool's streams
     wfbp_each = with_policy(api.WFBP_EACH)
+    wfbp_sfb_last = with_policy(api.WFBP_SFB_LAST)
     wfbp_all_last = with_policy(api.WFBP_ALL_LAST)
 
-    t_bw, t_bw_ev, t_sync, t_serial, t_wfbp, t_each, t_all_last = timed_interleaved(
-        [lambda: bw.run(cs), lambda: bw.run(cs, events), lambda: it(cs), serial, wfbp, wfbp_each, wfbp_all_last])
+    t_bw, t_bw_ev, t_sync, t_serial, t_serial_ev, t_wfbp, t_each, t_sfb_last, t_all_last = timed_interleaved(
+        [lambda: bw.run(cs), lambda: bw.run(cs, events), lambda: it(cs), serial, serial_events, wfbp, wfbp_each,
+         wfbp_sfb_last, wfbp_all_last])
     hidden = t_serial - t_wfbp
     # One more of each with the library's launch timing: the updates' own
     # durations show whether they ran beside the backward pass.
     launch = {}
-    for name, fn in (("serial", serial), ("wfbp", wfbp), ("wfbp_each", wfbp_each), ("wfbp_all_last", wfbp_all_last)):
+    for name, fn in (("serial", serial), ("wfbp", wfbp), ("wfbp_each", wfbp_each), ("wfbp_sfb_last", wfbp_sfb_last),
+                     ("wfbp_all_last", wfbp_all_last)):
         pool.set_timing(True)
         fn()
         recs = pool.launch_times()
@@ -196,19 +204,25 @@ def _wfbp_phase(wl, devt, it, pool, d, steps):
         "backward_ms": round(t_bw, 3), "backward_with_events_ms": round(t_bw_ev, 3), "sync_ms": round(t_sync, 3),
         "events_note": "backward_with_events: the same backward pass recording one event per layer (what every "
                        "wait-free schedule needs); hidden_* compare with the backward pass without events "
-                       "followed by the iteration",
-        "serial_ms": round(t_serial, 3), "wfbp_ms": round(t_wfbp, 3),
+                       "followed by the iteration; serial_with_events: the backward pass recording its events, "
+                       "then the plain iteration; schedule_cost: the default schedule against that, i.e. what the "
+                       "schedule adds beyond the caller's events",
+        "serial_ms": round(t_serial, 3), "serial_with_events_ms": round(t_serial_ev, 3), "wfbp_ms": round(t_wfbp, 3),
+        "schedule_cost_ms": round(t_wfbp - t_serial_ev, 3),
         "hidden_sync_ms": round(hidden, 3), "hidden_frac": round(hidden / t_sync, 3),
         "stall_ms": round(max(0.0, t_wfbp - t_bw), 3), "busy_frac": round(t_bw / t_wfbp, 3),
         "wfbp_each_ms": round(t_each, 3), "hidden_each_ms": round(t_serial - t_each, 3),
+        "wfbp_sfb_last_ms": round(t_sfb_last, 3), "hidden_sfb_last_ms": round(t_serial - t_sfb_last, 3),
         "wfbp_all_last_ms": round(t_all_last, 3), "hidden_all_last_ms": round(t_serial - t_all_last, 3),
-        "schedule_note": "wfbp: the library's default schedule on one GPU (POSEIDON_WFBP_SFB_LAST: the PS applies "
-                         "on their own layers' events, the SFB rebuilds after every event as one grouped launch); "
-                         "wfbp_each: every update on its own layer's event (Alg. 2); wfbp_all_last: every update "
-                         "waits for every layer's event, then the plain iteration's launches",
+        "schedule_note": "wfbp: the library's default schedule on one GPU (POSEIDON_WFBP_SERIAL: the caller's stream "
+                         "waits for every layer's event, then the plain iteration on it, the serial order); "
+                         "wfbp_each: every update on its own layer's event (Alg. 2); wfbp_sfb_last: the PS applies "
+                         "on their own layers' events, the SFB rebuilds after every event as one grouped launch; "
+                         "wfbp_all_last: every update waits for every layer's event, then the plain iteration's "
+                         "launches on the pool's streams",
         "update_launch_ms": launch,
         "steps": steps,
-        "timing_note": "each figure the median of `steps` passes, the seven variants run in turn in every round",
+        "timing_note": "each figure the median of `steps` passes, the nine variants run in turn in every round",
     }
 
 

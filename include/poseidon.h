@@ -60,9 +60,11 @@ extern "C" {
 #define POSEIDON_KIND_OTHER  1
 
 /* Schedules of poseidon_sync_iteration_wfbp (poseidon_pool_set_wfbp_policy). */
-#define POSEIDON_WFBP_ALL_LAST 0   /* every update after every ready event (the serial order) */
-#define POSEIDON_WFBP_SFB_LAST 1   /* PS applies on their own events, SFB rebuilds after every event (default) */
+#define POSEIDON_WFBP_ALL_LAST 0   /* every update after every ready event, on the pool's streams */
+#define POSEIDON_WFBP_SFB_LAST 1   /* PS applies on their own events, SFB rebuilds after every event */
 #define POSEIDON_WFBP_EACH     2   /* every update on its own ready event (Alg. 2) */
+#define POSEIDON_WFBP_SERIAL   3   /* the caller's stream waits for every ready event, then the plain
+                                      iteration on it: the serial order (default) */
 
 /* Arithmetic of the SF reconstruction's contraction (poseidon_sf_set_arithmetic). */
 #define POSEIDON_SF_BF16X6 0   /* split-bf16 products, fp32 accumulation (default) */
@@ -507,16 +509,22 @@ int poseidon_sync_iteration(poseidon_stream_pool* pool,
  * reads W_t or writes t's payload (U/V rows or shards) in this iteration;
  * tensors of one layer may share an event.  Issue order, schemes, payload
  * rules and results are those of poseidon_sync_iteration (bitwise: the same
- * kernels), except that every update runs on the pool's streams (the SFB
- * updates on its first, the PS updates on its second, or all on the first in
- * a one-stream iteration), none on `stream`, that only PS tensors of fewer than 2^17 values
- * share the batched pass, so that each other PS update starts after its own
- * event, and that the pool's schedule (poseidon_pool_set_wfbp_policy) can
- * hold updates back: by default (POSEIDON_WFBP_SFB_LAST) the SFB tensors wait
- * for every ready event and share one grouped launch; under
- * POSEIDON_WFBP_ALL_LAST every update waits for every ready event and the
- * launches are poseidon_sync_iteration's; under POSEIDON_WFBP_EACH every SFB
- * tensor keeps a launch of its own that starts after its own event.  `stream` waits for every update at the end.
+ * kernels).  The pool's schedule (poseidon_pool_set_wfbp_policy) decides
+ * what the updates wait for.  By default (POSEIDON_WFBP_SERIAL) `stream`
+ * waits for every ready event and the call then is poseidon_sync_iteration
+ * on `stream`: the updates also wait for whatever was enqueued on `stream`
+ * before the call (the serial order; on one GPU the cheapest, see
+ * poseidon_pool_set_wfbp_policy).  Under the other schedules every update
+ * runs on the pool's streams (the SFB updates on its first, the PS updates on
+ * its second, or all on the first in a one-stream iteration), none on
+ * `stream`, so that later work on `stream` can run beside them; only PS
+ * tensors of fewer than 2^17 values share the batched pass, so that each
+ * other PS update starts after its own event; under POSEIDON_WFBP_SFB_LAST
+ * the SFB tensors wait for every ready event and share one grouped launch;
+ * under POSEIDON_WFBP_ALL_LAST every update waits for every ready event and
+ * the launches are poseidon_sync_iteration's; under POSEIDON_WFBP_EACH every
+ * SFB tensor keeps a launch of its own that starts after its own event.
+ * `stream` waits for every update at the end.
  * ready: count non-NULL events, caller-owned, not retained after the call.
  * Returns POSEIDON_OK, POSEIDON_ERR_INVALID_ARG (also for NULL ready or a NULL
  * entry), POSEIDON_ERR_PAYLOAD or POSEIDON_ERR_HIP.
@@ -538,22 +546,25 @@ int poseidon_pool_set_timing(poseidon_stream_pool* pool, int32_t enable);
 /*
  * The schedule poseidon_sync_iteration_wfbp uses on this pool.
  * POSEIDON_WFBP_EACH is Alg. 2's: every tensor's update starts on its own
- * ready event.  POSEIDON_WFBP_SFB_LAST (the default) starts the PS applies on
- * their own events but holds the SFB rebuilds until every tensor's event has
- * completed and runs them as one grouped launch.  POSEIDON_WFBP_ALL_LAST
- * holds every update until every tensor's event has completed and then
- * issues poseidon_sync_iteration's launches (on the pool's streams): the
- * serial order.  On one GPU the updates are local computation that competes
- * with the caller's backward pass: the rebuilds for the matrix cores its
- * GEMMs use, the applies for the memory bandwidth and CU slots of its
- * elementwise steps.  Measured on a 34.5 ms synthetic VGG19-22K backward
- * pass with a 1.2 ms iteration (medians of 16 interleaved passes; the median
- * of six such runs on six machines), against the backward pass followed
- * by the iteration: SFB_LAST 0.06 ms later (the applies beside the backward
- * pass's last layers make up for the events the backward pass records),
- * ALL_LAST 0.12 ms, EACH 0.40 ms; single runs move by +-0.15 ms.  What
- * Alg. 2 hides is time the GPU would otherwise spend waiting for the
- * network; EACH is for callers that have such time.  Results are the same under every schedule (bit-identical kernels).
+ * ready event.  POSEIDON_WFBP_SFB_LAST starts the PS applies on their own
+ * events but holds the SFB rebuilds until every tensor's event has completed
+ * and runs them as one grouped launch.  POSEIDON_WFBP_ALL_LAST holds every
+ * update until every tensor's event has completed and then issues
+ * poseidon_sync_iteration's launches on the pool's streams.
+ * POSEIDON_WFBP_SERIAL (the default) makes the caller's stream wait for every
+ * event and runs poseidon_sync_iteration on it.  On one GPU the updates are
+ * local computation that competes with the caller's backward pass -- the
+ * rebuilds for the matrix cores its GEMMs use, the applies for the memory
+ * bandwidth and CU slots of its elementwise steps -- so nothing is hidden,
+ * and the serial order on the caller's stream is the cheapest: the first
+ * update starts 10-12 us after the backward pass's last kernel (7 us without
+ * events), against 72-84 us for the other held schedules, whose updates wait
+ * on another queue.  What the events themselves cost the backward pass that
+ * records them (19 per-layer events in a 34.5 ms synthetic VGG19-22K
+ * backward pass: 0.06-0.11 ms) is the caller's.  What Alg. 2 hides is time
+ * the GPU would otherwise spend waiting for the network; EACH is for callers
+ * that have such time.  Results are the same under every schedule
+ * (bit-identical kernels).
  * Returns POSEIDON_OK or POSEIDON_ERR_INVALID_ARG (NULL pool, unknown policy).
  */
 int poseidon_pool_set_wfbp_policy(poseidon_stream_pool* pool, int32_t policy);

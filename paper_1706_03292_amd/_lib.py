@@ -23,6 +23,7 @@ KIND_OTHER = 1
 WFBP_ALL_LAST = 0
 WFBP_SFB_LAST = 1
 WFBP_EACH = 2
+WFBP_SERIAL = 3
 SF_BF16X6 = 0
 SF_FP32 = 1
 

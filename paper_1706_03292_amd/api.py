@@ -14,7 +14,7 @@ import torch
 
 from . import _lib as L
 from ._lib import (ADAM, ERR_HIP, ERR_INVALID_ARG, ERR_PAYLOAD, KIND_FC, KIND_OTHER, PS, SFB,  # noqa: F401
-                   SF_BF16X6, SF_FP32, WFBP_ALL_LAST, WFBP_EACH, WFBP_SFB_LAST)
+                   SF_BF16X6, SF_FP32, WFBP_ALL_LAST, WFBP_EACH, WFBP_SERIAL, WFBP_SFB_LAST)
 
 
 class PoseidonError(RuntimeError):
@@ -268,7 +268,7 @@ class StreamPool:
         return self._h
 
     def set_wfbp_policy(self, policy: int) -> None:
-        """WFBP_SFB_LAST (default), WFBP_ALL_LAST or WFBP_EACH (poseidon_pool_set_wfbp_policy)."""
+        """WFBP_SERIAL (default), WFBP_SFB_LAST, WFBP_ALL_LAST or WFBP_EACH (poseidon_pool_set_wfbp_policy)."""
         _check("poseidon_pool_set_wfbp_policy", L.lib().poseidon_pool_set_wfbp_policy(self.handle, int(policy)))
 
     def set_timing(self, enable: bool) -> None:

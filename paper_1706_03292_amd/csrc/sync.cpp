@@ -19,7 +19,7 @@ struct poseidon_stream_pool {
     std::vector<hipEvent_t> joined;   // one per stream: its last update of the iteration
     hipEvent_t fork = nullptr;        // work enqueued on the caller's stream before the iteration
     bool timing = false;
-    int32_t wfbp_policy = POSEIDON_WFBP_SFB_LAST;
+    int32_t wfbp_policy = POSEIDON_WFBP_SERIAL;
     std::vector<hipEvent_t> t_start;  // per launch of the last timed iteration
     std::vector<hipEvent_t> t_stop;
     std::vector<poseidon_launch_record> t_rec;
@@ -187,7 +187,7 @@ constexpr double LEAN_OF_SF = 0.85;
 // poseidon_sync_iteration_wfbp (tensor t's update waits for ready[t], or for
 // every ready event, as the pool's schedule says).
 int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_t count, int64_t B, int32_t P,
-              float lr, float momentum, const hipEvent_t* ready, hipStream_t stream, int32_t* schemes)
+              float lr, float momentum, const hipEvent_t* events, hipStream_t stream, int32_t* schemes)
 {
     using namespace poseidon;
     if (!pool || count < 0 || (count > 0 && !tensors) || B < 0 || P < 1)
@@ -198,6 +198,12 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     if (dev != pool->device)
         return POSEIDON_ERR_INVALID_ARG;
     const int64_t K = B * static_cast<int64_t>(P);
+    // Under POSEIDON_WFBP_SERIAL the caller's stream waits for every ready
+    // event (below, once everything has been validated) and the iteration is
+    // then poseidon_sync_iteration's on that stream: `ready` is what the
+    // scheduling sees, `events` what the arguments hold.
+    const bool serial = events && pool->wfbp_policy == POSEIDON_WFBP_SERIAL;
+    const hipEvent_t* const ready = serial ? nullptr : events;
 
     // Validate everything and fix every scheme before enqueueing anything.
     std::vector<int32_t> plan(static_cast<size_t>(count));
@@ -231,7 +237,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         }
         if (rc != POSEIDON_OK)
             return rc;
-        if (ready && !ready[t])
+        if (events && !events[t])
             return POSEIDON_ERR_INVALID_ARG;
         plan[static_cast<size_t>(t)] = scheme;
     }
@@ -298,7 +304,7 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
     // last tiles (and a layer that is exactly one round of tiles, whose W
     // epilogues would otherwise all run at once) overlap the next layer's
     // (VGG19-22K iteration: 1.75 vs 1.78 ms, A/B in alternating processes).
-    // With ready events that holds under the default schedule, where the SFB
+    // With ready events that holds under the held schedules, where the SFB
     // rebuilds wait for the end of the caller's backward pass (on one GPU they
     // need the matrix cores its GEMMs use); under POSEIDON_WFBP_EACH every
     // SFB layer keeps its own launch, so that each starts as soon as its own
@@ -364,6 +370,21 @@ int sync_impl(poseidon_stream_pool* pool, const poseidon_tensor* tensors, int32_
         forked = 1 - crit;
         st[crit] = stream;
         st[forked] = pool->streams[0];
+    }
+    if (serial) {
+        // The caller's stream itself waits: for events recorded on it these
+        // waits are met in order, without a wake-up from another queue (the
+        // waits gathered on a pool stream, and the caller's stream waiting for
+        // that stream once, started the first update 81-84 us after the
+        // backward pass's last kernel instead of 6-9).
+        std::vector<hipEvent_t> seen;
+        for (int32_t t = 0; t < count; ++t) {
+            if (std::find(seen.begin(), seen.end(), events[t]) != seen.end())
+                continue;
+            seen.push_back(events[t]);
+            if (hipStreamWaitEvent(stream, events[t], 0) != hipSuccess)
+                return POSEIDON_ERR_HIP;
+        }
     }
     if (split) {
         if (hipEventRecord(pool->fork, stream) != hipSuccess ||
@@ -533,7 +554,8 @@ extern "C" int poseidon_sync_iteration_wfbp(poseidon_stream_pool* pool,
 
 extern "C" int poseidon_pool_set_wfbp_policy(poseidon_stream_pool* pool, int32_t policy)
 {
-    if (!pool || (policy != POSEIDON_WFBP_EACH && policy != POSEIDON_WFBP_SFB_LAST && policy != POSEIDON_WFBP_ALL_LAST))
+    if (!pool || (policy != POSEIDON_WFBP_EACH && policy != POSEIDON_WFBP_SFB_LAST && policy != POSEIDON_WFBP_ALL_LAST &&
+                  policy != POSEIDON_WFBP_SERIAL))
         return POSEIDON_ERR_INVALID_ARG;
     pool->wfbp_policy = policy;
     return POSEIDON_OK;

@@ -165,8 +165,8 @@ int main(void)
         float *dW1 = dev_copy(W1, M * N), *dU = dev_copy(U, K * M), *dV = dev_copy(V, K * N);
         float *dW2 = dev_copy(W2, n), *dG = dev_copy(G, P * n), *dB2 = dev_copy(B2, n);
         /* the same start for the wait-free iterations below, one copy per schedule */
-        float *eW1[2], *eW2[2], *eB2[2];
-        for (int c = 0; c < 2; ++c)
+        float *eW1[3], *eW2[3], *eB2[3];
+        for (int c = 0; c < 3; ++c)
             eW1[c] = dev_copy(W1, M * N), eW2[c] = dev_copy(W2, n), eB2[c] = dev_copy(B2, n);
         poseidon_stream_pool *pool = NULL;
         int rc = poseidon_pool_create(2, &pool);
@@ -182,18 +182,19 @@ int main(void)
         HIP_OK(hipDeviceSynchronize());
         to_host(g1, dW1, M * N);
         to_host(g2, dW2, n);
-        /* The wait-free iteration under Alg. 2's schedule and under
-         * POSEIDON_WFBP_ALL_LAST (every update after every event): the same
-         * results. */
+        /* The wait-free iteration under Alg. 2's schedule, under
+         * POSEIDON_WFBP_ALL_LAST (every update after every event) and under
+         * POSEIDON_WFBP_SERIAL (the caller's stream waits, then the plain
+         * iteration): the same results. */
         {
             hipEvent_t ev;
             HIP_OK(hipEventCreate(&ev));
             HIP_OK(hipEventRecord(ev, 0));
             const hipEvent_t ready[2] = {ev, ev};
-            const int32_t pol[2] = {POSEIDON_WFBP_EACH, POSEIDON_WFBP_ALL_LAST};
+            const int32_t pol[3] = {POSEIDON_WFBP_EACH, POSEIDON_WFBP_ALL_LAST, POSEIDON_WFBP_SERIAL};
             int same = 1, wrc = POSEIDON_OK;
             float *h1 = malloc(M * N * 4), *h2 = malloc(n * 4);
-            for (int c = 0; c < 2 && wrc == POSEIDON_OK; ++c) {
+            for (int c = 0; c < 3 && wrc == POSEIDON_OK; ++c) {
                 poseidon_tensor u[2];
                 memcpy(u, t, sizeof u);
                 u[0].W = eW1[c], u[1].W = eW2[c], u[1].buf = eB2[c];
@@ -206,12 +207,12 @@ int main(void)
                 same &= memcmp(h1, g1, M * N * 4) == 0 && memcmp(h2, g2, n * 4) == 0;
             }
             const int bad_policy = poseidon_pool_set_wfbp_policy(pool, 17) == POSEIDON_ERR_INVALID_ARG;
-            printf("%-44s rc %d %s\n", "poseidon_sync_iteration_wfbp (2 schedules)", wrc,
+            printf("%-44s rc %d %s\n", "poseidon_sync_iteration_wfbp (3 schedules)", wrc,
                    wrc == POSEIDON_OK && same && bad_policy ? "ok" : "FAIL");
             failures += !(wrc == POSEIDON_OK && same && bad_policy);
             free(h1), free(h2);
             HIP_OK(hipEventDestroy(ev));
-            for (int c = 0; c < 2; ++c) {
+            for (int c = 0; c < 3; ++c) {
                 HIP_OK(hipFree(eW1[c]));
                 HIP_OK(hipFree(eW2[c]));
                 HIP_OK(hipFree(eB2[c]));

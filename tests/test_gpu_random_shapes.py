@@ -106,7 +106,7 @@ def test_sync_iteration_random_networks(seed):
                          "buf": I.randn(base + 4, (n,), 1e-3) if rng.random() < 0.7 else None})
     streams = int(rng.choice([1, 2, 4]))
     wfbp = bool(rng.random() < 0.5)
-    policy = int(rng.choice([api.WFBP_ALL_LAST, api.WFBP_SFB_LAST, api.WFBP_EACH]))
+    policy = int(rng.choice([api.WFBP_ALL_LAST, api.WFBP_SFB_LAST, api.WFBP_EACH, api.WFBP_SERIAL]))
     devt = [{k: (v.to(d) if isinstance(v, torch.Tensor) else v) for k, v in h.items() if v is not None}
             for h in host]
     log(f"sync random seed={seed} P={P} B={B} layers={len(host)} streams={streams} wfbp={wfbp} policy={policy}")
