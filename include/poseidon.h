@@ -472,10 +472,11 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * its tiles, sized to take about 90% of the applies' estimated time, so that
  * the rebuilds run thin beside the applies.  Conversely, when the SFB
  * rebuilds are the longer kind (and the applies would still end first at
- * 1.3 TB/s), the rebuilds leave each SIMD the registers of one more wave and
- * the PS applies of aligned tensors use a low-register kernel that runs in
- * them, on the CUs the rebuilds keep busy.  Every variant computes the same
- * results, bitwise.
+ * the rate they get beside them: 1.9 TB/s beside the split-bf16 rebuild,
+ * 1.3 beside the fp32 one), the rebuilds leave each SIMD the registers of
+ * more waves and the PS applies of aligned tensors use a low-register kernel
+ * that runs in them, on the CUs the rebuilds keep busy.  Every variant
+ * computes the same results, bitwise.
  * SFB tensors take poseidon_sf_apply(W, U, V, M, N, P*B, lr), or
  * poseidon_sf_apply_momentum(W, buf, U, V, M, N, P*B, lr, momentum) when
  * buf != NULL; PS tensors take poseidon_ps_apply(W, shards, P, M*N, lr,
@@ -491,6 +492,11 @@ int poseidon_pool_destroy(poseidon_stream_pool* pool);
  * V, or shards); tensors may share a payload.  Returns POSEIDON_OK,
  * POSEIDON_ERR_INVALID_ARG (also for such an overlap), POSEIDON_ERR_PAYLOAD
  * (the chosen scheme's payload is NULL) or POSEIDON_ERR_HIP.
+ * The call may be captured into a HIP graph (stream capture on `stream`, with
+ * launch timing off): it enqueues only kernel launches and event records and
+ * waits that fork from `stream` and join back to it.  A replay repeats the
+ * launches chosen at capture (for the shapes, the pool and the arithmetic
+ * setting of that time) on the same arrays.
  */
 int poseidon_sync_iteration(poseidon_stream_pool* pool,
                             const poseidon_tensor* tensors, int32_t count,
