@@ -6,23 +6,27 @@
 //
 // The kernels are bound by HBM bandwidth: per element they read P shard
 // values plus W and buf and write W and buf (4P + 16 bytes), against ~P + 3
-// flops.  Each thread owns one group of four consecutive elements and issues
-// all of its shard loads before the dependent adds (bytes in flight); the
-// thread whose group runs past the end of the tensor finishes the last one to
-// three elements one by one.  Every access is 16 bytes wide: aligned when all
+// flops.  Each thread owns a group of four consecutive elements -- two such
+// groups, 256 elements apart, in the single-tensor launch (apply_pair: a
+// wave's accesses to each array read 2 KB in a row) -- and issues its shard
+// loads before the dependent adds (bytes in flight); the thread whose group
+// runs past the end of the tensor finishes the last one to three elements
+// one by one.  Every access is 16 bytes wide: aligned when all
 // arrays are 16-byte aligned and the size is a multiple of four (so every
 // shard row starts at a 16-byte boundary), otherwise at 4-byte alignment,
 // which global loads and stores accept (a tensor of 2,786,166 values over 32
 // shards: 5.0 TB/s this way against 3.9 TB/s with 4-byte accesses).  Every
 // array is touched once per launch (shards read; W and buf read, then
 // written), so all accesses are non-temporal (1-2% faster than cached W/buf
-// accesses on 2.4M-16.8M elements).  One group per thread and as many
-// workgroups as needed (one pass): a launch-shape sweep over 37K-16.8M
-// elements (block size 64-1024, one or two groups per thread, grid-stride
-// loops capped at 4-16 workgroups per CU) found this within 3% of the best
+// accesses on 2.4M-16.8M elements).  As many workgroups as needed (one
+// pass): a launch-shape sweep over 37K-16.8M elements (block size 64-1024,
+// one or two adjacent groups per thread, grid-stride loops capped at 4-16
+// workgroups per CU) found one group per thread within 3% of the best
 // everywhere and 10% faster than a capped grid-stride loop on large tensors,
 // whose last partial pass leaves the chip half idle; of the block sizes,
-// 256 threads (PS_THREADS) is the best beside the SF rebuild.
+// 256 threads (PS_THREADS) is the best beside the SF rebuild.  Two groups
+// 256 elements apart (rather than adjacent) then measured faster for single
+// tensors at P = 8 and P = 32 and the same at P = 16 (ps_group.h).
 //
 // Three launch forms share the per-group update: one tensor with P
 // contiguous shards, many such tensors in one launch, and the KV store's
@@ -41,7 +45,20 @@ namespace {
 // workgroup's slot gives that slot back whole (the Inception-shaped
 // iteration 0.657 vs 0.681 ms; VGG19-22K 1.739 vs 1.745 ms).
 constexpr int PS_THREADS = 256;
-constexpr int PS_BLOCK_ELEMS = 4 * PS_THREADS;  // elements per workgroup: one group of four per thread
+// Elements per work block of a single-tensor workgroup: two groups of four per
+// thread (apply_pair), each wave covering 512 consecutive elements.  The
+// batched pass keeps one group per thread (PS_BATCH_BLOCK_ELEMS): with two,
+// its many mid-sized tensors ran slower (the Inception-shaped step's batched
+// pass 0.445-0.447 against 0.428-0.429 ms in the iteration), its grid half as
+// many workgroups with a longer last round.
+constexpr int PS_BLOCK_ELEMS = 8 * PS_THREADS;
+constexpr int PS_BATCH_BLOCK_ELEMS = 4 * PS_THREADS;
+
+// Offset of thread `tid`'s first element inside a work block.
+__device__ inline int64_t pair_offset(int tid)
+{
+    return (tid >> 6) * (2 * PS_PAIR_GAP) + 4 * (tid & 63);
+}
 // The KV store's launches are small (one server's share of a tensor, a few
 // hundred thousand elements): one-wave workgroups fill the chip better there
 // (server 0's VGG19-22K applies at 5.5 vs 4.8 TB/s).
@@ -58,10 +75,9 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_kernel(float* __restrict_
                                                               float* __restrict__ buf)
 {
     const Contiguous src{G, n};
-    const int64_t groups = (n + 3) / 4;
-    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_THREADS;
-    for (int64_t i = static_cast<int64_t>(blockIdx.x) * PS_THREADS + threadIdx.x; i < groups; i += stride)
-        apply_group<PT, MOM, AL>(W, buf, src, P, 4 * i, n, lr, mu);
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * PS_BLOCK_ELEMS;
+    for (int64_t e = static_cast<int64_t>(blockIdx.x) * PS_BLOCK_ELEMS + pair_offset(threadIdx.x); e < n; e += stride)
+        apply_pair<PT, MOM, AL>(W, buf, src, P, e, n, lr, mu);
 }
 
 // ---------------------------------------------------------------------------
@@ -147,8 +163,8 @@ hipError_t launch_pt(float* W, const float* G, int32_t P, int64_t n, float lr, f
             W, G, P, static_cast<int>(n), lr, mu, buf);
         return hipGetLastError();
     }
-    // One group per thread; the grid-stride loop only matters beyond 2^30 workgroups.
-    const int64_t want = ((n + 3) / 4 + PS_THREADS - 1) / PS_THREADS;
+    // One work block per workgroup; the grid-stride loop only matters beyond 2^30 workgroups.
+    const int64_t want = (n + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
     const int grid = static_cast<int>(want < PS_MAX_GRID ? want : PS_MAX_GRID);
     if (al)
         ps_apply_kernel<PT, MOM, true><<<grid, PS_THREADS, 0, stream>>>(W, G, P, n, lr, mu, buf);
@@ -175,7 +191,8 @@ hipError_t launch_mom(float* W, const float* G, int32_t P, int64_t n, float lr, 
 // ---------------------------------------------------------------------------
 // Many tensors in one launch.  The descriptors travel by value in the kernel
 // arguments; tensor t owns the workgroups [first_block[t], first_block[t+1]),
-// each of which updates PS_BLOCK_ELEMS consecutive elements of it.
+// each of which updates PS_BATCH_BLOCK_ELEMS consecutive elements of it, one
+// group of four per thread.
 // ---------------------------------------------------------------------------
 struct PsBatchItem {
     float* W;
@@ -208,7 +225,7 @@ __global__ __launch_bounds__(PS_THREADS) void ps_apply_batch_kernel(const PsBatc
         for (int k = 1; k < PS_BATCH_MAX; ++k)
             t += (k < args.count && args.first_block[k] <= b) ? 1 : 0;
         const PsBatchItem& it = args.item[t];
-        const int64_t e = static_cast<int64_t>(b - it.first_block) * PS_BLOCK_ELEMS + 4 * threadIdx.x;
+        const int64_t e = static_cast<int64_t>(b - it.first_block) * PS_BATCH_BLOCK_ELEMS + 4 * threadIdx.x;
         if (e < it.n) {
             const Contiguous src{it.G, it.n};
             if (it.aligned)
@@ -383,7 +400,7 @@ hipError_t launch_ps_apply_batch(const PsTensor* t, int32_t count, int32_t P, fl
         for (int32_t i = 0; i < count; ++i) {
             if (t[i].n == 0 || (t[i].buf != nullptr) != mom)
                 continue;
-            const int64_t nb = (t[i].n + PS_BLOCK_ELEMS - 1) / PS_BLOCK_ELEMS;
+            const int64_t nb = (t[i].n + PS_BATCH_BLOCK_ELEMS - 1) / PS_BATCH_BLOCK_ELEMS;
             if (a.count == PS_BATCH_MAX || blocks + nb > INT32_MAX) {
                 const hipError_t e = flush();
                 if (e != hipSuccess)
