@@ -49,8 +49,8 @@ constexpr int PS_THREADS = 256;
 // thread (apply_pair), each wave covering 512 consecutive elements.  The
 // batched pass keeps one group per thread (PS_BATCH_BLOCK_ELEMS): with two,
 // its many mid-sized tensors ran slower (the Inception-shaped step's batched
-// pass 0.445-0.447 against 0.428-0.429 ms in the iteration), its grid half as
-// many workgroups with a longer last round.
+// pass 0.445-0.447 against 0.428-0.430 ms in the iteration, and 0.449-0.453
+// with 128- or 64-thread workgroups, which keep the workgroup count).
 constexpr int PS_BLOCK_ELEMS = 8 * PS_THREADS;
 constexpr int PS_BATCH_BLOCK_ELEMS = 4 * PS_THREADS;
 
