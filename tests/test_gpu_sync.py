@@ -173,8 +173,8 @@ def test_sync_iteration_launch_records():
 def test_sync_iteration_groups_the_fc_layers_unless_wfbp_each():
     """Several SFB layers without a buffer share one grouped launch (record
     tensor -1) in the plain iteration and under the held wait-free schedules,
-    POSEIDON_WFBP_ALL_LAST and POSEIDON_WFBP_SFB_LAST (the default; the
-    rebuilds wait for every event);
+    POSEIDON_WFBP_ALL_LAST and POSEIDON_WFBP_SFB_LAST (the rebuilds wait for
+    every event);
     under POSEIDON_WFBP_EACH each keeps its own launch, in backprop order;
     the results are bit-identical."""
     d = dev()

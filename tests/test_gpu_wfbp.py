@@ -267,9 +267,10 @@ def test_wfbp_launch_records_and_errors(policy):
 
 @pytest.mark.parametrize("policy", ["ALL_LAST", "SFB_LAST", "SERIAL"])
 def test_wfbp_held_schedules_start_the_rebuilds_after_every_event(policy):
-    """Under POSEIDON_WFBP_ALL_LAST and POSEIDON_WFBP_SFB_LAST (the default)
-    an SFB rebuild waits for every tensor's ready event, not only its own: the FC layer's
-    event is recorded first, then the stream is kept busy and the layer's own
+    """Under POSEIDON_WFBP_ALL_LAST, POSEIDON_WFBP_SFB_LAST and
+    POSEIDON_WFBP_SERIAL (the default) an SFB rebuild waits for every
+    tensor's ready event, not only its own: the FC layer's event is recorded
+    first, then the stream is kept busy and the layer's own
     factor rows are scaled by 64 (exact in fp32) before the last tensor's
     event.  The rebuild must see the scaled factors (W as the oracle on them,
     far from the oracle on the unscaled ones); the PS tensors' results are
