@@ -67,13 +67,16 @@ def _oracle_layers(host):
     return out
 
 
+@pytest.mark.parametrize("where", ["caller", "side"])
 @pytest.mark.parametrize("policy", ["ALL_LAST", "SFB_LAST", "EACH", "SERIAL"])
-def test_wfbp_update_waits_for_payload_written_by_backward(policy):
+def test_wfbp_update_waits_for_payload_written_by_backward(policy, where):
     """Each layer's 'backward' first keeps the compute stream busy, then
     scales this node's own payload (its B rows of U, or shard 0) by 64 --
     exact in fp32 -- and records the layer's event.  The updates must see the
     scaled payload: W matches the oracle on the scaled inputs and is far from
-    the oracle on the unscaled ones."""
+    the oracle on the unscaled ones.  The backward runs on the caller's
+    stream or on another one that the caller's stream never waits for (only
+    the events tie the iteration to it)."""
     d = dev()
     wl = I.workload(5)
     names = ["fc7.W", "fc7.b", "conv5_4.W", "conv5_4.b", "conv5_3.W", "conv5_3.b"]
@@ -99,8 +102,10 @@ def test_wfbp_update_waits_for_payload_written_by_backward(policy):
     busy_a = torch.randn(4096, 4096, device=d)
     busy_c = torch.empty_like(busy_a)
     events = [torch.cuda.Event() for _ in devt]
-    log(f"wfbp payload written by the backward pass ({policy})")
-    with torch.cuda.stream(cs):
+    bs = cs if where == "caller" else torch.cuda.Stream(d)
+    bs.wait_stream(cs)                     # the inputs' copies are on the caller's stream
+    log(f"wfbp payload written by the backward pass ({policy}, {where} stream)")
+    with torch.cuda.stream(bs):
         for i in reversed(range(len(devt))):
             for _ in range(4):
                 torch.mm(busy_a, busy_a, out=busy_c)
@@ -109,9 +114,10 @@ def test_wfbp_update_waits_for_payload_written_by_backward(policy):
                 t["U"][: wl.B].mul_(64)
             else:
                 t["shards"][0].mul_(64)
-            events[i].record(cs)
+            events[i].record(bs)
     it(cs, ready=events)
     cs.synchronize()
+    torch.cuda.synchronize()
     for i, t in enumerate(devt):
         name = host[i]["spec"].name
         want = ref[i]["W"].reshape(-1)
