@@ -678,6 +678,20 @@ def main():
         result["sfb_tflops"] = sf["roofline"]["achieved"]
         result["layers_sfb"] = sf["layers"]
         result["layers_sfb_momentum"] = sf["layers_momentum"]
+        # the same grouped launch with nothing beside it: the kernel's own rate,
+        # against which the in-iteration figure shows what the PS applies cost it
+        idx = [i for i, s_ in enumerate(schemes) if s_ == api.SFB and "buf" not in devt[i]]
+        if idx:
+            layers = [(devt[i]["W"].clone(), devt[i]["U"], devt[i]["V"]) for i in idx]
+            flops = sum(_sf_flops(host[i]["spec"], wl.K) for i in idx)
+            g_ms = _time(lambda: api.sf_apply_batch(layers, wl.lr, stream=stream), queued=True)
+            del layers
+            peak = result["roofline_sf"]["peak"]
+            result["roofline_sf"]["grouped_alone"] = {
+                "ms": round(g_ms, 4), "achieved": round(flops / g_ms / 1e9, 2),
+                "frac": round(flops / g_ms / 1e9 / peak, 4),
+                "what": "the same grouped launch (poseidon_sf_apply_batch) on copies of W, alone on the stream, "
+                        "queued behind a device-side wait, median"}
     if ps:
         result["roofline_ps"] = dict(ps["roofline"], step=ps["step"], batched_pass=ps["batched_pass"])
         if copy:
