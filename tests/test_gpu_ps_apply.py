@@ -300,3 +300,26 @@ def test_ps_apply_ragged_rows_single_batched_misaligned_bitwise(P, n):
     w_ref, b_ref = oracle.ps_apply_points(W.numpy(), G.numpy(), 0.01, 0.9, buf.numpy(), idx)
     assert_close(to_np(Wa)[idx], w_ref, W_TOL, "W")
     assert_close(to_np(ba)[idx], b_ref, BUF_TOL, "buf")
+
+
+@pytest.mark.parametrize("P", [1, 2, 8, 16, 32, 3])
+def test_ps_apply_pair_boundaries_bitwise_and_oracle(P):
+    """The single-tensor launch gives each thread two groups 256 elements
+    apart in 2048-element work blocks; sizes around those boundaries (the
+    second group whole, partial or absent; one or several blocks; aligned and
+    ragged rows) must give the batched launch's results (one group per
+    thread) bitwise and the oracle's."""
+    d = dev()
+    for n in (4, 256, 259, 260, 512, 516, 1024 + 256 + 2, 2048, 2048 + 256, 2048 + 258, 2048 * 3 + 256 + 3,
+              2048 * 5 + 511, 2048 * 7 + 1796):
+        W, G, buf = _draw(P, n, seed=P * 7 + n, buf_std=1e-3)
+        Wa, Ga, ba = W.to(d), G.to(d), buf.to(d)
+        Wb, bb = W.to(d), buf.to(d)
+        log(f"ps_apply pair boundaries P={P} n={n}")
+        api.ps_apply(Wa, Ga, 0.01, 0.9, ba)
+        api.ps_apply_batch([(Wb, Ga, bb)], 0.01, 0.9)
+        torch.cuda.synchronize()
+        assert torch.equal(Wa, Wb) and torch.equal(ba, bb), n
+        w_ref, b_ref = oracle.ps_apply(W.numpy(), G.numpy(), 0.01, 0.9, buf.numpy())
+        assert_close(to_np(Wa), w_ref, W_TOL, f"W P={P} n={n}")
+        assert_close(to_np(ba), b_ref, BUF_TOL, f"buf P={P} n={n}")
